@@ -1,0 +1,162 @@
+"""Pins for the oracle's Algorithm 2: lossless decoding against brute-force greedy, per-round
+acceptance against brute-force prefix matching, verify rows against full recomputation, the
+incremental drafter against the parallel block-mask drafter pass, and the method's special
+cases (d = 0 is plain greedy; l' = 0 accepts everything; no decoder layers = closed form)."""
+import numpy as np
+import pytest
+
+from oracle import model as om
+from oracle import seed as os_
+from paper_2609_36590_amd import synth
+
+# 4 layers so that every split n_dec in 0..4 exists; GQA 4q/2kv.
+SMALL = synth.Config("s4", 4, 2, 64, 4, 2, 16, 96, 61, 1e4, dtype=synth.F32)
+
+
+def _model(cfg, n_dec=None, enc_out_scale=1.0, seed=0, dtype=np.float64, std=0.2):
+    if n_dec is not None:
+        cfg = cfg.replace(n_dec_layers=n_dec)
+    w = synth.make_weights(cfg, seed=seed, std=std, enc_out_scale=enc_out_scale)
+    return om.Model(cfg, w, dtype)
+
+
+def _prompt(cfg, n, seed=1):
+    return np.random.default_rng(seed).integers(0, cfg.vocab, size=n)
+
+
+def test_verify_rows_equal_full_recompute():
+    m = _model(SMALL)
+    prompt = _prompt(SMALL, 12)
+    st = os_.prefill(m, prompt, 64)
+    drafts = np.array([prompt[-1], 5, 17, 3, 40])
+    logits = os_.verify(st, drafts)
+    for r in range(len(drafts)):
+        seq = list(prompt) + list(drafts[1:r + 1])
+        np.testing.assert_allclose(logits[r], om.full_forward(m, seq)[-1], rtol=1e-10, atol=1e-12)
+
+
+@pytest.mark.parametrize("n_dec", [1, 2, 3])
+def test_incremental_draft_equals_block_mask_pass(n_dec):
+    m = _model(SMALL, n_dec=n_dec)
+    prompt = _prompt(SMALL, 15, seed=2)
+    st = os_.prefill(m, prompt, 64)
+    # advance one round so the deep cache comes from a verification, not only the prefill
+    d, ql = os_.draft(st, 3)
+    n, b = os_.accept(d, os_.verify(st, d))
+    os_.commit(st, d, n, b)
+    ctx = list(st.tokens)
+    drafts, qlog = os_.draft(st, 5)
+    ref = os_.block_draft_logits(m, ctx, drafts[1:5])
+    np.testing.assert_allclose(qlog, ref, rtol=1e-9, atol=1e-11)
+
+
+def test_draft_without_decoder_layers_is_head_of_raw_embedding():
+    m = _model(SMALL, n_dec=0)
+    st = os_.prefill(m, _prompt(SMALL, 9), 32)
+    drafts, qlog = os_.draft(st, 3)
+    E = m.w["embed"]
+    for i in range(3):
+        e = E[drafts[i]]
+        closed = (e / np.sqrt(np.mean(e * e) + SMALL.rms_eps)) @ E.T
+        np.testing.assert_allclose(qlog[i], closed, rtol=1e-12, atol=1e-13)
+
+
+@pytest.fixture(scope="module")
+def damped():
+    """One weight set (encoder output projections damped so drafts are often right) and its
+    brute-force greedy continuation, shared by every split."""
+    cfg = SMALL
+    w = synth.make_weights(cfg, seed=3, std=0.2, enc_out_scale=0.15)
+    prompt = _prompt(cfg, 10, seed=4)
+    # 24 tokens are generated; 7 more let the last round's drafts be checked too
+    ref = os_.greedy_brute_force(om.Model(cfg, w, np.float64), prompt, 24 + 7)
+    return w, prompt, ref
+
+
+@pytest.mark.parametrize("n_dec", [0, 1, 2, 3, 4])
+@pytest.mark.parametrize("d", [0, 1, 2, 3, 4, 5, 6])
+def test_lossless_against_brute_force(damped, n_dec, d):
+    w, prompt, ref = damped
+    m = om.Model(SMALL.replace(n_dec_layers=n_dec), w, np.float64)
+    toks, rounds = os_.generate(m, prompt, d, 24, record=True)
+    np.testing.assert_array_equal(toks, ref[:24])
+    # every round's n_accept is the longest prefix of drafts that matches greedy decoding
+    full = list(prompt) + list(ref)
+    for rd in rounds:
+        cont = full[rd.p + 1:rd.p + 1 + d]
+        n = 0
+        assert len(cont) == d
+        while n < d and rd.drafts[n + 1] == cont[n]:
+            n += 1
+        assert rd.n_accept == n
+        assert rd.bonus == full[rd.p + 1 + rd.n_accept]
+
+
+def test_damped_model_exercises_partial_acceptance(damped):
+    w, prompt, ref = damped
+    m = om.Model(SMALL, w, np.float64)
+    _, rounds = os_.generate(m, prompt, 4, 24, record=True)
+    seen = {r.n_accept for r in rounds}
+    assert len(seen) >= 2 and max(seen) >= 1, seen
+
+
+def test_decoder_is_whole_model_accepts_every_draft():
+    m = _model(SMALL, n_dec=SMALL.n_layers, seed=5)
+    prompt = _prompt(SMALL, 8, seed=6)
+    toks, rounds = os_.generate(m, prompt, 4, 20, record=True)
+    assert all(r.n_accept == 4 for r in rounds)
+    np.testing.assert_array_equal(toks, os_.greedy_brute_force(m, prompt, 20))
+
+
+def test_draft_length_zero_is_plain_greedy():
+    m = _model(SMALL, seed=7)
+    prompt = _prompt(SMALL, 6, seed=8)
+    toks, rounds = os_.generate(m, prompt, 0, 12, record=True)
+    assert len(rounds) == 12 and all(r.n_accept == 0 for r in rounds)
+    np.testing.assert_array_equal(toks, os_.greedy_brute_force(m, prompt, 12))
+
+
+@pytest.mark.parametrize("j", [0, 1, 2, 3, 4])
+def test_forced_drafts_accept_exactly_the_greedy_prefix(j):
+    m = _model(SMALL, seed=9)
+    prompt = _prompt(SMALL, 7, seed=10)
+    g = os_.greedy_brute_force(m, prompt, 6)
+    st = os_.prefill(m, prompt, 32)
+    drafts = [prompt[-1]] + list(g[:j])
+    if j < 4:
+        drafts += [(g[j] + 1) % SMALL.vocab] + [0] * (3 - j)
+    n, bonus = os_.accept(np.array(drafts), os_.verify(st, np.array(drafts)))
+    assert n == j and bonus == g[j]
+
+
+def test_commit_keeps_deep_cache_for_accepted_tokens_only():
+    m = _model(SMALL, seed=11)
+    prompt = _prompt(SMALL, 9, seed=12)
+    st = os_.prefill(m, prompt, 32)
+    assert st.cache.valid.tolist() == [8] * SMALL.n_layers
+    d, _ = os_.draft(st, 3)
+    dec = m.first_decoder_layer
+    assert st.cache.valid[dec:].tolist() == [11] * (SMALL.n_layers - dec)
+    assert st.cache.valid[:dec].tolist() == [8] * dec
+    n, b = os_.accept(d, os_.verify(st, d))
+    os_.commit(st, d, n, b)
+    assert st.cache.valid.tolist() == [st.t - 1] * SMALL.n_layers
+
+
+def test_eos_stops_generation():
+    m = _model(SMALL, seed=13)
+    prompt = _prompt(SMALL, 5, seed=14)
+    ref = os_.greedy_brute_force(m, prompt, 10)
+    eos = int(ref[4])
+    first = list(ref).index(eos)
+    toks, _ = os_.generate(m, prompt, 3, 10, eos=eos)
+    np.testing.assert_array_equal(toks, ref[:first + 1])
+
+
+def test_fp32_oracle_tracks_fp64_on_tiny_config():
+    cfg = synth.C1_TINY
+    w = synth.make_weights(cfg, seed=0)
+    prompt = synth.make_prompts(cfg)[0][:16]
+    l32 = om.full_forward(om.Model(cfg, w, np.float32), prompt)
+    l64 = om.full_forward(om.Model(cfg, w, np.float64), prompt)
+    assert np.abs(l32 - l64).max() < 1e-5
