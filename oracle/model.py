@@ -15,12 +15,23 @@ readings used here are:
   q.k / sqrt(d); row r attends to every position <= its own.
 * SwiGLU MLP: down(silu(gate(x)) * up(x)); no biases anywhere.
 * tied embedding: W_out = W_in (Appendix E).
-
-Arithmetic runs in ``dtype`` (float32 by default; float64 for the pins that need it).
+* storage precision: the paper does not state the inference precision. A bf16 model stores its
+  weights and its KV cache in bfloat16, so each key/value is rounded to bf16 (round to nearest
+  even) as it is produced, before any attention reads it. All arithmetic (norms, products,
+  softmax, residual stream, logits) runs in ``dtype``: float32 by default, float64 for the pins
+  that need it.
 """
 from __future__ import annotations
 
 import numpy as np
+
+
+def round_to_bf16(x):
+    """Round to the nearest bfloat16 (ties to even) and return the value in x's dtype."""
+    f = np.asarray(x, dtype=np.float32)
+    u = f.view(np.uint32).astype(np.uint64)
+    u = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16) << 16
+    return u.astype(np.uint32).view(np.float32).astype(np.asarray(x).dtype)
 
 
 def rmsnorm(x, g, eps):
@@ -75,9 +86,10 @@ def attention(q, K, V, q_pos):
 class Model:
     """Weights of f plus the per-layer block, embedding and head."""
 
-    def __init__(self, cfg, weights, dtype=np.float32):
+    def __init__(self, cfg, weights, dtype=np.float32, kv_bf16=None):
         self.cfg = cfg
         self.dtype = np.dtype(dtype)
+        self.kv_bf16 = (getattr(cfg, "dtype", "f32") == "bf16") if kv_bf16 is None else kv_bf16
         self.w = {k: np.asarray(v, dtype=self.dtype) for k, v in weights.items()}
 
     @property
@@ -118,6 +130,8 @@ class Model:
         cos, sin = rope_cos_sin(pos, c.head_dim, c.rope_base)
         q = apply_rope(q, cos, sin)
         k = apply_rope(k, cos, sin)
+        if self.kv_bf16:
+            k, v = round_to_bf16(k), round_to_bf16(v)
         K = np.concatenate([K_prefix, k], axis=0)
         V = np.concatenate([V_prefix, v], axis=0)
         o = attention(q, K, V, pos)

@@ -129,19 +129,15 @@ def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
     return (b.astype(np.uint32) << np.uint32(16)).view(np.float32)
 
 
-def _draw_normal(seed: int, idx: int, n: int, std: float, as_bf16: bool, pool) -> np.ndarray:
-    out = np.empty(n, dtype=np.uint16 if as_bf16 else np.float32)
-
-    def fill(c):
-        s = c * _CHUNK
-        e = min(n, s + _CHUNK)
-        g = np.random.default_rng([seed, idx, c])
-        v = g.standard_normal(e - s, dtype=np.float32)
-        v *= np.float32(std)
-        out[s:e] = f32_to_bf16_bits(v) if as_bf16 else v
-
-    list(pool.map(fill, range((n + _CHUNK - 1) // _CHUNK)))
-    return out
+def _round_chunk_to_bf16(v: np.ndarray, out16: np.ndarray) -> None:
+    """RNE-round float32 ``v`` to bf16 bits into ``out16`` (same length), in place on ``v``."""
+    u = v.view(np.uint32)
+    b = u >> np.uint32(16)
+    b &= np.uint32(1)
+    b += np.uint32(0x7FFF)
+    b += u
+    b >>= np.uint32(16)
+    out16[:] = b
 
 
 def make_weights(cfg: Config, seed: int = 0, std: float = 0.02, enc_out_scale: float = 1.0):
@@ -159,27 +155,60 @@ def make_weights(cfg: Config, seed: int = 0, std: float = 0.02, enc_out_scale: f
     as_bf16 = cfg.dtype == BF16
     n_enc = cfg.n_layers - cfg.n_dec_layers
     out = {}
+    jobs = []
+    for idx, (name, shape, kind) in enumerate(tensor_specs(cfg)):
+        n = int(np.prod(shape))
+        if kind == "ones":
+            a = np.ones(n, dtype=np.float32)
+            out[name] = (f32_to_bf16_bits(a) if as_bf16 else a).reshape(shape)
+            continue
+        s = std
+        if name.startswith("layers.") and name.endswith((".wo", ".w_down")):
+            if int(name.split(".")[1]) < n_enc:
+                s = std * enc_out_scale
+        flat = np.empty(n, dtype=np.uint16 if as_bf16 else np.float32)
+        out[name] = flat.reshape(shape)
+        jobs += [(idx, c, flat, s) for c in range((n + _CHUNK - 1) // _CHUNK)]
+
+    def fill(job):
+        idx, c, flat, s = job
+        lo = c * _CHUNK
+        hi = min(len(flat), lo + _CHUNK)
+        v = np.random.default_rng([seed, idx, c]).standard_normal(hi - lo, dtype=np.float32)
+        v *= np.float32(s)
+        if as_bf16:
+            _round_chunk_to_bf16(v, flat[lo:hi])
+        else:
+            flat[lo:hi] = v
+
     with ThreadPoolExecutor(_threads()) as pool:
-        for idx, (name, shape, kind) in enumerate(tensor_specs(cfg)):
-            n = int(np.prod(shape))
-            s = std
-            if name.startswith("layers.") and name.endswith((".wo", ".w_down")):
-                if int(name.split(".")[1]) < n_enc:
-                    s = std * enc_out_scale
-            if kind == "ones":
-                a = np.ones(n, dtype=np.float32)
-                a = f32_to_bf16_bits(a) if as_bf16 else a
-            else:
-                a = _draw_normal(seed, idx, n, s, as_bf16, pool)
-            out[name] = a.reshape(shape)
+        list(pool.map(fill, jobs))
     return out
 
 
 def weights_as_f32(cfg: Config, weights: dict) -> dict:
     """float32 copies of ``weights`` (bf16 bit patterns widened exactly)."""
-    if cfg.dtype == BF16:
-        return {k: bf16_bits_to_f32(v) for k, v in weights.items()}
-    return {k: np.asarray(v, dtype=np.float32) for k, v in weights.items()}
+    if cfg.dtype != BF16:
+        return {k: np.asarray(v, dtype=np.float32) for k, v in weights.items()}
+    out = {}
+    jobs = []
+    for k, v in weights.items():
+        src = v.reshape(-1)
+        dst = np.empty(src.shape, dtype=np.uint32)
+        out[k] = dst.view(np.float32).reshape(v.shape)
+        jobs += [(src, dst, c) for c in range((len(src) + _CHUNK - 1) // _CHUNK)]
+
+    def widen(job):
+        src, dst, c = job
+        lo = c * _CHUNK
+        hi = min(len(src), lo + _CHUNK)
+        d = dst[lo:hi]
+        d[:] = src[lo:hi]
+        d <<= np.uint32(16)
+
+    with ThreadPoolExecutor(_threads()) as pool:
+        list(pool.map(widen, jobs))
+    return out
 
 
 def make_prompt_lengths(cfg: Config, seed: int = 2) -> list:

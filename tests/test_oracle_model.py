@@ -158,3 +158,25 @@ def test_kvcache_rejects_gaps_and_reads_past_valid():
         c.prefix(0, 3)
     c.truncate(1)
     assert c.valid[0] == 1
+
+
+def test_bf16_rounding_matches_torch():
+    rng = np.random.default_rng(9)
+    x = np.concatenate([rng.standard_normal(4000) * 10.0 ** rng.integers(-8, 8, 4000),
+                        [0.0, -0.0, 1.0, 1.00390625, 1.01171875, 65504.0, 3.0e38]])
+    ref = torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(om.round_to_bf16(x), ref)
+
+
+def test_bf16_model_rounds_kv_only():
+    cfg = TINY_GQA.replace(dtype=synth.BF16)
+    w = synth.weights_as_f32(cfg, synth.make_weights(cfg, seed=1, std=0.2))
+    toks = np.random.default_rng(3).integers(0, cfg.vocab, size=12)
+    exact = om.Model(cfg, w, np.float64, kv_bf16=False)
+    rounded = om.Model(cfg, w, np.float64)
+    assert rounded.kv_bf16 and not exact.kv_bf16
+    _, K, V = om.full_forward(rounded, toks, return_kv=True)
+    np.testing.assert_array_equal(om.round_to_bf16(K), K)
+    np.testing.assert_array_equal(om.round_to_bf16(V), V)
+    d = np.abs(om.full_forward(rounded, toks) - om.full_forward(exact, toks)).max()
+    assert 0 < d < 0.2  # bf16 storage is a small but visible perturbation
