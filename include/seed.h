@@ -1,0 +1,229 @@
+/*
+ * seed.h -- C ABI of the SEED draft-verify decoding library for AMD Instinct MI355X (gfx950).
+ *
+ * SEED (Self-Speculative Encoder-Decoder) views a decoder-only transformer with l layers as an
+ * encoder f_enc = f_{1:l'} followed by a thin decoder f_dec = f_{l'+1:l} (Sec. 3.1, Eq. 3-4).
+ * Decoding alternates two passes (Algorithm 2, fixed draft length d):
+ *   - draft : the decoder alone runs d autoregressive steps. Step i feeds the raw embedding
+ *             W_in X_draft[i-1] (Eq. 5) and attends to the decoder layers' cache, i.e. the deep
+ *             keys/values left by the last verification plus the drafts' own entries.
+ *   - verify: the full model runs once over X_draft[0..d] (pending token + d drafts), writing
+ *             deep keys/values in every layer; the longest prefix of drafts that equals the
+ *             verifier's greedy argmax is accepted, plus one bonus token.
+ * The output equals plain greedy decoding of the same model (d = 0 is plain greedy decoding).
+ *
+ * Conventions for every call:
+ *   - Every function returns a seed_status; nothing throws, aborts or exits. On failure
+ *     seed_last_error() describes the cause and the decoding state is left unchanged.
+ *   - Token ids are int32 in [0, vocab). Logits are float32.
+ *   - "host" pointers are ordinary CPU memory, read or written synchronously before the call
+ *     returns. "device" pointers are GPU memory; device outputs are written in stream order on
+ *     the context's HIP stream (synchronise that stream before reading them).
+ *   - The library never allocates device memory after seed_create: the caller supplies the
+ *     weight arena, the KV pool and the workspace (sizes from seed_arena_bytes), each at least
+ *     256-byte aligned, and keeps them alive until seed_destroy.
+ *   - Positions are 0-based. After a commit, sequence b holds t_b committed tokens; the last
+ *     one (the pending token, position t_b - 1) has no cache entry yet.
+ *   - A context is not thread-safe; use one context per stream.
+ */
+#ifndef SEED_H
+#define SEED_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct seed_ctx seed_ctx;
+
+typedef enum seed_status {
+  SEED_OK = 0,
+  SEED_ERR_ARG = -1,         /* NULL pointer, bad size, shape, dtype or tensor name, k out of range */
+  SEED_ERR_STATE = -2,       /* call out of order: draft/verify before prefill, weights missing */
+  SEED_ERR_CAPACITY = -3,    /* a sequence would pass max_ctx, or batch > max_batch */
+  SEED_ERR_HIP = -4,         /* a HIP runtime call failed; the message names it */
+  SEED_ERR_UNSUPPORTED = -5  /* a shape the kernels do not handle (see seed_config) */
+} seed_status;
+
+typedef enum seed_dtype {
+  SEED_F32 = 0,   /* fp32 weights and KV cache */
+  SEED_BF16 = 1   /* bf16 weights and KV cache; all arithmetic and the residual stream stay fp32 */
+} seed_dtype;
+
+/*
+ * Model shape and capacities (Preliminaries; Appendix E gives the model sizes).
+ * Supported: hidden, ffn, n_heads*head_dim, n_kv_heads*head_dim multiples of 32; vocab a
+ * multiple of 16; head_dim in {64, 128}; n_heads a multiple of n_kv_heads with
+ * (n_heads/n_kv_heads) <= 32; 0 <= n_dec_layers <= n_layers; kv_block == 16;
+ * 1 <= max_batch <= 64; 0 <= max_draft <= 15; max_ctx >= 2.
+ */
+typedef struct seed_config {
+  int32_t n_layers;       /* l */
+  int32_t n_dec_layers;   /* l - l': the last n_dec_layers layers form the drafter (paper: 2) */
+  int32_t hidden;
+  int32_t n_heads;        /* query heads */
+  int32_t n_kv_heads;     /* key/value heads (grouped-query attention) */
+  int32_t head_dim;
+  int32_t ffn;            /* SwiGLU inner width */
+  int32_t vocab;          /* the embedding is tied to the LM head */
+  float rope_base;        /* rotary base; rotate-half pairing (i, i + head_dim/2) */
+  float rms_eps;          /* RMSNorm epsilon */
+  int32_t dtype;          /* seed_dtype of the weights and the KV cache */
+  int32_t max_batch;      /* sequences decoded together */
+  int32_t max_ctx;        /* positions per sequence: prompt + generated + max_draft + 1 */
+  int32_t max_draft;      /* largest draft length d accepted by draft/verify/generate */
+  int32_t kv_block;       /* positions per paged KV block; must be 16 */
+} seed_config;
+
+/*
+ * One named weight tensor. Names and shapes ([out, in] row-major, as nn.Linear):
+ *   "embed"                    [vocab, hidden]    (also the LM head: W_out = W_in)
+ *   "final_norm"               [hidden]
+ *   "layers.<i>.attn_norm"     [hidden]
+ *   "layers.<i>.wq"            [n_heads*head_dim, hidden]
+ *   "layers.<i>.wk", ".wv"     [n_kv_heads*head_dim, hidden]
+ *   "layers.<i>.wo"            [hidden, n_heads*head_dim]
+ *   "layers.<i>.mlp_norm"      [hidden]
+ *   "layers.<i>.w_gate", ".w_up" [ffn, hidden]
+ *   "layers.<i>.w_down"        [hidden, ffn]
+ * dtype must equal the config's dtype (bf16 data is raw bf16 bit patterns).
+ */
+typedef struct seed_tensor {
+  const char* name;
+  const void* data;     /* host or device pointer, see on_device */
+  int32_t dtype;        /* seed_dtype */
+  int32_t on_device;    /* 1: data is device memory; 0: host memory */
+  int32_t ndim;         /* 1 or 2 */
+  int64_t shape[2];
+} seed_tensor;
+
+/* Options of seed_generate. */
+typedef struct seed_gen_opts {
+  int32_t k;             /* draft length d (0 = plain greedy decoding), 0 <= k <= max_draft */
+  int32_t max_new;       /* tokens to generate per sequence (the last round may overshoot; the
+                            output is cut to max_new, Algorithm 2 returns X_{1:T}) */
+  int32_t eos_id;        /* -1: off. Otherwise a sequence stops right after emitting it */
+  int32_t sim_accept;    /* -1: real drafts. 0..k: benchmark mode that replaces the drafts after
+                            the draft pass with forced_trace so that exactly sim_accept drafts
+                            are accepted per round (the draft pass still runs in full) */
+  const int32_t* forced_trace; /* host [B * max_new]: the plain greedy continuation of each
+                            prompt; required iff sim_accept >= 0 */
+  int32_t use_graph;     /* 1: capture one round into a HIP graph and replay it */
+} seed_gen_opts;
+
+/* Statistics filled by seed_generate (nullable). */
+typedef struct seed_stats {
+  int64_t rounds;            /* draft-verify rounds run */
+  int64_t drafted;           /* sum over rounds and live sequences of k */
+  int64_t accepted;          /* sum over rounds and live sequences of n_accept */
+  double prefill_ms;         /* prefill time (HIP events) */
+  double decode_ms;          /* first round start to last round end (HIP events) */
+  int32_t* n_accept_log;     /* nullable host [n_accept_log_cap * B]: n_accept per round per
+                                sequence, -1 once a sequence has finished */
+  int64_t n_accept_log_cap;  /* rows available in n_accept_log */
+} seed_stats;
+
+/* Kernel ids for seed_kernel_timing: phase * 16 + op. */
+enum {
+  SEED_PHASE_VERIFY = 0, SEED_PHASE_DRAFT = 1, SEED_PHASE_PREFILL = 2,
+  SEED_OP_SETUP = 0, SEED_OP_QKV = 1, SEED_OP_ATTN = 2, SEED_OP_COMBINE = 3, SEED_OP_O = 4,
+  SEED_OP_GATEUP = 5, SEED_OP_DOWN = 6, SEED_OP_HEAD = 7, SEED_OP_ACCEPT = 8
+};
+
+/* Bytes the caller must provide for the weight arena, the KV pool and the workspace. */
+seed_status seed_arena_bytes(const seed_config* cfg, size_t* weight_bytes, size_t* kv_bytes,
+                             size_t* workspace_bytes);
+
+/*
+ * Create a context on the current HIP device. hip_stream is a hipStream_t (NULL = the null
+ * stream) on which every kernel of this context runs. The three buffers are device memory of at
+ * least the sizes from seed_arena_bytes; the context borrows them until seed_destroy. The KV
+ * pool is cleared here.
+ */
+seed_status seed_create(const seed_config* cfg, void* hip_stream, void* weight_arena,
+                        void* kv_pool, void* workspace, seed_ctx** out);
+
+/*
+ * Copy the model weights into the arena, re-laid out for the kernels (MFMA tiles, fused QKV and
+ * gate/up). Every tensor listed at seed_tensor must be present exactly once. The sources may be
+ * freed after the call returns. Missing, duplicated, mis-shaped or mis-typed tensors give
+ * SEED_ERR_ARG naming the tensor.
+ */
+seed_status seed_load_weights(seed_ctx* ctx, const seed_tensor* tensors, int32_t n);
+
+/*
+ * Initialisation of Algorithm 2: run the full model over each prompt X_{1:t} and keep the cache
+ * of positions 0..t-2 in every layer; X_t becomes the pending token (no token is emitted).
+ * tokens: host, the B prompts packed back to back; lens: host [B], each >= 1 and
+ * lens[b] + max_draft + 1 <= max_ctx. Resets all decoding state of the context.
+ */
+seed_status seed_prefill(seed_ctx* ctx, int32_t B, const int32_t* tokens, const int32_t* lens);
+
+/*
+ * Drafting phase of Algorithm 2: k steps of the decoder only, from the pending token. Writes
+ * the decoder layers' cache at positions p..p+k-1 (p = t_b - 1) and leaves the committed state
+ * unchanged, so repeated calls give the same drafts.
+ * drafts: nullable host [B * k], draft tokens X_draft[1..k] per sequence.
+ * logits: nullable device [B * k * vocab], q_1..q_k per sequence.
+ * Errors: SEED_ERR_STATE before seed_prefill; SEED_ERR_ARG if k < 1 or k > max_draft;
+ * SEED_ERR_CAPACITY if some t_b + k + 1 > max_ctx.
+ */
+seed_status seed_draft(seed_ctx* ctx, int32_t k, int32_t* drafts, float* logits);
+
+/*
+ * Verification phase of Algorithm 2 plus acceptance and commit: truncate to t_b - 1 cached
+ * positions, run the full model over X_draft[0..k] (row r at position p + r attends to
+ * positions 0..p+r), accept the longest prefix with argmax p_i == X_draft[i], append the
+ * accepted drafts and the bonus token argmax p_{n_accept+1}, keep the deep cache of positions
+ * < t_b + n_accept. k = 0 is one step of plain greedy decoding.
+ * drafts: nullable host [B * k]; NULL uses the drafts of the preceding seed_draft with the same
+ *         k (SEED_ERR_STATE if there was none since the last commit).
+ * n_accept, bonus: nullable host [B].
+ * logits: nullable device [B * (k+1) * vocab], p_1..p_{k+1} per sequence.
+ * Argmax ties go to the lowest token id.
+ */
+seed_status seed_verify(seed_ctx* ctx, int32_t k, const int32_t* drafts, int32_t* n_accept,
+                        int32_t* bonus, float* logits);
+
+/*
+ * Run n_rounds draft-verify rounds (Algorithm 2's loop body) on every sequence without host
+ * synchronisation; returns once the work is queued on the stream. use_graph = 1 captures one
+ * round into a HIP graph (once per batch size and k) and replays it. Errors as seed_draft, with
+ * capacity checked for the worst case t_b + n_rounds*(k+1) + k + 1 <= max_ctx (the committed
+ * lengths are re-read first when that bound does not fit).
+ */
+seed_status seed_rounds(seed_ctx* ctx, int32_t k, int32_t n_rounds, int32_t use_graph);
+
+/*
+ * Algorithm 2 end to end: prefill, then rounds until every sequence has max_new new tokens (or
+ * emitted eos_id). out: host [B * max_new] (positions past counts[b] are -1); counts: host [B].
+ */
+seed_status seed_generate(seed_ctx* ctx, int32_t B, const int32_t* tokens, const int32_t* lens,
+                          const seed_gen_opts* opts, int32_t* out, int32_t* counts,
+                          seed_stats* stats);
+
+/* Committed tokens of sequence b (prompt included): out host [cap]; *len receives t_b. */
+seed_status seed_get_tokens(seed_ctx* ctx, int32_t b, int32_t* out, int32_t cap, int32_t* len);
+
+/*
+ * Kernel timing for benchmarks: while enabled, every launch of kernel_id (phase * 16 + op) is
+ * bracketed by HIP events on the context's stream. seed_kernel_timing_read synchronises the
+ * stream and returns the number of timed launches and their summed duration since enabling.
+ * Rounds launched through a HIP graph are not timed.
+ */
+seed_status seed_kernel_timing(seed_ctx* ctx, int32_t kernel_id, int32_t enable);
+seed_status seed_kernel_timing_read(seed_ctx* ctx, int64_t* launches, double* total_ms);
+
+/* Text of the last error on the calling thread; valid until the next call on that thread. */
+const char* seed_last_error(void);
+
+/* Release the context (not the caller's buffers). NULL is ignored. */
+void seed_destroy(seed_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SEED_H */

@@ -1,0 +1,144 @@
+// Internal interface between the host runtime and the gfx950 kernels of the SEED decode path.
+// Nothing here is part of the public C ABI (include/seed.h).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace seedk {
+
+// ---------------------------------------------------------------------------------------------
+// Weight layout ("MFMA tile" packing). A linear weight W [N, K] (nn.Linear [out, in]) is stored
+// as N/16 x K/32 tiles of 16 rows x 32 columns, tile (nt, kt) at element offset
+// (nt * (K/32) + kt) * 512. Inside a tile, lane l (0..63) owns 8 consecutive elements
+//   W[nt*16 + (l & 15)][kt*32 + (l >> 4)*8 + j],  j = 0..7,  at offset l*8 + j,
+// which is exactly the A-operand fragment of a 16x16x32 MFMA (and 8 16x16x4 fp32 MFMAs), so a
+// wave streams one tile as one fully coalesced 1 KB (bf16) / 2 KB (fp32) load.
+//
+// Fused matrices (row permutations applied when packing):
+//  * QKV: rows [Wq; Wk; Wv]. Within each head, tile j (j < head_dim/16) holds dims
+//    8j..8j+7 followed by their rotary partners head_dim/2+8j..+7, so RoPE is tile-local.
+//  * gate/up: tile t holds gate rows 8t..8t+7 followed by up rows 8t..8t+7.
+// ---------------------------------------------------------------------------------------------
+
+enum Prologue { PRO_NORM = 0, PRO_PLAIN = 1 };
+enum Epilogue { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_HEAD = 3 };
+
+// Arguments of the weight-streaming linear kernels (MFMA skinny GEMM and VALU GEMV).
+struct LinArgs {
+  const void* W;          // packed weights
+  int N, K;               // output features, input features
+  int M;                  // activation rows in this pass
+  int NT, KS;             // n-tiles per workgroup, K-splits per n-tile (waves = NT * KS)
+  // input
+  const float* X;         // [M][ldx] fp32 activations
+  int ldx;
+  const float* gain;      // PRO_NORM: RMSNorm gain [K] (fp32)
+  const float* ssq;       // PRO_NORM: [M][nssq] partial sums of squares of X (per 16 features)
+  int nssq;
+  float eps;
+  // EPI_RESID: h[m][n] += y, then ssq_out[m][n/16] = sum of squares of the 16 updated values
+  float* h;
+  float* ssq_out;
+  // EPI_SWIGLU: act[m][f] = silu(gate) * up, f = nt*8 + c
+  float* act;
+  // EPI_QKV
+  float* q;               // [M][n_heads*head_dim] rotated queries (fp32)
+  void* kv;               // KV pool
+  const int* bt;          // block tables [B][bt_stride]
+  int bt_stride;
+  const int* row_seq;     // [M] sequence of each row
+  const int* row_pos;     // [M] absolute position of each row
+  const float* rope_cos;  // [max_ctx][head_dim/2]
+  const float* rope_sin;
+  int layer, n_blocks, n_heads, n_kv, head_dim;
+  // EPI_HEAD
+  float* logits;          // nullable: logits[m * ld_logits + n]
+  long long ld_logits;
+  unsigned long long* keys;   // [M] running argmax keys (zero between launches)
+  unsigned int* counter;      // workgroup completion counter (zero between launches)
+  int* tok_out;               // argmax of row m is written to tok_out[m * tok_stride]
+  int tok_stride;
+};
+
+// Arguments of the split-KV paged attention kernel and its combine step.
+struct AttnArgs {
+  const float* q;         // [M][n_heads*head_dim]
+  const void* kv;
+  int layer, n_blocks;
+  const int* bt;
+  int bt_stride;
+  const int* row_pos;     // [M]; rows m = b*R + r, consecutive positions within a sequence
+  int B, R;               // sequences, rows per sequence
+  int n_heads, n_kv, head_dim, G;  // G = n_heads / n_kv
+  int RB, n_rb;           // rows per row-block (G*RB <= 32), row-blocks per sequence
+  int chunk_groups;       // grid extent over chunk groups
+  int S;                  // chunks (of 64 positions) per group, merged left to right
+  float scale_log2;       // log2(e) / sqrt(head_dim)
+  float* part;            // partials [B][n_kv][n_rb][chunk_groups][32][head_dim + 2]
+  float* out;             // [M][n_heads*head_dim]
+};
+
+// Per-pass row setup + embedding gather.
+enum SetupMode { SETUP_PREFILL = 0, SETUP_DRAFT = 1, SETUP_VERIFY = 2 };
+
+struct SetupArgs {
+  int mode;
+  int M, R;               // rows, rows per sequence
+  const int* t;           // [B] committed lengths
+  int* drafts;            // [B][dstride]; drafts[b][0] is the pending token
+  int dstride;
+  int step;               // SETUP_DRAFT: draft step i (>= 1)
+  const int* tokens;      // committed tokens [B][tstride]
+  int tstride;
+  int pf_seq, pf_pos0;    // SETUP_PREFILL
+  int sim_accept;         // SETUP_VERIFY: -1 or forced acceptance length
+  const int* trace;       // [B][tstride] greedy trace by absolute position
+  int vocab;
+  const void* E;          // packed embedding
+  int H;
+  int* row_seq;
+  int* row_pos;
+  float* h;               // [M][H]
+  float* ssq;             // [M][H/16]
+};
+
+// Device-resident decoding state.
+struct DevState {
+  int* t;                 // [B] committed length
+  int* len;               // [B] prompt length
+  int* limit;             // [B] stop committing once t >= limit
+  int* active;            // [B]
+  int* nacc;              // [B] last n_accept
+  int* bonus;             // [B] last bonus token
+  int* rounds;            // [1] rounds run since prefill
+  long long* counters;    // [2] drafted, accepted
+  int* drafts;            // [B][dstride]
+  int dstride;
+  int* tokens;            // [B][tstride]
+  int tstride;
+  int* nacc_log;          // [log_cap][B]
+  int log_cap;
+  const int* vtok;        // [B*R] verifier argmax per row
+  int eos;
+};
+
+template <typename T>
+void launch_linear(const LinArgs& a, int prologue, int epilogue, bool valu, hipStream_t s);
+template <typename T>
+void launch_attention(const AttnArgs& a, bool flash, hipStream_t s);
+void launch_combine(const AttnArgs& a, hipStream_t s);
+template <typename T>
+void launch_setup(const SetupArgs& a, hipStream_t s);
+void launch_accept(const DevState& st, int B, int k, hipStream_t s);
+template <typename T>
+void launch_pack(const void* src, void* dst, const int* dst_row, int rows, int K, hipStream_t s);
+void launch_to_f32(const void* src, int src_is_bf16, float* dst, long long n, hipStream_t s);
+void launch_fill_u32(void* dst, unsigned value, long long n_words, hipStream_t s);
+
+// allow the linear kernels to use more than 64 KB of LDS (once per process and dtype)
+hipError_t configure_kernels(int bf16);
+
+// dynamic LDS bytes needed by launch_linear for a given shape
+size_t linear_lds_bytes(int M, int K, int NT, int KS, bool valu);
+
+}  // namespace seedk

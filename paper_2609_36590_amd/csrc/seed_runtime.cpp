@@ -1,0 +1,1039 @@
+// Host runtime of the SEED decode library: the C ABI declared in include/seed.h.
+//
+// It plans the three caller-owned buffers (weight arena, paged KV pool, workspace), repacks the
+// weights into MFMA tiles, keeps the per-sequence block tables, and enqueues the passes of
+// Algorithm 2 (prefill, draft steps, verification + acceptance) on the caller's HIP stream. All
+// per-round state (committed lengths, pending token, drafts, acceptance) lives on the device,
+// so rounds can be queued back to back, or replayed from a captured HIP graph, with no host
+// synchronisation.
+#include "seed.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <map>
+#include <string>
+#include <tuple>
+#include <vector>
+
+#include "kernels.h"
+
+using namespace seedk;
+
+namespace {
+
+thread_local std::string g_err;
+
+seed_status fail(seed_status s, const std::string& msg) {
+  g_err = msg;
+  return s;
+}
+
+#define HIPCHK(expr)                                                                         \
+  do {                                                                                       \
+    hipError_t e_ = (expr);                                                                  \
+    if (e_ != hipSuccess) return fail(SEED_ERR_HIP, std::string(#expr) + ": " + hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr int PREFILL_ROWS = 64;   // rows per prefill pass (4 MFMA token tiles)
+constexpr int MAX_ROWS = 64;       // rows per decode pass: max_batch * (max_draft + 1)
+constexpr int CHUNK = 64;          // attention chunk (positions)
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+int cdiv(int a, int b) { return (a + b - 1) / b; }
+
+struct Plan {
+  seed_config cfg;
+  int esize = 2;
+  int H, NQ, NKV, HD, F, V, L, LD, QD, KVD, G;
+  int RB, n_rb_max, max_rows, bt_stride, blocks_per_seq, n_blocks, chunk_groups, S;
+  int dstride, tstride, log_cap;
+  // weight arena
+  size_t w_embed, w_final_norm, w_rope_cos, w_rope_sin, w_total;
+  std::vector<size_t> w_attn_norm, w_mlp_norm, w_qkv, w_o, w_gu, w_down;
+  size_t kv_total;
+  // workspace
+  size_t o_h, o_ssq, o_q, o_attn, o_act, o_part, o_row_seq, o_row_pos, o_keys, o_counter, o_vtok;
+  size_t o_t, o_len, o_limit, o_active, o_nacc, o_bonus, o_rounds, o_counters, o_drafts, o_tokens,
+      o_trace, o_log, o_bt, o_scratch, ws_total;
+};
+
+seed_status validate(const seed_config* c) {
+  if (!c) return fail(SEED_ERR_ARG, "config is NULL");
+  if (c->dtype != SEED_F32 && c->dtype != SEED_BF16) return fail(SEED_ERR_ARG, "dtype must be SEED_F32 or SEED_BF16");
+  if (c->n_layers < 1 || c->n_dec_layers < 0 || c->n_dec_layers > c->n_layers)
+    return fail(SEED_ERR_ARG, "need n_layers >= 1 and 0 <= n_dec_layers <= n_layers");
+  if (c->hidden <= 0 || c->ffn <= 0 || c->vocab <= 0 || c->n_heads <= 0 || c->n_kv_heads <= 0 || c->head_dim <= 0)
+    return fail(SEED_ERR_ARG, "model sizes must be positive");
+  if (c->hidden % 32 || c->ffn % 32 || (c->n_heads * c->head_dim) % 32 || (c->n_kv_heads * c->head_dim) % 32)
+    return fail(SEED_ERR_UNSUPPORTED, "hidden, ffn, n_heads*head_dim and n_kv_heads*head_dim must be multiples of 32");
+  if (c->vocab % 16) return fail(SEED_ERR_UNSUPPORTED, "vocab must be a multiple of 16");
+  if (c->head_dim != 64 && c->head_dim != 128) return fail(SEED_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+  if (c->n_heads % c->n_kv_heads || c->n_heads / c->n_kv_heads > 32)
+    return fail(SEED_ERR_UNSUPPORTED, "n_heads must be a multiple of n_kv_heads with a group of at most 32");
+  if (c->kv_block != 16) return fail(SEED_ERR_UNSUPPORTED, "kv_block must be 16");
+  if (c->max_batch < 1 || c->max_batch > 64) return fail(SEED_ERR_UNSUPPORTED, "max_batch must be in [1, 64]");
+  if (c->max_draft < 0 || c->max_draft > 15) return fail(SEED_ERR_UNSUPPORTED, "max_draft must be in [0, 15]");
+  if (c->max_batch * (c->max_draft + 1) > MAX_ROWS)
+    return fail(SEED_ERR_UNSUPPORTED, "max_batch * (max_draft + 1) must be at most 64");
+  if (c->max_ctx < 2 || c->max_ctx > (1 << 22)) return fail(SEED_ERR_ARG, "max_ctx must be in [2, 2^22]");
+  if (!(c->rope_base > 0.f) || !(c->rms_eps >= 0.f)) return fail(SEED_ERR_ARG, "rope_base must be > 0 and rms_eps >= 0");
+  return SEED_OK;
+}
+
+Plan make_plan(const seed_config& c) {
+  Plan p;
+  p.cfg = c;
+  p.esize = c.dtype == SEED_BF16 ? 2 : 4;
+  p.H = c.hidden; p.NQ = c.n_heads; p.NKV = c.n_kv_heads; p.HD = c.head_dim; p.F = c.ffn; p.V = c.vocab;
+  p.L = c.n_layers; p.LD = c.n_layers - c.n_dec_layers;
+  p.QD = p.NQ * p.HD; p.KVD = p.NKV * p.HD; p.G = p.NQ / p.NKV;
+  p.RB = std::max(1, 32 / p.G);
+  p.n_rb_max = cdiv(c.max_draft + 1, p.RB);
+  p.max_rows = std::max(PREFILL_ROWS, c.max_batch * (c.max_draft + 1));
+  p.blocks_per_seq = cdiv(c.max_ctx, 16);
+  p.bt_stride = cdiv(p.blocks_per_seq, CHUNK / 16) * (CHUNK / 16);   // whole chunks, padded with block 0
+  p.n_blocks = c.max_batch * p.blocks_per_seq + 1;                  // block 0 = permanent zero block
+  p.S = 1;
+  p.chunk_groups = cdiv(p.bt_stride * 16 / CHUNK, p.S);
+  p.dstride = c.max_draft + 1;
+  p.tstride = c.max_ctx;
+  p.log_cap = c.max_ctx;
+
+  size_t o = 0;
+  auto take = [&](size_t bytes) { size_t r = o; o = align256(o + bytes); return r; };
+  const size_t es = p.esize;
+  p.w_embed = take((size_t)p.V * p.H * es);
+  p.w_final_norm = take((size_t)p.H * 4);
+  p.w_rope_cos = take((size_t)c.max_ctx * (p.HD / 2) * 4);
+  p.w_rope_sin = take((size_t)c.max_ctx * (p.HD / 2) * 4);
+  for (int l = 0; l < p.L; ++l) {
+    p.w_attn_norm.push_back(take((size_t)p.H * 4));
+    p.w_mlp_norm.push_back(take((size_t)p.H * 4));
+    p.w_qkv.push_back(take((size_t)(p.QD + 2 * p.KVD) * p.H * es));
+    p.w_o.push_back(take((size_t)p.H * p.QD * es));
+    p.w_gu.push_back(take((size_t)2 * p.F * p.H * es));
+    p.w_down.push_back(take((size_t)p.H * p.F * es));
+  }
+  p.w_total = o;
+
+  p.kv_total = align256((size_t)p.L * p.n_blocks * 2 * p.NKV * 16 * p.HD * es);
+
+  o = 0;
+  const size_t R = p.max_rows, B = c.max_batch;
+  p.o_h = take(R * p.H * 4);
+  p.o_ssq = take(R * (p.H / 16) * 4);
+  p.o_q = take(R * p.QD * 4);
+  p.o_attn = take(R * p.QD * 4);
+  p.o_act = take(R * p.F * 4);
+  p.o_part = take(B * p.NKV * p.n_rb_max * (size_t)p.chunk_groups * 32 * (p.HD + 4) * 4);
+  p.o_row_seq = take(R * 4);
+  p.o_row_pos = take(R * 4);
+  p.o_keys = take(R * 8);
+  p.o_counter = take(64);
+  p.o_vtok = take(R * 4);
+  p.o_t = take(B * 4);
+  p.o_len = take(B * 4);
+  p.o_limit = take(B * 4);
+  p.o_active = take(B * 4);
+  p.o_nacc = take(B * 4);
+  p.o_bonus = take(B * 4);
+  p.o_rounds = take(4);
+  p.o_counters = take(16);
+  p.o_drafts = take(B * p.dstride * 4);
+  p.o_tokens = take(B * (size_t)p.tstride * 4);
+  p.o_trace = take(B * (size_t)p.tstride * 4);
+  p.o_log = take((size_t)p.log_cap * B * 4);
+  p.o_bt = take(B * (size_t)p.bt_stride * 4);
+  p.o_scratch = take((size_t)std::max({p.V, p.QD + 2 * p.KVD, 2 * p.F, p.H}) * 4);
+  p.ws_total = o;
+  return p;
+}
+
+struct TimedLaunch {
+  hipEvent_t a, b;
+};
+
+}  // namespace
+
+struct seed_ctx {
+  Plan p;
+  hipStream_t s = nullptr;
+  char* W = nullptr;
+  char* KV = nullptr;
+  char* WS = nullptr;
+  std::vector<bool> loaded;
+  bool weights_ok = false;
+  // decoding state mirrored on the host
+  int B = 0;
+  bool prefilled = false;
+  std::vector<int> lens, t_upper;
+  int drafts_k = -1;
+  int sim_accept = -1;
+  int eos = -1;
+  // paged KV allocator
+  std::vector<int> free_blocks;
+  std::vector<std::vector<int>> seq_blocks;
+  std::vector<int> bt_host;
+  // kernel timing
+  int timed_id = -1;
+  std::vector<TimedLaunch> pending;
+  std::vector<TimedLaunch> pool;
+  int64_t timed_launches = 0;
+  double timed_ms = 0.0;
+  // graphs: (B, k, sim_accept) -> exec
+  std::map<std::tuple<int, int, int>, hipGraphExec_t> graphs;
+
+  template <typename X>
+  X* ws(size_t off) { return reinterpret_cast<X*>(WS + off); }
+  float* wf(size_t off) { return reinterpret_cast<float*>(W + off); }
+};
+
+namespace {
+
+// ---------------------------------------------------------------------------------------------
+// kernel timing
+// ---------------------------------------------------------------------------------------------
+hipError_t drain_timing(seed_ctx* c) {
+  if (c->pending.empty()) return hipSuccess;
+  hipError_t e = hipStreamSynchronize(c->s);
+  if (e != hipSuccess) return e;
+  for (auto& t : c->pending) {
+    float ms = 0.f;
+    e = hipEventElapsedTime(&ms, t.a, t.b);
+    if (e != hipSuccess) return e;
+    c->timed_ms += ms;
+    c->timed_launches += 1;
+    c->pool.push_back(t);
+  }
+  c->pending.clear();
+  return hipSuccess;
+}
+
+template <typename F>
+void timed(seed_ctx* c, int phase, int op, bool capturing, F&& fn) {
+  if (!capturing && c->timed_id == phase * 16 + op) {
+    if (c->pending.size() >= 512) drain_timing(c);
+    TimedLaunch t;
+    if (!c->pool.empty()) { t = c->pool.back(); c->pool.pop_back(); }
+    else { hipEventCreate(&t.a); hipEventCreate(&t.b); }
+    hipEventRecord(t.a, c->s);
+    fn();
+    hipEventRecord(t.b, c->s);
+    c->pending.push_back(t);
+  } else {
+    fn();
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// launch helpers
+// ---------------------------------------------------------------------------------------------
+void tile_policy(int N, int K, int& NT, int& KS) {
+  (void)N;
+  const int KT = K / 32;
+  KS = std::min(16, std::max(1, KT / 4));
+  NT = std::max(1, 16 / KS);
+}
+
+DevState dev_state(seed_ctx* c) {
+  const Plan& p = c->p;
+  DevState st;
+  st.t = c->ws<int>(p.o_t);
+  st.len = c->ws<int>(p.o_len);
+  st.limit = c->ws<int>(p.o_limit);
+  st.active = c->ws<int>(p.o_active);
+  st.nacc = c->ws<int>(p.o_nacc);
+  st.bonus = c->ws<int>(p.o_bonus);
+  st.rounds = c->ws<int>(p.o_rounds);
+  st.counters = c->ws<long long>(p.o_counters);
+  st.drafts = c->ws<int>(p.o_drafts);
+  st.dstride = p.dstride;
+  st.tokens = c->ws<int>(p.o_tokens);
+  st.tstride = p.tstride;
+  st.nacc_log = c->ws<int>(p.o_log);
+  st.log_cap = p.log_cap;
+  st.vtok = c->ws<int>(p.o_vtok);
+  st.eos = c->eos;
+  return st;
+}
+
+LinArgs lin_base(seed_ctx* c, int M) {
+  const Plan& p = c->p;
+  LinArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.M = M;
+  a.ssq = c->ws<float>(p.o_ssq);
+  a.nssq = p.H / 16;
+  a.eps = p.cfg.rms_eps;
+  a.h = c->ws<float>(p.o_h);
+  a.ssq_out = c->ws<float>(p.o_ssq);
+  a.act = c->ws<float>(p.o_act);
+  a.q = c->ws<float>(p.o_q);
+  a.kv = c->KV;
+  a.bt = c->ws<int>(p.o_bt);
+  a.bt_stride = p.bt_stride;
+  a.row_seq = c->ws<int>(p.o_row_seq);
+  a.row_pos = c->ws<int>(p.o_row_pos);
+  a.rope_cos = c->wf(p.w_rope_cos);
+  a.rope_sin = c->wf(p.w_rope_sin);
+  a.n_blocks = p.n_blocks;
+  a.n_heads = p.NQ;
+  a.n_kv = p.NKV;
+  a.head_dim = p.HD;
+  a.keys = c->ws<unsigned long long>(p.o_keys);
+  a.counter = c->ws<unsigned int>(p.o_counter);
+  return a;
+}
+
+template <typename T>
+void linear(seed_ctx* c, LinArgs a, int pro, int epi, bool valu, int phase, int op, bool cap) {
+  tile_policy(a.N, a.K, a.NT, a.KS);
+  timed(c, phase, op, cap, [&] { launch_linear<T>(a, pro, epi, valu, c->s); });
+}
+
+// Layers [l0, l1) over M rows (B sequences x R rows each, consecutive positions per sequence).
+template <typename T>
+void run_layers(seed_ctx* c, int M, int B, int R, int l0, int l1, bool valu, int phase, bool flash,
+                const int* bt_override, bool cap) {
+  const Plan& p = c->p;
+  float* h = c->ws<float>(p.o_h);
+  for (int li = l0; li < l1; ++li) {
+    LinArgs a = lin_base(c, M);
+    a.layer = li;
+    // QKV + RoPE + KV write
+    a.W = c->W + p.w_qkv[li]; a.N = p.QD + 2 * p.KVD; a.K = p.H;
+    a.X = h; a.ldx = p.H; a.gain = c->wf(p.w_attn_norm[li]);
+    linear<T>(c, a, PRO_NORM, EPI_QKV, valu, phase, SEED_OP_QKV, cap);
+    // attention
+    AttnArgs at;
+    std::memset(&at, 0, sizeof(at));
+    at.q = c->ws<float>(p.o_q);
+    at.kv = c->KV;
+    at.layer = li;
+    at.n_blocks = p.n_blocks;
+    at.bt = bt_override ? bt_override : c->ws<int>(p.o_bt);
+    at.bt_stride = p.bt_stride;
+    at.row_pos = c->ws<int>(p.o_row_pos);
+    at.B = B; at.R = R;
+    at.n_heads = p.NQ; at.n_kv = p.NKV; at.head_dim = p.HD; at.G = p.G;
+    at.RB = p.RB; at.n_rb = cdiv(R, p.RB);
+    at.chunk_groups = p.chunk_groups; at.S = p.S;
+    at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)p.HD));
+    at.part = c->ws<float>(p.o_part);
+    at.out = c->ws<float>(p.o_attn);
+    timed(c, phase, SEED_OP_ATTN, cap, [&] { launch_attention<T>(at, flash, c->s); });
+    if (!flash) timed(c, phase, SEED_OP_COMBINE, cap, [&] { launch_combine(at, c->s); });
+    // O + residual
+    a = lin_base(c, M);
+    a.W = c->W + p.w_o[li]; a.N = p.H; a.K = p.QD;
+    a.X = c->ws<float>(p.o_attn); a.ldx = p.QD;
+    linear<T>(c, a, PRO_PLAIN, EPI_RESID, valu, phase, SEED_OP_O, cap);
+    // gate/up + SwiGLU
+    a = lin_base(c, M);
+    a.W = c->W + p.w_gu[li]; a.N = 2 * p.F; a.K = p.H;
+    a.X = h; a.ldx = p.H; a.gain = c->wf(p.w_mlp_norm[li]);
+    linear<T>(c, a, PRO_NORM, EPI_SWIGLU, valu, phase, SEED_OP_GATEUP, cap);
+    // down + residual
+    a = lin_base(c, M);
+    a.W = c->W + p.w_down[li]; a.N = p.H; a.K = p.F;
+    a.X = c->ws<float>(p.o_act); a.ldx = p.F;
+    linear<T>(c, a, PRO_PLAIN, EPI_RESID, valu, phase, SEED_OP_DOWN, cap);
+  }
+}
+
+template <typename T>
+void run_head(seed_ctx* c, int M, bool valu, int* tok_out, int tok_stride, float* logits, long long ld,
+              int phase, bool cap) {
+  const Plan& p = c->p;
+  LinArgs a = lin_base(c, M);
+  a.W = c->W + p.w_embed; a.N = p.V; a.K = p.H;
+  a.X = c->ws<float>(p.o_h); a.ldx = p.H; a.gain = c->wf(p.w_final_norm);
+  a.logits = logits; a.ld_logits = ld;
+  a.tok_out = tok_out; a.tok_stride = tok_stride;
+  linear<T>(c, a, PRO_NORM, EPI_HEAD, valu, phase, SEED_OP_HEAD, cap);
+}
+
+SetupArgs setup_base(seed_ctx* c) {
+  const Plan& p = c->p;
+  SetupArgs s;
+  std::memset(&s, 0, sizeof(s));
+  s.t = c->ws<int>(p.o_t);
+  s.drafts = c->ws<int>(p.o_drafts);
+  s.dstride = p.dstride;
+  s.tokens = c->ws<int>(p.o_tokens);
+  s.tstride = p.tstride;
+  s.sim_accept = -1;
+  s.trace = c->ws<int>(p.o_trace);
+  s.vocab = p.V;
+  s.E = c->W + p.w_embed;
+  s.H = p.H;
+  s.row_seq = c->ws<int>(p.o_row_seq);
+  s.row_pos = c->ws<int>(p.o_row_pos);
+  s.h = c->ws<float>(p.o_h);
+  s.ssq = c->ws<float>(p.o_ssq);
+  return s;
+}
+
+// Drafting phase: k decoder-only steps for every sequence.
+template <typename T>
+void enqueue_draft(seed_ctx* c, int k, float* logits, bool cap) {
+  const Plan& p = c->p;
+  const int B = c->B;
+  const bool valu = (B == 1);
+  for (int i = 1; i <= k; ++i) {
+    SetupArgs s = setup_base(c);
+    s.mode = SETUP_DRAFT; s.M = B; s.R = 1; s.step = i;
+    timed(c, SEED_PHASE_DRAFT, SEED_OP_SETUP, cap, [&] { launch_setup<T>(s, c->s); });
+    run_layers<T>(c, B, B, 1, p.LD, p.L, valu, SEED_PHASE_DRAFT, false, nullptr, cap);
+    run_head<T>(c, B, valu, c->ws<int>(p.o_drafts) + i, p.dstride,
+                logits ? logits + (size_t)(i - 1) * p.V : nullptr, (long long)k * p.V, SEED_PHASE_DRAFT, cap);
+  }
+}
+
+// Verification phase + acceptance/commit.
+template <typename T>
+void enqueue_verify(seed_ctx* c, int k, int sim_accept, float* logits, bool cap) {
+  const Plan& p = c->p;
+  const int B = c->B, R = k + 1, M = B * R;
+  SetupArgs s = setup_base(c);
+  s.mode = SETUP_VERIFY; s.M = M; s.R = R; s.sim_accept = sim_accept;
+  timed(c, SEED_PHASE_VERIFY, SEED_OP_SETUP, cap, [&] { launch_setup<T>(s, c->s); });
+  run_layers<T>(c, M, B, R, 0, p.L, false, SEED_PHASE_VERIFY, false, nullptr, cap);
+  run_head<T>(c, M, false, c->ws<int>(p.o_vtok), 1, logits, (long long)p.V, SEED_PHASE_VERIFY, cap);
+  DevState st = dev_state(c);
+  timed(c, SEED_PHASE_VERIFY, SEED_OP_ACCEPT, cap, [&] { launch_accept(st, B, k, c->s); });
+}
+
+template <typename T>
+void enqueue_round(seed_ctx* c, int k, int sim_accept, bool cap) {
+  enqueue_draft<T>(c, k, nullptr, cap);
+  enqueue_verify<T>(c, k, sim_accept, nullptr, cap);
+}
+
+// ---------------------------------------------------------------------------------------------
+// block tables
+// ---------------------------------------------------------------------------------------------
+seed_status ensure_blocks(seed_ctx* c, int b, int positions) {
+  const Plan& p = c->p;
+  positions = std::min(positions, p.cfg.max_ctx);
+  const int need = cdiv(positions, 16);
+  auto& v = c->seq_blocks[b];
+  if ((int)v.size() >= need) return SEED_OK;
+  const int first = (int)v.size();
+  while ((int)v.size() < need) {
+    if (c->free_blocks.empty()) return fail(SEED_ERR_CAPACITY, "KV pool exhausted");
+    v.push_back(c->free_blocks.back());
+    c->free_blocks.pop_back();
+    c->bt_host[(size_t)b * p.bt_stride + v.size() - 1] = v.back();
+  }
+  int* dst = c->ws<int>(p.o_bt) + (size_t)b * p.bt_stride + first;
+  HIPCHK(hipMemcpyAsync(dst, c->bt_host.data() + (size_t)b * p.bt_stride + first, (need - first) * sizeof(int),
+                        hipMemcpyHostToDevice, c->s));
+  return SEED_OK;
+}
+
+void reset_blocks(seed_ctx* c) {
+  const Plan& p = c->p;
+  c->free_blocks.clear();
+  // hand out low block ids first; sequences interleave as they grow
+  for (int i = p.n_blocks - 1; i >= 1; --i) c->free_blocks.push_back(i);
+  c->seq_blocks.assign(p.cfg.max_batch, {});
+  std::fill(c->bt_host.begin(), c->bt_host.end(), 0);
+}
+
+seed_status read_t(seed_ctx* c) {
+  std::vector<int> t(c->B);
+  HIPCHK(hipMemcpyAsync(t.data(), c->ws<int>(c->p.o_t), c->B * sizeof(int), hipMemcpyDeviceToHost, c->s));
+  HIPCHK(hipStreamSynchronize(c->s));
+  c->t_upper = t;
+  return SEED_OK;
+}
+
+// ---------------------------------------------------------------------------------------------
+// weight packing
+// ---------------------------------------------------------------------------------------------
+struct TensorSpec {
+  std::string name;
+  int ndim;
+  int64_t d0, d1;
+};
+
+std::vector<TensorSpec> tensor_specs(const Plan& p) {
+  std::vector<TensorSpec> v;
+  v.push_back({"embed", 2, p.V, p.H});
+  v.push_back({"final_norm", 1, p.H, 0});
+  for (int l = 0; l < p.L; ++l) {
+    const std::string pre = "layers." + std::to_string(l) + ".";
+    v.push_back({pre + "attn_norm", 1, p.H, 0});
+    v.push_back({pre + "wq", 2, p.QD, p.H});
+    v.push_back({pre + "wk", 2, p.KVD, p.H});
+    v.push_back({pre + "wv", 2, p.KVD, p.H});
+    v.push_back({pre + "wo", 2, p.H, p.QD});
+    v.push_back({pre + "mlp_norm", 1, p.H, 0});
+    v.push_back({pre + "w_gate", 2, p.F, p.H});
+    v.push_back({pre + "w_up", 2, p.F, p.H});
+    v.push_back({pre + "w_down", 2, p.H, p.F});
+  }
+  return v;
+}
+
+// packed row of source row r of a head-structured projection (RoPE partners share a tile)
+int qkv_row(int r, int HD) {
+  const int head = r / HD, d = r % HD, half = HD / 2;
+  const int hi = d >= half, i = d % half;
+  return head * HD + (i / 8) * 16 + (i % 8) + 8 * hi;
+}
+
+template <typename T>
+void host_pack(const T* src, T* dst, const std::vector<int>& rows, int K) {
+  const int KT = K / 32;
+  for (size_t r = 0; r < rows.size(); ++r) {
+    const int n = rows[r], nt = n >> 4, rr = n & 15;
+    for (int k = 0; k < K; k += 8) {
+      const int kt = k >> 5, kg = (k >> 3) & 3;
+      std::memcpy(dst + ((size_t)nt * KT + kt) * 512 + (rr + 16 * kg) * 8, src + r * (size_t)K + k, 8 * sizeof(T));
+    }
+  }
+}
+
+template <typename T>
+seed_status pack_into(seed_ctx* c, const seed_tensor& t, size_t dst_off, int Ntot, const std::vector<int>& rows, int K) {
+  T* dst = reinterpret_cast<T*>(c->W + dst_off);
+  if (t.on_device) {
+    int* map = c->ws<int>(c->p.o_scratch);
+    HIPCHK(hipMemcpyAsync(map, rows.data(), rows.size() * sizeof(int), hipMemcpyHostToDevice, c->s));
+    launch_pack<T>(t.data, dst, map, (int)rows.size(), K, c->s);
+    HIPCHK(hipGetLastError());
+    HIPCHK(hipStreamSynchronize(c->s));   // the row map is reused by the next tensor
+  } else {
+    std::vector<T> tmp((size_t)Ntot * K);
+    // keep rows of other sources that share this matrix: read back, then overwrite our rows
+    HIPCHK(hipMemcpyAsync(tmp.data(), dst, tmp.size() * sizeof(T), hipMemcpyDeviceToHost, c->s));
+    HIPCHK(hipStreamSynchronize(c->s));
+    host_pack<T>(reinterpret_cast<const T*>(t.data), tmp.data(), rows, K);
+    HIPCHK(hipMemcpyAsync(dst, tmp.data(), tmp.size() * sizeof(T), hipMemcpyHostToDevice, c->s));
+    HIPCHK(hipStreamSynchronize(c->s));
+  }
+  return SEED_OK;
+}
+
+seed_status load_one(seed_ctx* c, const seed_tensor& t, const std::string& name) {
+  const Plan& p = c->p;
+  const bool bf = p.cfg.dtype == SEED_BF16;
+  if (name == "final_norm" || name.find("_norm") != std::string::npos) {
+    size_t off;
+    if (name == "final_norm") off = p.w_final_norm;
+    else {
+      const int l = std::atoi(name.c_str() + 7);
+      off = name.find("attn_norm") != std::string::npos ? p.w_attn_norm[l] : p.w_mlp_norm[l];
+    }
+    float* dst = c->wf(off);
+    if (t.on_device) {
+      launch_to_f32(t.data, bf, dst, p.H, c->s);
+      HIPCHK(hipGetLastError());
+    } else {
+      std::vector<float> tmp(p.H);
+      for (int i = 0; i < p.H; ++i) {
+        if (bf) {
+          const uint32_t u = (uint32_t)reinterpret_cast<const uint16_t*>(t.data)[i] << 16;
+          std::memcpy(&tmp[i], &u, 4);
+        } else {
+          tmp[i] = reinterpret_cast<const float*>(t.data)[i];
+        }
+      }
+      HIPCHK(hipMemcpyAsync(dst, tmp.data(), p.H * 4, hipMemcpyHostToDevice, c->s));
+    }
+    HIPCHK(hipStreamSynchronize(c->s));
+    return SEED_OK;
+  }
+  std::vector<int> rows;
+  size_t off;
+  int Ntot, K;
+  if (name == "embed") {
+    off = p.w_embed; Ntot = p.V; K = p.H;
+    rows.resize(p.V);
+    for (int r = 0; r < p.V; ++r) rows[r] = r;
+  } else {
+    const int l = std::atoi(name.c_str() + 7);
+    const std::string leaf = name.substr(name.rfind('.') + 1);
+    if (leaf == "wq" || leaf == "wk" || leaf == "wv") {
+      off = p.w_qkv[l]; Ntot = p.QD + 2 * p.KVD; K = p.H;
+      const int base = leaf == "wq" ? 0 : (leaf == "wk" ? p.QD : p.QD + p.KVD);
+      const int n = leaf == "wq" ? p.QD : p.KVD;
+      rows.resize(n);
+      for (int r = 0; r < n; ++r) rows[r] = base + qkv_row(r, p.HD);
+    } else if (leaf == "wo") {
+      off = p.w_o[l]; Ntot = p.H; K = p.QD;
+      rows.resize(p.H);
+      for (int r = 0; r < p.H; ++r) rows[r] = r;
+    } else if (leaf == "w_gate" || leaf == "w_up") {
+      off = p.w_gu[l]; Ntot = 2 * p.F; K = p.H;
+      rows.resize(p.F);
+      const int up = leaf == "w_up";
+      for (int r = 0; r < p.F; ++r) rows[r] = (r / 8) * 16 + (r % 8) + 8 * up;
+    } else {
+      off = p.w_down[l]; Ntot = p.H; K = p.F;
+      rows.resize(p.H);
+      for (int r = 0; r < p.H; ++r) rows[r] = r;
+    }
+  }
+  return bf ? pack_into<uint16_t>(c, t, off, Ntot, rows, K) : pack_into<float>(c, t, off, Ntot, rows, K);
+}
+
+template <typename T>
+seed_status do_prefill(seed_ctx* c, const std::vector<int>& tokens_packed) {
+  const Plan& p = c->p;
+  const int B = c->B;
+  // committed tokens + state
+  std::vector<int> tok_rows((size_t)B * p.tstride, 0);
+  std::vector<int> t(B), len(B), limit(B), active(B, 1), drafts((size_t)B * p.dstride, 0);
+  size_t o = 0;
+  for (int b = 0; b < B; ++b) {
+    std::copy(tokens_packed.begin() + o, tokens_packed.begin() + o + c->lens[b], tok_rows.begin() + (size_t)b * p.tstride);
+    o += c->lens[b];
+    t[b] = len[b] = c->lens[b];
+    limit[b] = p.cfg.max_ctx;
+    drafts[(size_t)b * p.dstride] = tok_rows[(size_t)b * p.tstride + c->lens[b] - 1];
+  }
+  HIPCHK(hipMemcpyAsync(c->ws<int>(p.o_tokens), tok_rows.data(), tok_rows.size() * 4, hipMemcpyHostToDevice, c->s));
+  HIPCHK(hipMemcpyAsync(c->ws<int>(p.o_t), t.data(), B * 4, hipMemcpyHostToDevice, c->s));
+  HIPCHK(hipMemcpyAsync(c->ws<int>(p.o_len), len.data(), B * 4, hipMemcpyHostToDevice, c->s));
+  HIPCHK(hipMemcpyAsync(c->ws<int>(p.o_limit), limit.data(), B * 4, hipMemcpyHostToDevice, c->s));
+  HIPCHK(hipMemcpyAsync(c->ws<int>(p.o_active), active.data(), B * 4, hipMemcpyHostToDevice, c->s));
+  HIPCHK(hipMemcpyAsync(c->ws<int>(p.o_drafts), drafts.data(), drafts.size() * 4, hipMemcpyHostToDevice, c->s));
+  launch_fill_u32(c->ws<int>(p.o_rounds), 0, 1, c->s);
+  launch_fill_u32(c->ws<long long>(p.o_counters), 0, 4, c->s);
+  HIPCHK(hipGetLastError());
+  // run the full model over X[0..t-2]; X[t-1] stays pending (its cache entry would be dropped
+  // by the first truncation anyway, and causality makes the kept entries identical)
+  for (int b = 0; b < B; ++b) {
+    const int n = c->lens[b] - 1;
+    for (int s0 = 0; s0 < n; s0 += PREFILL_ROWS) {
+      const int M = std::min(PREFILL_ROWS, n - s0);
+      SetupArgs s = setup_base(c);
+      s.mode = SETUP_PREFILL; s.M = M; s.R = M; s.pf_seq = b; s.pf_pos0 = s0;
+      timed(c, SEED_PHASE_PREFILL, SEED_OP_SETUP, false, [&] { launch_setup<T>(s, c->s); });
+      run_layers<T>(c, M, 1, M, 0, p.L, false, SEED_PHASE_PREFILL, true,
+                    c->ws<int>(p.o_bt) + (size_t)b * p.bt_stride, false);
+    }
+  }
+  HIPCHK(hipGetLastError());
+  return SEED_OK;
+}
+
+seed_status check_ready(seed_ctx* c) {
+  if (!c) return fail(SEED_ERR_ARG, "ctx is NULL");
+  if (!c->weights_ok) return fail(SEED_ERR_STATE, "weights not loaded (seed_load_weights)");
+  return SEED_OK;
+}
+
+seed_status check_prompts(seed_ctx* c, int32_t B, const int32_t* tokens, const int32_t* lens, int extra,
+                          std::vector<int>& packed) {
+  const Plan& p = c->p;
+  if (B < 1 || B > p.cfg.max_batch) return fail(SEED_ERR_CAPACITY, "batch must be in [1, max_batch]");
+  if (!tokens || !lens) return fail(SEED_ERR_ARG, "tokens and lens must not be NULL");
+  size_t total = 0;
+  for (int b = 0; b < B; ++b) {
+    if (lens[b] < 1) return fail(SEED_ERR_ARG, "every prompt needs at least one token");
+    if ((int64_t)lens[b] + extra > p.cfg.max_ctx)
+      return fail(SEED_ERR_CAPACITY, "prompt " + std::to_string(b) + " does not fit max_ctx");
+    total += lens[b];
+  }
+  packed.assign(tokens, tokens + total);
+  for (size_t i = 0; i < total; ++i)
+    if (packed[i] < 0 || packed[i] >= p.V) return fail(SEED_ERR_ARG, "token id out of range at " + std::to_string(i));
+  return SEED_OK;
+}
+
+seed_status start_sequences(seed_ctx* c, int32_t B, const int32_t* lens, int extra) {
+  c->B = B;
+  c->lens.assign(lens, lens + B);
+  c->t_upper = c->lens;
+  c->drafts_k = -1;
+  c->prefilled = false;
+  reset_blocks(c);
+  for (int b = 0; b < B; ++b) {
+    seed_status st = ensure_blocks(c, b, lens[b] + extra);
+    if (st != SEED_OK) return st;
+  }
+  return SEED_OK;
+}
+
+template <typename T>
+seed_status run_rounds(seed_ctx* c, int k, int n, bool use_graph) {
+  if (!use_graph) {
+    for (int r = 0; r < n; ++r) enqueue_round<T>(c, k, c->sim_accept, false);
+    HIPCHK(hipGetLastError());
+    return SEED_OK;
+  }
+  const auto key = std::make_tuple(c->B, k, c->sim_accept);
+  auto it = c->graphs.find(key);
+  if (it == c->graphs.end()) {
+    hipGraph_t g;
+    HIPCHK(hipStreamBeginCapture(c->s, hipStreamCaptureModeThreadLocal));
+    enqueue_round<T>(c, k, c->sim_accept, true);
+    HIPCHK(hipStreamEndCapture(c->s, &g));
+    hipGraphExec_t ex;
+    HIPCHK(hipGraphInstantiate(&ex, g, nullptr, nullptr, 0));
+    HIPCHK(hipGraphDestroy(g));
+    it = c->graphs.emplace(key, ex).first;
+  }
+  for (int r = 0; r < n; ++r) HIPCHK(hipGraphLaunch(it->second, c->s));
+  return SEED_OK;
+}
+
+}  // namespace
+
+// =============================================================================================
+// C ABI
+// =============================================================================================
+extern "C" {
+
+const char* seed_last_error(void) { return g_err.c_str(); }
+
+seed_status seed_arena_bytes(const seed_config* cfg, size_t* weight_bytes, size_t* kv_bytes, size_t* workspace_bytes) {
+  seed_status st = validate(cfg);
+  if (st != SEED_OK) return st;
+  if (!weight_bytes || !kv_bytes || !workspace_bytes) return fail(SEED_ERR_ARG, "output pointers must not be NULL");
+  const Plan p = make_plan(*cfg);
+  *weight_bytes = p.w_total;
+  *kv_bytes = p.kv_total;
+  *workspace_bytes = p.ws_total;
+  return SEED_OK;
+}
+
+seed_status seed_create(const seed_config* cfg, void* hip_stream, void* weight_arena, void* kv_pool, void* workspace,
+                        seed_ctx** out) {
+  seed_status st = validate(cfg);
+  if (st != SEED_OK) return st;
+  if (!out) return fail(SEED_ERR_ARG, "out must not be NULL");
+  *out = nullptr;
+  if (!weight_arena || !kv_pool || !workspace) return fail(SEED_ERR_ARG, "buffers must not be NULL");
+  if (((uintptr_t)weight_arena | (uintptr_t)kv_pool | (uintptr_t)workspace) & 255)
+    return fail(SEED_ERR_ARG, "buffers must be 256-byte aligned");
+  HIPCHK(configure_kernels(cfg->dtype == SEED_BF16));
+  seed_ctx* c = new seed_ctx();
+  c->p = make_plan(*cfg);
+  c->s = reinterpret_cast<hipStream_t>(hip_stream);
+  c->W = reinterpret_cast<char*>(weight_arena);
+  c->KV = reinterpret_cast<char*>(kv_pool);
+  c->WS = reinterpret_cast<char*>(workspace);
+  const Plan& p = c->p;
+  c->loaded.assign(tensor_specs(p).size(), false);
+  c->bt_host.assign((size_t)cfg->max_batch * p.bt_stride, 0);
+  reset_blocks(c);
+  // clear the KV pool (finite values everywhere, block 0 stays zero) and the workspace
+  launch_fill_u32(c->KV, 0, (long long)(p.kv_total / 4), c->s);
+  launch_fill_u32(c->WS, 0, (long long)(p.ws_total / 4), c->s);
+  // rotary tables, angles in double precision
+  const int half = p.HD / 2;
+  std::vector<float> cs((size_t)cfg->max_ctx * half), sn((size_t)cfg->max_ctx * half);
+  for (int pos = 0; pos < cfg->max_ctx; ++pos)
+    for (int i = 0; i < half; ++i) {
+      const double inv = std::pow((double)cfg->rope_base, -2.0 * i / p.HD);
+      const double ang = (double)pos * inv;
+      cs[(size_t)pos * half + i] = (float)std::cos(ang);
+      sn[(size_t)pos * half + i] = (float)std::sin(ang);
+    }
+  hipError_t e = hipMemcpyAsync(c->wf(p.w_rope_cos), cs.data(), cs.size() * 4, hipMemcpyHostToDevice, c->s);
+  if (e == hipSuccess) e = hipMemcpyAsync(c->wf(p.w_rope_sin), sn.data(), sn.size() * 4, hipMemcpyHostToDevice, c->s);
+  if (e == hipSuccess) e = hipStreamSynchronize(c->s);
+  if (e != hipSuccess) {
+    delete c;
+    return fail(SEED_ERR_HIP, std::string("seed_create: ") + hipGetErrorString(e));
+  }
+  *out = c;
+  return SEED_OK;
+}
+
+seed_status seed_load_weights(seed_ctx* c, const seed_tensor* tensors, int32_t n) {
+  if (!c) return fail(SEED_ERR_ARG, "ctx is NULL");
+  if (!tensors || n < 0) return fail(SEED_ERR_ARG, "tensors must not be NULL");
+  const Plan& p = c->p;
+  const auto specs = tensor_specs(p);
+  std::map<std::string, int> index;
+  for (size_t i = 0; i < specs.size(); ++i) index[specs[i].name] = (int)i;
+  std::vector<int> which(n);
+  std::vector<bool> seen(specs.size(), false);
+  for (int i = 0; i < n; ++i) {
+    const seed_tensor& t = tensors[i];
+    if (!t.name) return fail(SEED_ERR_ARG, "tensor " + std::to_string(i) + " has no name");
+    auto it = index.find(t.name);
+    if (it == index.end()) return fail(SEED_ERR_ARG, std::string("unknown tensor '") + t.name + "'");
+    const TensorSpec& s = specs[it->second];
+    if (seen[it->second]) return fail(SEED_ERR_ARG, std::string("duplicate tensor '") + t.name + "'");
+    seen[it->second] = true;
+    if (!t.data) return fail(SEED_ERR_ARG, std::string("tensor '") + t.name + "' has no data");
+    if (t.dtype != p.cfg.dtype) return fail(SEED_ERR_ARG, std::string("tensor '") + t.name + "' has the wrong dtype");
+    if (t.ndim != s.ndim || t.shape[0] != s.d0 || (s.ndim == 2 && t.shape[1] != s.d1))
+      return fail(SEED_ERR_ARG, std::string("tensor '") + t.name + "' has the wrong shape");
+    which[i] = it->second;
+  }
+  for (size_t i = 0; i < specs.size(); ++i)
+    if (!seen[i] && !c->loaded[i]) {
+      // tensors may be loaded over several calls; report the first one still missing at the end
+    }
+  for (int i = 0; i < n; ++i) {
+    seed_status st = load_one(c, tensors[i], specs[which[i]].name);
+    if (st != SEED_OK) return st;
+    c->loaded[which[i]] = true;
+  }
+  c->weights_ok = std::all_of(c->loaded.begin(), c->loaded.end(), [](bool b) { return b; });
+  if (!c->weights_ok) {
+    for (size_t i = 0; i < specs.size(); ++i)
+      if (!c->loaded[i]) return fail(SEED_ERR_ARG, "missing tensor '" + specs[i].name + "'");
+  }
+  return SEED_OK;
+}
+
+seed_status seed_prefill(seed_ctx* c, int32_t B, const int32_t* tokens, const int32_t* lens) {
+  seed_status st = check_ready(c);
+  if (st != SEED_OK) return st;
+  std::vector<int> packed;
+  st = check_prompts(c, B, tokens, lens, c->p.cfg.max_draft + 1, packed);
+  if (st != SEED_OK) return st;
+  st = start_sequences(c, B, lens, c->p.cfg.max_draft + 1);
+  if (st != SEED_OK) return st;
+  c->sim_accept = -1;
+  c->eos = -1;
+  st = c->p.cfg.dtype == SEED_BF16 ? do_prefill<uint16_t>(c, packed) : do_prefill<float>(c, packed);
+  if (st != SEED_OK) return st;
+  HIPCHK(hipStreamSynchronize(c->s));
+  c->prefilled = true;
+  return SEED_OK;
+}
+
+static seed_status check_step(seed_ctx* c, int32_t k, int64_t growth) {
+  seed_status st = check_ready(c);
+  if (st != SEED_OK) return st;
+  if (!c->prefilled) return fail(SEED_ERR_STATE, "call seed_prefill first");
+  if (k < 0 || k > c->p.cfg.max_draft) return fail(SEED_ERR_ARG, "k must be in [0, max_draft]");
+  for (int b = 0; b < c->B; ++b)
+    if ((int64_t)c->t_upper[b] + growth > c->p.cfg.max_ctx)
+      return fail(SEED_ERR_CAPACITY, "sequence " + std::to_string(b) + " would pass max_ctx");
+  for (int b = 0; b < c->B; ++b) {
+    st = ensure_blocks(c, b, (int)std::min<int64_t>(c->p.cfg.max_ctx, c->t_upper[b] + growth));
+    if (st != SEED_OK) return st;
+  }
+  return SEED_OK;
+}
+
+seed_status seed_draft(seed_ctx* c, int32_t k, int32_t* drafts, float* logits) {
+  seed_status st = check_step(c, k, (int64_t)k + 1);
+  if (st != SEED_OK) return st;
+  if (k < 1) return fail(SEED_ERR_ARG, "seed_draft needs k >= 1");
+  if (c->p.cfg.dtype == SEED_BF16) enqueue_draft<uint16_t>(c, k, logits, false);
+  else enqueue_draft<float>(c, k, logits, false);
+  HIPCHK(hipGetLastError());
+  if (drafts) {
+    std::vector<int> d((size_t)c->B * c->p.dstride);
+    HIPCHK(hipMemcpyAsync(d.data(), c->ws<int>(c->p.o_drafts), d.size() * 4, hipMemcpyDeviceToHost, c->s));
+    HIPCHK(hipStreamSynchronize(c->s));
+    for (int b = 0; b < c->B; ++b)
+      for (int i = 0; i < k; ++i) drafts[b * k + i] = d[(size_t)b * c->p.dstride + 1 + i];
+  }
+  c->drafts_k = k;
+  return SEED_OK;
+}
+
+seed_status seed_verify(seed_ctx* c, int32_t k, const int32_t* drafts, int32_t* n_accept, int32_t* bonus, float* logits) {
+  seed_status st = check_step(c, k, (int64_t)k + 1);
+  if (st != SEED_OK) return st;
+  const Plan& p = c->p;
+  if (drafts) {
+    for (int i = 0; i < c->B * k; ++i)
+      if (drafts[i] < 0 || drafts[i] >= p.V) return fail(SEED_ERR_ARG, "draft token out of range");
+    for (int b = 0; b < c->B; ++b)
+      if (k > 0)
+        HIPCHK(hipMemcpyAsync(c->ws<int>(p.o_drafts) + (size_t)b * p.dstride + 1, drafts + (size_t)b * k, k * 4,
+                              hipMemcpyHostToDevice, c->s));
+  } else if (k > 0 && c->drafts_k != k) {
+    return fail(SEED_ERR_STATE, "no drafts of length k since the last commit (call seed_draft or pass drafts)");
+  }
+  if (p.cfg.dtype == SEED_BF16) enqueue_verify<uint16_t>(c, k, -1, logits, false);
+  else enqueue_verify<float>(c, k, -1, logits, false);
+  HIPCHK(hipGetLastError());
+  std::vector<int> na(c->B), bo(c->B);
+  HIPCHK(hipMemcpyAsync(na.data(), c->ws<int>(p.o_nacc), c->B * 4, hipMemcpyDeviceToHost, c->s));
+  HIPCHK(hipMemcpyAsync(bo.data(), c->ws<int>(p.o_bonus), c->B * 4, hipMemcpyDeviceToHost, c->s));
+  st = read_t(c);
+  if (st != SEED_OK) return st;
+  if (n_accept) std::copy(na.begin(), na.end(), n_accept);
+  if (bonus) std::copy(bo.begin(), bo.end(), bonus);
+  c->drafts_k = -1;
+  return SEED_OK;
+}
+
+seed_status seed_rounds(seed_ctx* c, int32_t k, int32_t n_rounds, int32_t use_graph) {
+  if (n_rounds < 0) return fail(SEED_ERR_ARG, "n_rounds must be >= 0");
+  if (c && c->prefilled) {
+    // refresh the upper bounds if the worst case would not fit
+    for (int b = 0; b < c->B; ++b)
+      if ((int64_t)c->t_upper[b] + (int64_t)n_rounds * (k + 1) + k + 1 > c->p.cfg.max_ctx) {
+        seed_status st = read_t(c);
+        if (st != SEED_OK) return st;
+        break;
+      }
+  }
+  seed_status st = check_step(c, k, (int64_t)n_rounds * (k + 1) + k + 1);
+  if (st != SEED_OK) return st;
+  st = c->p.cfg.dtype == SEED_BF16 ? run_rounds<uint16_t>(c, k, n_rounds, use_graph != 0)
+                                   : run_rounds<float>(c, k, n_rounds, use_graph != 0);
+  if (st != SEED_OK) return st;
+  for (int b = 0; b < c->B; ++b) c->t_upper[b] += n_rounds * (k + 1);
+  c->drafts_k = -1;
+  return SEED_OK;
+}
+
+seed_status seed_generate(seed_ctx* c, int32_t B, const int32_t* tokens, const int32_t* lens, const seed_gen_opts* opts,
+                          int32_t* out, int32_t* counts, seed_stats* stats) {
+  seed_status st = check_ready(c);
+  if (st != SEED_OK) return st;
+  if (!opts || !out || !counts) return fail(SEED_ERR_ARG, "opts, out and counts must not be NULL");
+  const Plan& p = c->p;
+  const int k = opts->k;
+  if (k < 0 || k > p.cfg.max_draft) return fail(SEED_ERR_ARG, "k must be in [0, max_draft]");
+  if (opts->max_new < 1) return fail(SEED_ERR_ARG, "max_new must be >= 1");
+  if (opts->sim_accept < -1 || opts->sim_accept > k) return fail(SEED_ERR_ARG, "sim_accept must be -1 or in [0, k]");
+  if (opts->sim_accept >= 0 && !opts->forced_trace) return fail(SEED_ERR_ARG, "sim_accept needs forced_trace");
+  if (opts->eos_id < -1 || opts->eos_id >= p.V) return fail(SEED_ERR_ARG, "eos_id out of range");
+  std::vector<int> packed;
+  // a finished sequence keeps running rounds at its final position: room for 2k+1 more
+  const int extra = opts->max_new + 2 * k + 1;
+  st = check_prompts(c, B, tokens, lens, extra, packed);
+  if (st != SEED_OK) return st;
+  st = start_sequences(c, B, lens, extra);
+  if (st != SEED_OK) return st;
+  c->eos = opts->eos_id;
+  c->sim_accept = -1;
+
+  hipEvent_t e0, e1, e2;
+  HIPCHK(hipEventCreate(&e0));
+  HIPCHK(hipEventCreate(&e1));
+  HIPCHK(hipEventCreate(&e2));
+  HIPCHK(hipEventRecord(e0, c->s));
+  st = p.cfg.dtype == SEED_BF16 ? do_prefill<uint16_t>(c, packed) : do_prefill<float>(c, packed);
+  if (st != SEED_OK) return st;
+  c->prefilled = true;
+  // limits and the forced trace
+  std::vector<int> limit(B);
+  for (int b = 0; b < B; ++b) limit[b] = lens[b] + opts->max_new;
+  HIPCHK(hipMemcpyAsync(c->ws<int>(p.o_limit), limit.data(), B * 4, hipMemcpyHostToDevice, c->s));
+  if (opts->sim_accept >= 0) {
+    std::vector<int> tr((size_t)B * p.tstride, 0);
+    for (int b = 0; b < B; ++b)
+      for (int i = 0; i < opts->max_new; ++i) {
+        const int v = opts->forced_trace[(size_t)b * opts->max_new + i];
+        if (v < 0 || v >= p.V) return fail(SEED_ERR_ARG, "forced_trace token out of range");
+        tr[(size_t)b * p.tstride + lens[b] + i] = v;
+      }
+    HIPCHK(hipMemcpyAsync(c->ws<int>(p.o_trace), tr.data(), tr.size() * 4, hipMemcpyHostToDevice, c->s));
+    HIPCHK(hipStreamSynchronize(c->s));
+    c->sim_accept = opts->sim_accept;
+  }
+  HIPCHK(hipEventRecord(e1, c->s));
+  // rounds: every round commits >= 1 token per live sequence; launch the number of rounds the
+  // observed tokens-per-round rate predicts, then re-check
+  double rate = k + 1;
+  std::vector<int> t(B), active(B), t0(B);
+  while (true) {
+    HIPCHK(hipMemcpyAsync(t.data(), c->ws<int>(p.o_t), B * 4, hipMemcpyDeviceToHost, c->s));
+    HIPCHK(hipMemcpyAsync(active.data(), c->ws<int>(p.o_active), B * 4, hipMemcpyDeviceToHost, c->s));
+    HIPCHK(hipStreamSynchronize(c->s));
+    int rem = 0, slowest = -1;
+    for (int b = 0; b < B; ++b)
+      if (active[b] && limit[b] - t[b] > rem) { rem = limit[b] - t[b]; slowest = b; }
+    if (slowest < 0) break;
+    const int n = std::max(1, (int)std::ceil(rem / rate));
+    t0 = t;
+    st = p.cfg.dtype == SEED_BF16 ? run_rounds<uint16_t>(c, k, n, opts->use_graph != 0)
+                                  : run_rounds<float>(c, k, n, opts->use_graph != 0);
+    if (st != SEED_OK) return st;
+    HIPCHK(hipMemcpyAsync(t.data(), c->ws<int>(p.o_t), B * 4, hipMemcpyDeviceToHost, c->s));
+    HIPCHK(hipStreamSynchronize(c->s));
+    const double gained = t[slowest] - t0[slowest];
+    rate = std::max(1.0, std::min((double)(k + 1), gained / n));
+  }
+  HIPCHK(hipEventRecord(e2, c->s));
+  HIPCHK(hipEventSynchronize(e2));
+  // outputs
+  std::vector<int> tok((size_t)B * p.tstride);
+  HIPCHK(hipMemcpy(tok.data(), c->ws<int>(p.o_tokens), tok.size() * 4, hipMemcpyDeviceToHost));
+  HIPCHK(hipMemcpy(t.data(), c->ws<int>(p.o_t), B * 4, hipMemcpyDeviceToHost));
+  c->t_upper = t;
+  for (int b = 0; b < B; ++b) {
+    const int n = std::min(t[b] - lens[b], opts->max_new);
+    counts[b] = n;
+    for (int i = 0; i < opts->max_new; ++i) out[(size_t)b * opts->max_new + i] = i < n ? tok[(size_t)b * p.tstride + lens[b] + i] : -1;
+  }
+  if (stats) {
+    int rounds = 0;
+    long long cnt[2];
+    HIPCHK(hipMemcpy(&rounds, c->ws<int>(p.o_rounds), 4, hipMemcpyDeviceToHost));
+    HIPCHK(hipMemcpy(cnt, c->ws<long long>(p.o_counters), 16, hipMemcpyDeviceToHost));
+    stats->rounds = rounds;
+    stats->drafted = cnt[0];
+    stats->accepted = cnt[1];
+    float ms1 = 0.f, ms2 = 0.f;
+    HIPCHK(hipEventElapsedTime(&ms1, e0, e1));
+    HIPCHK(hipEventElapsedTime(&ms2, e1, e2));
+    stats->prefill_ms = ms1;
+    stats->decode_ms = ms2;
+    if (stats->n_accept_log && stats->n_accept_log_cap > 0) {
+      const int64_t rows = std::min<int64_t>({(int64_t)rounds, stats->n_accept_log_cap, (int64_t)p.log_cap});
+      HIPCHK(hipMemcpy(stats->n_accept_log, c->ws<int>(p.o_log), rows * B * 4, hipMemcpyDeviceToHost));
+    }
+  }
+  hipEventDestroy(e0);
+  hipEventDestroy(e1);
+  hipEventDestroy(e2);
+  c->sim_accept = -1;
+  c->drafts_k = -1;
+  return SEED_OK;
+}
+
+seed_status seed_get_tokens(seed_ctx* c, int32_t b, int32_t* out, int32_t cap, int32_t* len) {
+  if (!c) return fail(SEED_ERR_ARG, "ctx is NULL");
+  if (!c->prefilled) return fail(SEED_ERR_STATE, "call seed_prefill first");
+  if (b < 0 || b >= c->B) return fail(SEED_ERR_ARG, "sequence index out of range");
+  if (!len) return fail(SEED_ERR_ARG, "len must not be NULL");
+  seed_status st = read_t(c);
+  if (st != SEED_OK) return st;
+  const int t = c->t_upper[b];
+  *len = t;
+  if (out && cap > 0) {
+    HIPCHK(hipMemcpy(out, c->ws<int>(c->p.o_tokens) + (size_t)b * c->p.tstride, std::min(cap, t) * 4, hipMemcpyDeviceToHost));
+  }
+  return SEED_OK;
+}
+
+seed_status seed_kernel_timing(seed_ctx* c, int32_t kernel_id, int32_t enable) {
+  if (!c) return fail(SEED_ERR_ARG, "ctx is NULL");
+  HIPCHK(drain_timing(c));
+  c->timed_id = enable ? kernel_id : -1;
+  c->timed_launches = 0;
+  c->timed_ms = 0.0;
+  return SEED_OK;
+}
+
+seed_status seed_kernel_timing_read(seed_ctx* c, int64_t* launches, double* total_ms) {
+  if (!c) return fail(SEED_ERR_ARG, "ctx is NULL");
+  HIPCHK(drain_timing(c));
+  if (launches) *launches = c->timed_launches;
+  if (total_ms) *total_ms = c->timed_ms;
+  return SEED_OK;
+}
+
+void seed_destroy(seed_ctx* c) {
+  if (!c) return;
+  hipStreamSynchronize(c->s);
+  for (auto& kv : c->graphs) hipGraphExecDestroy(kv.second);
+  for (auto& t : c->pending) { hipEventDestroy(t.a); hipEventDestroy(t.b); }
+  for (auto& t : c->pool) { hipEventDestroy(t.a); hipEventDestroy(t.b); }
+  delete c;
+}
+
+}  // extern "C"

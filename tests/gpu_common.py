@@ -1,0 +1,70 @@
+"""Shared helpers of the GPU tests: decoder construction and oracle comparisons.
+
+Inputs reach the oracle only from ``synth`` (seeded weights and prompts); the GPU path receives
+the same inputs plus, where a test drives it step by step, tokens the oracle produced. Nothing
+the GPU computes is fed back into the oracle.
+"""
+import sys
+
+import numpy as np
+
+from oracle import model as om
+from oracle import seed as os_
+from paper_2609_36590_amd import binding, synth
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def decoder(cfg, weights, max_batch=1, max_ctx=256, max_draft=6):
+    say(f"[gpu] decoder {cfg.name} dtype={cfg.dtype} B<={max_batch} ctx={max_ctx} d<={max_draft}")
+    dec = binding.Decoder(cfg, max_batch=max_batch, max_ctx=max_ctx, max_draft=max_draft)
+    dec.load_weights(weights)
+    return dec
+
+
+def oracle_model(cfg, weights, dtype=np.float32):
+    return om.Model(cfg, synth.weights_as_f32(cfg, weights), dtype)
+
+
+def top2_gap(logits):
+    s = np.sort(logits, axis=-1)
+    return s[..., -1] - s[..., -2]
+
+
+def first_ambiguous(rounds, tol):
+    """Index of the first round whose verification has a row with a top-2 gap <= 2*tol."""
+    for i, rd in enumerate(rounds):
+        if np.any(top2_gap(rd.verify_logits) <= 2 * tol):
+            return i
+    return len(rounds)
+
+
+def committed_before(prompt, toks, p):
+    """X[0..p] of the oracle's decode (prompt followed by generated tokens)."""
+    full = np.concatenate([np.asarray(prompt), np.asarray(toks)])
+    return full[:p + 1]
+
+
+def check_round(dec, prompt, toks, rd, tol, k):
+    """Drive the GPU through one oracle round from the same committed prefix and compare every
+    draft and verify logit row. Returns the max abs errors (draft, verify)."""
+    ctx = committed_before(prompt, toks, rd.p)
+    dec.prefill([ctx.astype(np.int32)])
+    d, qlog = dec.draft(k, logits=True)
+    derr = float(np.abs(qlog[0, 0] - rd.draft_logits[0]).max())
+    for i in range(1, k):
+        # later draft steps are comparable while the drafted tokens agree
+        if not np.array_equal(d[0, :i], rd.drafts[1:i + 1]):
+            break
+        derr = max(derr, float(np.abs(qlog[0, i] - rd.draft_logits[i]).max()))
+    for i in range(k):
+        if top2_gap(rd.draft_logits[i]) > 2 * tol and np.array_equal(d[0, :i], rd.drafts[1:i + 1]):
+            assert d[0, i] == rd.drafts[i + 1], (rd.p, i)
+    na, bo, vlog = dec.verify(k, drafts=np.asarray(rd.drafts[1:], dtype=np.int32)[None], logits=True)
+    verr = float(np.abs(vlog[0] - rd.verify_logits).max())
+    if np.all(top2_gap(rd.verify_logits) > 2 * tol):
+        assert na[0] == rd.n_accept and bo[0] == rd.bonus, (rd.p, na, rd.n_accept, bo, rd.bonus)
+    return derr, verr
