@@ -147,9 +147,11 @@ seed_status seed_create(const seed_config* cfg, void* hip_stream, void* weight_a
 
 /*
  * Copy the model weights into the arena, re-laid out for the kernels (MFMA tiles, fused QKV and
- * gate/up). Every tensor listed at seed_tensor must be present exactly once. The sources may be
- * freed after the call returns. Missing, duplicated, mis-shaped or mis-typed tensors give
- * SEED_ERR_ARG naming the tensor.
+ * gate/up). Tensors may be loaded over several calls, each name at most once per call; a later
+ * load of the same name replaces it. The sources may be freed after the call returns. Unknown,
+ * duplicated, mis-shaped or mis-typed tensors give SEED_ERR_ARG naming the tensor. Until every
+ * tensor listed at seed_tensor has been loaded, prefill/draft/verify/generate return
+ * SEED_ERR_STATE naming the first missing one.
  */
 seed_status seed_load_weights(seed_ctx* ctx, const seed_tensor* tensors, int32_t n);
 

@@ -228,8 +228,8 @@ __device__ __forceinline__ float row_rsqrt(const LinArgs& a, int m) {
 template <typename T, int PRO, int EPI, int TT>
 __global__ void __launch_bounds__(1024) k_linear_mfma(LinArgs a) {
   extern __shared__ float smem[];
-  float* s_rs = smem;          // [64]
-  float* s_red = smem + 64;    // [NW][M][16]
+  __shared__ float s_rs[64];
+  float* s_red = smem;         // [NW][M][16]
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int KT = a.K >> 5, n_tiles = a.N >> 4;
   const int M = a.M;
@@ -755,7 +755,7 @@ __global__ void k_fill_u32(uint32_t* dst, uint32_t v, long long n) {
 size_t linear_lds_bytes(int M, int K, int NT, int KS, bool valu) {
   const int NW = NT * KS;
   if (valu) return (size_t)(K + NW * 16) * sizeof(float);
-  return (size_t)(64 + NW * M * 16) * sizeof(float);
+  return (size_t)(NW * M * 16) * sizeof(float);
 }
 
 template <typename T, int PRO, int EPI>
@@ -834,30 +834,32 @@ void launch_fill_u32(void* dst, unsigned value, long long n_words, hipStream_t s
 }
 
 template <typename T, int PRO, int EPI>
-static hipError_t allow_big_lds() {
-  const int bytes = 160 * 1024;
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_linear_valu<T, PRO, EPI>),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
-  if (e != hipSuccess) return e;
-  e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 1>), hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
-  if (e != hipSuccess) return e;
-  e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 2>), hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
-  if (e != hipSuccess) return e;
-  e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 3>), hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
-  if (e != hipSuccess) return e;
-  return hipFuncSetAttribute(reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 4>), hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+static void allow_big_lds(int bytes) {
+  const void* fns[] = {reinterpret_cast<const void*>(&k_linear_valu<T, PRO, EPI>),
+                       reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 1>),
+                       reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 2>),
+                       reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 3>),
+                       reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 4>)};
+  for (const void* f : fns) (void)hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
 }
 
-template <typename T>
-static hipError_t configure_type() {
-  hipError_t e;
-  if ((e = allow_big_lds<T, PRO_NORM, EPI_QKV>()) != hipSuccess) return e;
-  if ((e = allow_big_lds<T, PRO_NORM, EPI_SWIGLU>()) != hipSuccess) return e;
-  if ((e = allow_big_lds<T, PRO_NORM, EPI_HEAD>()) != hipSuccess) return e;
-  return allow_big_lds<T, PRO_PLAIN, EPI_RESID>();
+// Every launch stays within 64 KB of dynamic LDS; where the device allows more, opt in anyway
+// (failures are harmless and cleared).
+hipError_t configure_kernels(int bf16) {
+  int dev = 0, optin = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return hipGetLastError();
+  if (hipDeviceGetAttribute(&optin, hipDeviceAttributeSharedMemPerBlockOptin, dev) == hipSuccess && optin > 65536) {
+    if (bf16) {
+      allow_big_lds<uint16_t, PRO_NORM, EPI_QKV>(optin); allow_big_lds<uint16_t, PRO_NORM, EPI_SWIGLU>(optin);
+      allow_big_lds<uint16_t, PRO_NORM, EPI_HEAD>(optin); allow_big_lds<uint16_t, PRO_PLAIN, EPI_RESID>(optin);
+    } else {
+      allow_big_lds<float, PRO_NORM, EPI_QKV>(optin); allow_big_lds<float, PRO_NORM, EPI_SWIGLU>(optin);
+      allow_big_lds<float, PRO_NORM, EPI_HEAD>(optin); allow_big_lds<float, PRO_PLAIN, EPI_RESID>(optin);
+    }
+  }
+  (void)hipGetLastError();
+  return hipSuccess;
 }
-
-hipError_t configure_kernels(int bf16) { return bf16 ? configure_type<uint16_t>() : configure_type<float>(); }
 
 template void launch_linear<uint16_t>(const LinArgs&, int, int, bool, hipStream_t);
 template void launch_linear<float>(const LinArgs&, int, int, bool, hipStream_t);

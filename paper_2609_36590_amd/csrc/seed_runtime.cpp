@@ -37,7 +37,7 @@ seed_status fail(seed_status s, const std::string& msg) {
     if (e_ != hipSuccess) return fail(SEED_ERR_HIP, std::string(#expr) + ": " + hipGetErrorString(e_)); \
   } while (0)
 
-constexpr int PREFILL_ROWS = 64;   // rows per prefill pass (4 MFMA token tiles)
+constexpr int PREFILL_ROWS = 48;   // rows per prefill pass (3 MFMA token tiles)
 constexpr int MAX_ROWS = 64;       // rows per decode pass: max_batch * (max_draft + 1)
 constexpr int CHUNK = 64;          // attention chunk (positions)
 
@@ -626,7 +626,11 @@ seed_status do_prefill(seed_ctx* c, const std::vector<int>& tokens_packed) {
 
 seed_status check_ready(seed_ctx* c) {
   if (!c) return fail(SEED_ERR_ARG, "ctx is NULL");
-  if (!c->weights_ok) return fail(SEED_ERR_STATE, "weights not loaded (seed_load_weights)");
+  if (!c->weights_ok) {
+    const auto specs = tensor_specs(c->p);
+    for (size_t i = 0; i < specs.size(); ++i)
+      if (!c->loaded[i]) return fail(SEED_ERR_STATE, "weights not loaded: missing tensor '" + specs[i].name + "'");
+  }
   return SEED_OK;
 }
 
@@ -772,20 +776,12 @@ seed_status seed_load_weights(seed_ctx* c, const seed_tensor* tensors, int32_t n
       return fail(SEED_ERR_ARG, std::string("tensor '") + t.name + "' has the wrong shape");
     which[i] = it->second;
   }
-  for (size_t i = 0; i < specs.size(); ++i)
-    if (!seen[i] && !c->loaded[i]) {
-      // tensors may be loaded over several calls; report the first one still missing at the end
-    }
   for (int i = 0; i < n; ++i) {
     seed_status st = load_one(c, tensors[i], specs[which[i]].name);
     if (st != SEED_OK) return st;
     c->loaded[which[i]] = true;
   }
   c->weights_ok = std::all_of(c->loaded.begin(), c->loaded.end(), [](bool b) { return b; });
-  if (!c->weights_ok) {
-    for (size_t i = 0; i < specs.size(); ++i)
-      if (!c->loaded[i]) return fail(SEED_ERR_ARG, "missing tensor '" + specs[i].name + "'");
-  }
   return SEED_OK;
 }
 
