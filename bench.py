@@ -1,0 +1,280 @@
+#!/usr/bin/env python3
+"""Benchmark of the SEED draft-verify decode loop on one MI355X.
+
+Workload: the 4B-scale model (36 layers = 34 encoder + 2 decoder, hidden 2560, GQA 32/8 x 128,
+SwiGLU 9728, vocab 151936, tied head), bf16 weights and KV cache, random-init N(0, 0.02),
+1024-token uniform-random prompt, draft length k = 4, batch 1. A step is one draft-verify round
+(k decoder-only draft steps, one verification of k+1 rows, acceptance and commit).
+
+Prints ONE JSON line. ``value`` is decoded tokens/s over the timed rounds (inputs resident in
+HBM, rounds replayed from a HIP graph). Also reported: verify- and draft-step latency and
+algorithmic HBM GB/s, throughput at forced acceptance lengths 0..k and for plain greedy
+decoding, per-kernel HIP-event timings, the roofline entry of the dominant kernel, and the CPU
+oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2609_36590_amd import binding, synth  # noqa: E402
+
+METRIC = "decoded tokens/sec at batch 1 (4B-scale, k=4); verify/draft step HBM GB/s"
+PEAK_HBM = 8.0e12   # MI355X HBM3E, bytes/s
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+# ------------------------------------------------------------------------------------------
+# algorithmic bytes
+# ------------------------------------------------------------------------------------------
+def kernel_bytes(cfg, op, M, L):
+    """Algorithmic HBM bytes of one launch: weights + activations in/out (+ KV for attention).
+    M rows; L = KV positions each row sees (mean); bf16 weights/KV, fp32 activations."""
+    H, QD, KVD, F, V = cfg.hidden, cfg.q_dim, cfg.kv_dim, cfg.ffn, cfg.vocab
+    es = 2 if cfg.dtype == "bf16" else 4
+    if op == binding.OP_QKV:
+        return (QD + 2 * KVD) * H * es + M * H * 4 + M * QD * 4 + M * 2 * KVD * es
+    if op == binding.OP_O:
+        return H * QD * es + M * QD * 4 + M * H * 8
+    if op == binding.OP_GATEUP:
+        return 2 * F * H * es + M * H * 4 + M * F * 4
+    if op == binding.OP_DOWN:
+        return H * F * es + M * F * 4 + M * H * 8
+    if op == binding.OP_HEAD:
+        return V * H * es + M * H * 4
+    if op == binding.OP_ATTN:
+        return L * 2 * KVD * es + M * QD * 4
+    return 0
+
+
+def step_bytes(cfg, M, L, layers):
+    per_layer = sum(kernel_bytes(cfg, op, M, L) for op in
+                    (binding.OP_QKV, binding.OP_ATTN, binding.OP_O, binding.OP_GATEUP, binding.OP_DOWN))
+    return layers * per_layer + kernel_bytes(cfg, binding.OP_HEAD, M, L)
+
+
+# ------------------------------------------------------------------------------------------
+# CPU oracle baseline
+# ------------------------------------------------------------------------------------------
+def cpu_baseline(cfg, weights, prompt, k, rounds):
+    from oracle import model as om
+    from oracle import seed as os_
+
+    cores = len(os.sched_getaffinity(0))
+    log(f"[cpu] widening weights to fp32 ({cores} host cores)")
+    model = om.Model(cfg, synth.weights_as_f32(cfg, weights), np.float32)
+    log("[cpu] oracle prefill (untimed)")
+    st = os_.prefill(model, prompt, len(prompt) + (k + 1) * rounds + 2)
+    log(f"[cpu] timing {rounds} oracle rounds")
+    t0 = time.perf_counter()
+    before = st.t
+    for _ in range(rounds):
+        d, _ = os_.draft(st, k)
+        n, b = os_.accept(d, os_.verify(st, d))
+        os_.commit(st, d, n, b)
+    dt = time.perf_counter() - t0
+    return {"value": (st.t - before) / dt, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": f"{rounds} rounds of Algorithm 2 (k={k}) on the same model and 1024-token prompt "
+                      f"after an untimed oracle prefill; {dt:.1f} s, {st.t - before} tokens, "
+                      f"{dt / rounds * 1e3:.0f} ms per round"}
+
+
+# ------------------------------------------------------------------------------------------
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200, help="timed draft-verify rounds")
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--k", type=int, default=4)
+    ap.add_argument("--config", default=synth.C3_4B.name, choices=sorted(synth.CONFIGS))
+    ap.add_argument("--cpu-rounds", type=int, default=2)
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-sweep", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        sys.exit(2)
+
+    import torch
+
+    cfg = synth.CONFIGS[args.config]
+    k = args.k
+    t_start = time.perf_counter()
+    log(f"[bench] generating weights for {cfg.name}")
+    weights = synth.make_weights(cfg)
+    prompt = synth.make_prompts(cfg)[0]
+    P = len(prompt)
+    gen = cfg.gen_len
+    max_ctx = P + max(gen + 2 * 6 + 2, (args.warmup + args.steps) * (k + 1) + k + 2)
+    log(f"[bench] weights ready in {time.perf_counter() - t_start:.1f}s; creating decoder (max_ctx={max_ctx})")
+    dec = binding.Decoder(cfg, max_batch=1, max_ctx=max_ctx, max_draft=6)
+    dec.load_weights(weights)
+    log(f"[bench] weights on device: {dec.bytes['weights'] / 1e9:.2f} GB")
+    ctx = dec.ctx
+    stream = dec.stream
+
+    def sync():
+        stream.synchronize()
+
+    # ---------------- timed rounds (graph replay) ----------------
+    dec.prefill([prompt])
+    binding.seed_rounds(ctx, k, args.warmup, True)
+    sync()
+    t_before = len(dec.tokens(0))
+    sync()
+    t0 = time.perf_counter()
+    binding.seed_rounds(ctx, k, args.steps, True)
+    sync()
+    t1 = time.perf_counter()
+    t_after = len(dec.tokens(0))
+    elapsed = t1 - t0
+    tokens = t_after - t_before
+    value = tokens / elapsed
+    log(f"[bench] graph: {args.steps} rounds, {tokens} tokens in {elapsed * 1e3:.1f} ms -> {value:.1f} tok/s")
+
+    # ---------------- same rounds, eager, with per-kernel HIP events ----------------
+    dec.prefill([prompt])
+    binding.seed_rounds(ctx, k, args.warmup, False)
+    sync()
+    kinds = []
+    for phase, M, layers in ((binding.PHASE_VERIFY, k + 1, cfg.n_layers), (binding.PHASE_DRAFT, 1, cfg.n_dec_layers)):
+        for op in (binding.OP_QKV, binding.OP_ATTN, binding.OP_COMBINE, binding.OP_O, binding.OP_GATEUP,
+                   binding.OP_DOWN, binding.OP_HEAD, binding.OP_HEAD_ARGMAX, binding.OP_SETUP, binding.OP_ACCEPT):
+            if phase == binding.PHASE_DRAFT and op == binding.OP_ACCEPT:
+                continue
+            kinds.append((phase, op, M, layers))
+    names = {binding.OP_SETUP: "setup", binding.OP_QKV: "qkv", binding.OP_ATTN: "attn", binding.OP_COMBINE: "combine",
+             binding.OP_O: "o", binding.OP_GATEUP: "gateup", binding.OP_DOWN: "down", binding.OP_HEAD: "head",
+             binding.OP_ACCEPT: "accept", binding.OP_HEAD_ARGMAX: "argmax"}
+    per_kernel = {}
+    probe_rounds = 4
+    for phase, op, M, layers in kinds:
+        dec.prefill([prompt])
+        binding.seed_rounds(ctx, k, 2, False)
+        binding.seed_kernel_timing(ctx, binding.kernel_id(phase, op), True)
+        binding.seed_rounds(ctx, k, probe_rounds, False)
+        n, ms = binding.seed_kernel_timing_read(ctx)
+        binding.seed_kernel_timing(ctx, 0, False)
+        if n == 0:
+            continue
+        L_here = len(dec.tokens(0)) - probe_rounds // 2
+        name = ("verify_" if phase == binding.PHASE_VERIFY else "draft_") + names[op]
+        avg = ms / n
+        b = kernel_bytes(cfg, op, M, L_here)
+        per_kernel[name] = {"launches_per_round": n / probe_rounds, "avg_us": avg * 1e3,
+                            "us_per_round": avg * 1e3 * n / probe_rounds,
+                            "alg_bytes": b, "gbps": (b / (avg * 1e-3) / 1e9) if b else None}
+    dominant = max(per_kernel, key=lambda kk: per_kernel[kk]["us_per_round"])
+    dom_phase = binding.PHASE_VERIFY if dominant.startswith("verify_") else binding.PHASE_DRAFT
+    dom_op = {v: kk for kk, v in names.items()}[dominant.split("_", 1)[1]]
+    dom_M = k + 1 if dom_phase == binding.PHASE_VERIFY else 1
+    log(f"[bench] dominant kernel: {dominant} ({per_kernel[dominant]['us_per_round']:.0f} us/round)")
+
+    # timed region of K eager rounds with HIP events around every launch of the dominant kernel
+    dec.prefill([prompt])
+    binding.seed_rounds(ctx, k, args.warmup, False)
+    sync()
+    binding.seed_kernel_timing(ctx, binding.kernel_id(dom_phase, dom_op), True)
+    tb = len(dec.tokens(0))
+    sync()
+    e0 = time.perf_counter()
+    binding.seed_rounds(ctx, k, args.steps, False)
+    sync()
+    e1 = time.perf_counter()
+    n_dom, ms_dom = binding.seed_kernel_timing_read(ctx)
+    binding.seed_kernel_timing(ctx, 0, False)
+    t_end = len(dec.tokens(0))
+    eager_value = (t_end - tb) / (e1 - e0)
+    L_mean = (tb + t_end) // 2
+    dom_avg_s = ms_dom / n_dom * 1e-3
+    dom_bytes = kernel_bytes(cfg, dom_op, dom_M, L_mean)
+    achieved = dom_bytes / dom_avg_s
+    roofline = {"bound": "hbm", "achieved": achieved / 1e9, "peak": PEAK_HBM / 1e9, "unit": "GB/s",
+                "frac": achieved / PEAK_HBM, "traffic": None, "kernel": dominant,
+                "launches": n_dom, "avg_us": dom_avg_s * 1e6, "alg_bytes_per_launch": dom_bytes}
+
+    # ---------------- verify / draft step latency ----------------
+    dec.prefill([prompt])
+    ver_ms, dr_ms = [], []
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    for _ in range(10):
+        ev[0].record(stream)
+        d, _ = dec.draft(k)
+        ev[1].record(stream)
+        dec.verify(k)
+        ev[2].record(stream)
+        sync()
+        dr_ms.append(ev[0].elapsed_time(ev[1]) / k)
+        ver_ms.append(ev[1].elapsed_time(ev[2]))
+    verify_ms = statistics.median(ver_ms)
+    draft_ms = statistics.median(dr_ms)
+    Lv = P + 5
+    verify_bytes = step_bytes(cfg, k + 1, Lv, cfg.n_layers)
+    draft_bytes = step_bytes(cfg, 1, Lv, cfg.n_dec_layers)
+
+    result = {
+        "metric": METRIC, "value": round(value, 2), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(elapsed / args.steps * 1e3, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": cfg.dtype, "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {cfg.n_layers} layers ({cfg.n_enc_layers} encoder + {cfg.n_dec_layers} "
+                               f"decoder), hidden {cfg.hidden}, GQA {cfg.n_heads}/{cfg.n_kv_heads}x{cfg.head_dim}, "
+                               f"SwiGLU {cfg.ffn}, vocab {cfg.vocab}, random-init N(0,0.02)",
+                   "prompt_len": P, "k": k, "batch": 1, "step": "one draft-verify round",
+                   "kv_positions": [t_before, t_after], "graph_replay": True},
+        "tokens_per_round": round(tokens / args.steps, 4),
+        "eager_value": round(eager_value, 2),
+        "verify_ms": round(verify_ms, 4), "draft_step_ms": round(draft_ms, 4),
+        "verify_gbps": round(verify_bytes / (verify_ms * 1e-3) / 1e9, 1),
+        "draft_gbps": round(draft_bytes / (draft_ms * 1e-3) / 1e9, 1),
+        "verify_frac": round(verify_bytes / (verify_ms * 1e-3) / PEAK_HBM, 4),
+        "draft_frac": round(draft_bytes / (draft_ms * 1e-3) / PEAK_HBM, 4),
+        "verify_alg_bytes": verify_bytes, "draft_alg_bytes": draft_bytes,
+        "per_kernel": {kk: {a: (round(b, 3) if isinstance(b, float) else b) for a, b in v.items()}
+                       for kk, v in per_kernel.items()},
+        "roofline": roofline,
+    }
+
+    # ---------------- forced acceptance sweep and plain greedy ----------------
+    if not args.no_sweep:
+        out0, _, st0 = dec.generate([prompt], 0, gen, use_graph=True)
+        trace = out0[0]
+        result["ar_tokens_per_s"] = round(gen / (st0["decode_ms"] * 1e-3), 2)
+        forced = {}
+        for a in range(k + 1):
+            out, cnt, st = dec.generate([prompt], k, gen, sim_accept=a, forced_trace=trace[None], use_graph=True,
+                                        log_cap=gen + 8)
+            ok = bool(np.array_equal(out[0], trace))
+            full = st["n_accept_log"][:, 0]
+            full_rounds = full[:max(0, len(full) - 2)]
+            forced[str(a)] = {"tokens_per_s": round(gen / (st["decode_ms"] * 1e-3), 2), "rounds": st["rounds"],
+                              "output_equals_greedy": ok, "n_accept_all_equal_a": bool(np.all(full_rounds == a))}
+            log(f"[bench] forced a={a}: {forced[str(a)]}")
+        result["forced_acceptance"] = forced
+        out4, _, st4 = dec.generate([prompt], k, gen, use_graph=True)
+        result["measured_acceptance"] = {"tokens_per_s": round(gen / (st4["decode_ms"] * 1e-3), 2),
+                                         "mean_accept": round(st4["accepted"] / max(1, st4["rounds"]), 4),
+                                         "output_equals_greedy": bool(np.array_equal(out4[0], trace))}
+
+    dec.close()
+    del dec
+    torch.cuda.empty_cache()
+    if not args.no_cpu:
+        result["cpu_baseline"] = cpu_baseline(cfg, weights, prompt, k, args.cpu_rounds)
+    log(f"[bench] total wall {time.perf_counter() - t_start:.1f}s")
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -129,7 +129,8 @@ typedef struct seed_stats {
 enum {
   SEED_PHASE_VERIFY = 0, SEED_PHASE_DRAFT = 1, SEED_PHASE_PREFILL = 2,
   SEED_OP_SETUP = 0, SEED_OP_QKV = 1, SEED_OP_ATTN = 2, SEED_OP_COMBINE = 3, SEED_OP_O = 4,
-  SEED_OP_GATEUP = 5, SEED_OP_DOWN = 6, SEED_OP_HEAD = 7, SEED_OP_ACCEPT = 8
+  SEED_OP_GATEUP = 5, SEED_OP_DOWN = 6, SEED_OP_HEAD = 7, SEED_OP_ACCEPT = 8,
+  SEED_OP_HEAD_ARGMAX = 9
 };
 
 /* Bytes the caller must provide for the weight arena, the KV pool and the workspace. */

@@ -17,7 +17,7 @@ from . import build as _build
 F32, BF16 = 0, 1
 
 PHASE_VERIFY, PHASE_DRAFT, PHASE_PREFILL = 0, 1, 2
-OP_SETUP, OP_QKV, OP_ATTN, OP_COMBINE, OP_O, OP_GATEUP, OP_DOWN, OP_HEAD, OP_ACCEPT = range(9)
+OP_SETUP, OP_QKV, OP_ATTN, OP_COMBINE, OP_O, OP_GATEUP, OP_DOWN, OP_HEAD, OP_ACCEPT, OP_HEAD_ARGMAX = range(10)
 
 
 def kernel_id(phase: int, op: int) -> int:
@@ -75,6 +75,10 @@ def load_library(path: str | None = None):
     path = path or lib_path()
     if not os.path.exists(path):
         raise FileNotFoundError(f"SEED HIP library not built: {path} (run __graft_entry__.build())")
+    # torch ships its own HIP runtime; load it first so the library binds to that same runtime
+    # (two HIP runtimes in one process do not share devices, streams or allocations)
+    import torch  # noqa: F401
+
     lib = ctypes.CDLL(path)
     sig = {
         "seed_arena_bytes": [ctypes.POINTER(SeedConfig), ctypes.POINTER(ctypes.c_size_t),

@@ -1,0 +1,300 @@
+// Paged split-KV attention on MFMA for the verify, draft and prefill passes.
+//
+// One workgroup = 4 waves = one group of 256 absolute positions (4 chunks of 64) for one
+// (sequence b, KV head h, row-block rb). The queries of a row-block (G query heads x RB rows,
+// <= 32) are the MFMA B operand. Per chunk, a wave computes S^T = K Q^T with the paged K block
+// rows as the A operand, masks positions later than each query's own, takes the chunk softmax in
+// base 2, and forms O^T = V^T P^T with the transposed V block as the A operand. All K/V loads of
+// the chunk are issued before any arithmetic, so a wave waits for one memory round trip.
+//
+// Merge order is a fixed function of absolute positions: chunks are merged left to right inside
+// the group (LDS), and the last workgroup of (b, h, rb) to finish merges the group partials left
+// to right. A chunk or group with no visible position is an exact identity of the merge, so a
+// query's result depends only on the positions it attends to, not on how many rows share the
+// pass (verify rows vs plain greedy decoding give bit-identical outputs).
+//
+// Position tile pt (16 positions) of chunk base P0, MFMA row r <-> position
+//   P0 + 32*(pt>>1) + 8*(r>>2) + (r&3) + 4*(pt&1),
+// so after S^T the lane group kg holds positions 8kg..8kg+7 of each 32-position step, which is
+// exactly the k-slot layout O^T needs for P^T: no cross-lane shuffle of P.
+#include "device_common.h"
+
+namespace seedk {
+
+static constexpr int ATT_CHUNK = 64;
+static constexpr int ATT_WAVES = 4;
+static constexpr int ATT_GROUP = ATT_CHUNK * ATT_WAVES;
+
+template <typename T, int HD>
+__global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
+  constexpr int DS = HD / 32;    // 32-dim steps of S^T
+  constexpr int DT = HD / 16;    // 16-dim tiles of O^T
+  constexpr int PS = HD + 4;     // floats per query vector in a group partial
+  __shared__ float s_o[ATT_WAVES - 1][32][HD];
+  __shared__ float s_ml[ATT_WAVES - 1][32][2];
+  __shared__ int s_last;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, tl = lane & 15, kg = lane >> 4;
+  const int g = blockIdx.x;
+  const int h = blockIdx.y % a.n_kv, rb = blockIdx.y / a.n_kv;
+  const int b = blockIdx.z;
+  const int r0 = rb * a.RB;
+  if (r0 >= a.R) return;
+  const int nr = min(a.RB, a.R - r0);
+  const int nqv = nr * a.G;
+  const int mrow0 = b * a.R + r0;
+  const int maxpos = a.row_pos[mrow0 + nr - 1];
+  const int n_groups = maxpos / ATT_GROUP + 1;
+  if (g >= n_groups) return;
+  const int QT = nqv > 16 ? 2 : 1;
+  const int qstride = a.n_heads * HD;
+  const int P0 = (g * ATT_WAVES + wave) * ATT_CHUNK;
+  const bool live = P0 <= maxpos;
+
+  const T* kvp = reinterpret_cast<const T*>(a.kv);
+  const int* btp = a.bt + b * a.bt_stride;
+  const size_t layer_base = (size_t)a.layer * a.n_blocks;
+
+  // ---- issue the chunk's K and V loads first ----
+  typename ET<T>::A kf[4][DS];
+  typename ET<T>::A vf[2][DT];
+  if (live) {
+#pragma unroll
+    for (int pt = 0; pt < 4; ++pt) {
+      const int pos = P0 + 32 * (pt >> 1) + 8 * (tl >> 2) + (tl & 3) + 4 * (pt & 1);
+      const int blk = btp[pos >> 4];
+      const T* kp = kvp + (((layer_base + blk) * 2 + 0) * a.n_kv + h) * 16 * HD + (pos & 15) * HD + kg * 8;
+#pragma unroll
+      for (int ds = 0; ds < DS; ++ds) kf[pt][ds] = ET<T>::load(kp + ds * 32);
+    }
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const int pos = P0 + 32 * s + 8 * kg;
+      const int blk = btp[pos >> 4];
+      const T* vp = kvp + (((layer_base + blk) * 2 + 1) * a.n_kv + h) * HD * 16 + tl * 16 + (pos & 15);
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) vf[s][dt] = ET<T>::load(vp + dt * 16 * 16);
+    }
+  }
+
+  // ---- queries: lane column qv = qt*16 + tl, k-slots d = ds*32 + kg*8 + j, scaled by log2(e)/sqrt(d)
+  typename ET<T>::B qf[2][DS];
+  int qpos[2];
+#pragma unroll
+  for (int qt = 0; qt < 2; ++qt) {
+    const int qv = qt * 16 + tl;
+    const bool ok = live && qt < QT && qv < nqv;
+    const int rl = qv / a.G, gq = qv - rl * a.G;
+    const int m = mrow0 + (ok ? rl : 0);
+    qpos[qt] = ok ? a.row_pos[m] : -1;
+    const float* qp = a.q + (size_t)m * qstride + (h * a.G + gq) * HD;
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds) {
+      float x[8];
+      if (ok) {
+        load8(qp + ds * 32 + kg * 8, x);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) x[j] *= a.scale_log2;
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) x[j] = 0.f;
+      }
+      qf[qt][ds] = ET<T>::split(x);
+    }
+  }
+
+  float m_c[2] = {NEG_INF, NEG_INF}, l_c[2] = {0.f, 0.f};
+  float o_c[2][DT][4];
+#pragma unroll
+  for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) o_c[qt][dt][i] = 0.f;
+
+  if (live) {
+    // ---- S^T = K Q^T ----
+    f32x4 sacc[4][2];
+#pragma unroll
+    for (int pt = 0; pt < 4; ++pt) {
+      sacc[pt][0] = f32x4{0.f, 0.f, 0.f, 0.f};
+      sacc[pt][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ds = 0; ds < DS; ++ds) {
+        ET<T>::mma(sacc[pt][0], kf[pt][ds], qf[0][ds]);
+        if (QT > 1) ET<T>::mma(sacc[pt][1], kf[pt][ds], qf[1][ds]);
+      }
+    }
+    // ---- mask + chunk softmax (base 2) ----
+    float p[2][4][4];
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+      float mx = NEG_INF;
+#pragma unroll
+      for (int pt = 0; pt < 4; ++pt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int pos = P0 + 32 * (pt >> 1) + 8 * kg + i + 4 * (pt & 1);
+          const float s = (pos <= qpos[qt]) ? sacc[pt][qt][i] : NEG_INF;
+          p[qt][pt][i] = s;
+          mx = fmaxf(mx, s);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      float sum = 0.f;
+#pragma unroll
+      for (int pt = 0; pt < 4; ++pt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float e = (mx == NEG_INF) ? 0.f : exp2f(p[qt][pt][i] - mx);
+          p[qt][pt][i] = e;
+          sum += e;
+        }
+      sum += __shfl_xor(sum, 16);
+      sum += __shfl_xor(sum, 32);
+      m_c[qt] = mx;
+      l_c[qt] = sum;
+    }
+    // ---- O^T = V^T P^T ----
+    typename ET<T>::B pf[2][2];
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        float x[8];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          x[j] = p[qt][2 * s][j];
+          x[j + 4] = p[qt][2 * s + 1][j];
+        }
+        pf[qt][s] = ET<T>::split(x);
+      }
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      f32x4 oacc0 = {0.f, 0.f, 0.f, 0.f}, oacc1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        ET<T>::mma(oacc0, vf[s][dt], pf[0][s]);
+        if (QT > 1) ET<T>::mma(oacc1, vf[s][dt], pf[1][s]);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        o_c[0][dt][i] = oacc0[i];
+        o_c[1][dt][i] = oacc1[i];
+      }
+    }
+  }
+
+  // ---- merge the group's 4 chunks left to right (wave 0 holds chunk 0) ----
+  if (wave > 0) {
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+      const int qv = qt * 16 + tl;
+      if (qt >= QT || qv >= nqv) continue;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+        *reinterpret_cast<float4*>(&s_o[wave - 1][qv][dt * 16 + 4 * kg]) =
+            make_float4(o_c[qt][dt][0], o_c[qt][dt][1], o_c[qt][dt][2], o_c[qt][dt][3]);
+      if (kg == 0) {
+        s_ml[wave - 1][qv][0] = m_c[qt];
+        s_ml[wave - 1][qv][1] = l_c[qt];
+      }
+    }
+  }
+  __syncthreads();
+  float* part = a.part + ((((size_t)(b * a.n_kv + h) * a.n_rb + rb) * a.n_groups_max + g) * 32) * PS;
+  if (wave == 0) {
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+      const int qv = qt * 16 + tl;
+      if (qt >= QT || qv >= nqv) continue;
+      for (int w = 0; w < ATT_WAVES - 1; ++w) {
+        float oc[DT * 4];
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+          const float4 v = *reinterpret_cast<const float4*>(&s_o[w][qv][dt * 16 + 4 * kg]);
+          oc[dt * 4 + 0] = v.x; oc[dt * 4 + 1] = v.y; oc[dt * 4 + 2] = v.z; oc[dt * 4 + 3] = v.w;
+        }
+        softmax_merge(m_c[qt], l_c[qt], &o_c[qt][0][0], s_ml[w][qv][0], s_ml[w][qv][1], oc, DT * 4);
+      }
+      if (n_groups == 1) {
+        // the only group: the combine below reduces to o / l for it (weight 1), so finish here
+        const int rl = qv / a.G, gq = qv - rl * a.G;
+        float* op = a.out + (size_t)(mrow0 + rl) * qstride + (h * a.G + gq) * HD;
+        const float l = l_c[qt];
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+          *reinterpret_cast<float4*>(op + dt * 16 + 4 * kg) =
+              make_float4(o_c[qt][dt][0] / l, o_c[qt][dt][1] / l, o_c[qt][dt][2] / l, o_c[qt][dt][3] / l);
+      } else {
+        float* pp = part + (size_t)qv * PS;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+          *reinterpret_cast<float4*>(pp + dt * 16 + 4 * kg) =
+              make_float4(o_c[qt][dt][0], o_c[qt][dt][1], o_c[qt][dt][2], o_c[qt][dt][3]);
+        if (kg == 0) {
+          pp[HD] = m_c[qt];
+          pp[HD + 1] = l_c[qt];
+        }
+      }
+    }
+  }
+  if (n_groups == 1) return;
+
+  // ---- the last group of (b, h, rb) to finish merges all group partials left to right ----
+  __threadfence();
+  __syncthreads();
+  int* cnt = a.cnt + (b * a.n_kv + h) * a.n_rb + rb;
+  if (threadIdx.x == 0) s_last = (atomicAdd(cnt, 1) == n_groups - 1);
+  __syncthreads();
+  if (!s_last) return;
+  __threadfence();
+  // Two passes over the group partials (g in increasing order): per query, the global max m*,
+  // the weights w_g = 2^(m_g - m*) and L = sum_g w_g l_g; then out = sum_g w_g o_g / L. A group
+  // that sees nothing has w_g = 0 exactly and adds exact zeros.
+  const float* part0 = a.part + ((((size_t)(b * a.n_kv + h) * a.n_rb + rb) * a.n_groups_max) * 32) * PS;
+  float* s_w = &s_o[0][0][0];                 // [n_groups][32] weights (n_groups <= 3*HD)
+  float* s_L = &s_ml[0][0][0];                // [32]
+  if (threadIdx.x < nqv) {
+    const int qv = threadIdx.x;
+    float mstar = NEG_INF;
+    for (int gi = 0; gi < n_groups; ++gi) mstar = fmaxf(mstar, part0[((size_t)gi * 32 + qv) * PS + HD]);
+    float L = 0.f;
+    for (int gi = 0; gi < n_groups; ++gi) {
+      const float* pp = part0 + ((size_t)gi * 32 + qv) * PS;
+      const float mg = pp[HD];
+      const float wg = (mg == NEG_INF) ? 0.f : exp2f(mg - mstar);
+      s_w[gi * 32 + qv] = wg;
+      L += wg * pp[HD + 1];
+    }
+    s_L[qv] = L;
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < nqv * HD; e += blockDim.x) {
+    const int qv = e / HD, d = e - qv * HD;
+    float o = 0.f;
+    int gi = 0;
+    for (; gi + 4 <= n_groups; gi += 4) {
+      float oo[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) oo[u] = part0[((size_t)(gi + u) * 32 + qv) * PS + d];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) o += s_w[(gi + u) * 32 + qv] * oo[u];
+    }
+    for (; gi < n_groups; ++gi) o += s_w[gi * 32 + qv] * part0[((size_t)gi * 32 + qv) * PS + d];
+    const int rl = qv / a.G, gq = qv - rl * a.G;
+    a.out[(size_t)(mrow0 + rl) * qstride + (h * a.G + gq) * HD + d] = o / s_L[qv];
+  }
+  if (threadIdx.x == 0) atomicExch(cnt, 0);
+}
+
+template <typename T>
+void launch_attention(const AttnArgs& a, hipStream_t s) {
+  const dim3 grid(a.n_groups_max, a.n_kv * a.n_rb, a.B);
+  if (a.head_dim == 128) hipLaunchKernelGGL((k_attention<T, 128>), grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL((k_attention<T, 64>), grid, dim3(256), 0, s, a);
+}
+
+template void launch_attention<uint16_t>(const AttnArgs&, hipStream_t);
+template void launch_attention<float>(const AttnArgs&, hipStream_t);
+
+}  // namespace seedk

@@ -30,14 +30,16 @@ struct LinArgs {
   int M;                  // activation rows in this pass
   int NT, KS;             // n-tiles per workgroup, K-splits per n-tile (waves = NT * KS)
   // input
-  const float* X;         // [M][ldx] fp32 activations
+  const float* X;         // [M][ldx] fp32 activations; PRO_NORM: x*g formed by the producer
   int ldx;
-  const float* gain;      // PRO_NORM: RMSNorm gain [K] (fp32)
-  const float* ssq;       // PRO_NORM: [M][nssq] partial sums of squares of X (per 16 features)
+  const float* ssq;       // PRO_NORM: [M][nssq] partial sums of squares of x (per 16 features)
   int nssq;
   float eps;
-  // EPI_RESID: h[m][n] += y, then ssq_out[m][n/16] = sum of squares of the 16 updated values
+  // EPI_RESID: h[m][n] += y, xg[m][n] = h[m][n] * gain_next[n] (input of the next RMSNorm
+  // consumer), ssq_out[m][n/16] = sum of squares of the 16 updated values
   float* h;
+  float* xg;
+  const float* gain_next;
   float* ssq_out;
   // EPI_SWIGLU: act[m][f] = silu(gate) * up, f = nt*8 + c
   float* act;
@@ -54,10 +56,9 @@ struct LinArgs {
   // EPI_HEAD
   float* logits;          // nullable: logits[m * ld_logits + n]
   long long ld_logits;
-  unsigned long long* keys;   // [M] running argmax keys (zero between launches)
-  unsigned int* counter;      // workgroup completion counter (zero between launches)
-  int* tok_out;               // argmax of row m is written to tok_out[m * tok_stride]
-  int tok_stride;
+  float* amax_val;        // per-workgroup argmax partials [M][amax_stride]
+  int* amax_idx;
+  int amax_stride;
 };
 
 // Arguments of the split-KV paged attention kernel and its combine step.
@@ -71,10 +72,10 @@ struct AttnArgs {
   int B, R;               // sequences, rows per sequence
   int n_heads, n_kv, head_dim, G;  // G = n_heads / n_kv
   int RB, n_rb;           // rows per row-block (G*RB <= 32), row-blocks per sequence
-  int chunk_groups;       // grid extent over chunk groups
-  int S;                  // chunks (of 64 positions) per group, merged left to right
+  int n_groups_max;       // grid extent over groups of 256 positions
   float scale_log2;       // log2(e) / sqrt(head_dim)
-  float* part;            // partials [B][n_kv][n_rb][chunk_groups][32][head_dim + 2]
+  float* part;            // group partials [B][n_kv][n_rb][n_groups_max][32][head_dim + 4]
+  int* cnt;               // [B][n_kv][n_rb] finished-group counters (zero between launches)
   float* out;             // [M][n_heads*head_dim]
 };
 
@@ -99,6 +100,8 @@ struct SetupArgs {
   int* row_seq;
   int* row_pos;
   float* h;               // [M][H]
+  float* xg;              // [M][H] h * gain (input of the pass's first RMSNorm consumer)
+  const float* gain;      // [H]
   float* ssq;             // [M][H/16]
 };
 
@@ -125,11 +128,14 @@ struct DevState {
 template <typename T>
 void launch_linear(const LinArgs& a, int prologue, int epilogue, bool valu, hipStream_t s);
 template <typename T>
-void launch_attention(const AttnArgs& a, bool flash, hipStream_t s);
-void launch_combine(const AttnArgs& a, hipStream_t s);
+void launch_attention(const AttnArgs& a, hipStream_t s);
 template <typename T>
 void launch_setup(const SetupArgs& a, hipStream_t s);
 void launch_accept(const DevState& st, int B, int k, hipStream_t s);
+// Reduce the head's per-workgroup argmax partials of M rows; row m's token goes to
+// tok_out[m * tok_stride] (lowest token id among equal maxima).
+void launch_argmax_finalize(const float* val, const int* idx, int stride, int n_parts, int M, int* tok_out,
+                            int tok_stride, hipStream_t s);
 template <typename T>
 void launch_pack(const void* src, void* dst, const int* dst_row, int rows, int K, hipStream_t s);
 void launch_to_f32(const void* src, int src_is_bf16, float* dst, long long n, hipStream_t s);

@@ -1,0 +1,169 @@
+// Row setup + embedding gather, acceptance/commit, and load-time helpers.
+#include "device_common.h"
+
+namespace seedk {
+
+// ---------------------------------------------------------------------------------------------
+// Row setup for a pass: pick each row's sequence, position and token (Algorithm 2: drafts feed
+// X_draft[i-1], verification feeds X_draft[0..d]), gather the raw embedding H^0 = W_in x from
+// the packed table into the fp32 residual stream, and write its per-16-feature sums of squares.
+// ---------------------------------------------------------------------------------------------
+template <typename T>
+__global__ void __launch_bounds__(256) k_setup(SetupArgs a) {
+  const int m = blockIdx.x;
+  __shared__ int s_tok;
+  if (threadIdx.x == 0) {
+    int b, pos, tok;
+    if (a.mode == SETUP_PREFILL) {
+      b = a.pf_seq;
+      pos = a.pf_pos0 + m;
+      tok = a.tokens[b * a.tstride + pos];
+    } else if (a.mode == SETUP_DRAFT) {
+      b = m;
+      pos = a.t[b] - 1 + (a.step - 1);
+      tok = a.drafts[b * a.dstride + a.step - 1];
+    } else {
+      b = m / a.R;
+      const int r = m - b * a.R;
+      pos = a.t[b] - 1 + r;
+      tok = a.drafts[b * a.dstride + r];
+      if (a.sim_accept >= 0 && r >= 1 && r <= a.sim_accept + 1) {
+        const int tr = a.trace[b * a.tstride + pos];
+        tok = (r <= a.sim_accept) ? tr : (tr + 1) % a.vocab;
+        a.drafts[b * a.dstride + r] = tok;
+      }
+    }
+    a.row_seq[m] = b;
+    a.row_pos[m] = pos;
+    s_tok = tok;
+  }
+  __syncthreads();
+  const int tok = s_tok;
+  const int KT = a.H >> 5;
+  const T* E = reinterpret_cast<const T*>(a.E);
+  const int nt = tok >> 4, rr = tok & 15;
+  for (int j = threadIdx.x; j < (a.H >> 4); j += blockDim.x) {
+    const int k0 = j * 16, kt = k0 >> 5, kg = (k0 >> 3) & 3;
+    const T* src = E + ((size_t)nt * KT + kt) * 512 + (rr + 16 * kg) * 8;
+    float v0[8], v1[8];
+    ET<T>::to_f32(ET<T>::load(src), v0);
+    ET<T>::to_f32(ET<T>::load(src + 128), v1);   // lane + 16 => next 8 features
+    float* hp = a.h + (size_t)m * a.H + k0;
+    float* xgp = a.xg + (size_t)m * a.H + k0;
+    const float* gp = a.gain + k0;
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) { hp[i] = v0[i]; xgp[i] = v0[i] * gp[i]; s += v0[i] * v0[i]; }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) { hp[8 + i] = v1[i]; xgp[8 + i] = v1[i] * gp[8 + i]; s += v1[i] * v1[i]; }
+    a.ssq[(size_t)m * (a.H >> 4) + j] = s;
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
+// Greedy acceptance and commit (Algorithm 2): n_accept = longest prefix with g_{i-1} ==
+// X_draft[i], append X_draft[1..n_accept] and the bonus token g_{n_accept}, advance t. The
+// cache needs no work: positions >= the new t-1 are simply treated as invalid.
+// ---------------------------------------------------------------------------------------------
+__global__ void __launch_bounds__(64) k_accept(DevState st, int B, int k) {
+  __shared__ int s_round;
+  if (threadIdx.x == 0) s_round = *st.rounds;
+  __syncthreads();
+  const int b = threadIdx.x;
+  if (b < B) {
+    int logv = -1;
+    if (st.active[b]) {
+      const int R = k + 1;
+      int t = st.t[b];
+      int* dr = st.drafts + b * st.dstride;
+      const int* gv = st.vtok + b * R;
+      int n = 0;
+      while (n < k && gv[n] == dr[n + 1]) ++n;
+      const int bonus = gv[n];
+      int* tk = st.tokens + b * st.tstride;
+      int stop = 0, ncommit = n + 1;
+      for (int i = 0; i < n + 1; ++i) {
+        const int tv = (i < n) ? dr[i + 1] : bonus;
+        tk[t + i] = tv;
+        if (st.eos >= 0 && tv == st.eos) { ncommit = i + 1; stop = 1; break; }
+      }
+      t += ncommit;
+      st.t[b] = t;
+      dr[0] = tk[t - 1];
+      st.nacc[b] = n;
+      st.bonus[b] = bonus;
+      if (stop || t >= st.limit[b]) st.active[b] = 0;
+      atomicAdd(reinterpret_cast<unsigned long long*>(&st.counters[0]), (unsigned long long)k);
+      atomicAdd(reinterpret_cast<unsigned long long*>(&st.counters[1]), (unsigned long long)n);
+      logv = n;
+    }
+    if (s_round < st.log_cap) st.nacc_log[(size_t)s_round * B + b] = logv;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) *st.rounds = s_round + 1;
+}
+
+// ---------------------------------------------------------------------------------------------
+// Load-time helpers.
+// ---------------------------------------------------------------------------------------------
+template <typename T>
+__global__ void k_pack(const T* src, T* dst, const int* dst_row, int rows, int K) {
+  const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  const int groups = K >> 3;
+  if (gid >= (long long)rows * groups) return;
+  const int r = (int)(gid / groups), kq = (int)(gid - (long long)r * groups);
+  const int k = kq * 8, n = dst_row[r];
+  const int KT = K >> 5, nt = n >> 4, rr = n & 15, kt = k >> 5, kg = (k >> 3) & 3;
+  const T* s = src + (size_t)r * K + k;
+  T* d = dst + ((size_t)nt * KT + kt) * 512 + (rr + 16 * kg) * 8;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) d[j] = s[j];
+}
+
+__global__ void k_to_f32(const void* src, int is_bf16, float* dst, long long n) {
+  const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  dst[i] = is_bf16 ? bf2f(reinterpret_cast<const uint16_t*>(src)[i]) : reinterpret_cast<const float*>(src)[i];
+}
+
+__global__ void k_fill_u32(uint32_t* dst, uint32_t v, long long n) {
+  for (long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (long long)gridDim.x * blockDim.x)
+    dst[i] = v;
+}
+
+// ---------------------------------------------------------------------------------------------
+// Launchers.
+// ---------------------------------------------------------------------------------------------
+template <typename T>
+void launch_setup(const SetupArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL((k_setup<T>), dim3(a.M), dim3(256), 0, s, a);
+}
+
+void launch_accept(const DevState& st, int B, int k, hipStream_t s) {
+  hipLaunchKernelGGL(k_accept, dim3(1), dim3(64), 0, s, st, B, k);
+}
+
+template <typename T>
+void launch_pack(const void* src, void* dst, const int* dst_row, int rows, int K, hipStream_t s) {
+  const long long n = (long long)rows * (K >> 3);
+  hipLaunchKernelGGL((k_pack<T>), dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s,
+                     reinterpret_cast<const T*>(src), reinterpret_cast<T*>(dst), dst_row, rows, K);
+}
+
+void launch_to_f32(const void* src, int src_is_bf16, float* dst, long long n, hipStream_t s) {
+  hipLaunchKernelGGL(k_to_f32, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, src, src_is_bf16, dst, n);
+}
+
+void launch_fill_u32(void* dst, unsigned value, long long n_words, hipStream_t s) {
+  long long blocks = (n_words + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(k_fill_u32, dim3((unsigned)blocks), dim3(256), 0, s, reinterpret_cast<uint32_t*>(dst), value, n_words);
+}
+
+template void launch_setup<uint16_t>(const SetupArgs&, hipStream_t);
+template void launch_setup<float>(const SetupArgs&, hipStream_t);
+template void launch_pack<uint16_t>(const void*, void*, const int*, int, int, hipStream_t);
+template void launch_pack<float>(const void*, void*, const int*, int, int, hipStream_t);
+
+}  // namespace seedk

@@ -39,7 +39,7 @@ seed_status fail(seed_status s, const std::string& msg) {
 
 constexpr int PREFILL_ROWS = 48;   // rows per prefill pass (3 MFMA token tiles)
 constexpr int MAX_ROWS = 64;       // rows per decode pass: max_batch * (max_draft + 1)
-constexpr int CHUNK = 64;          // attention chunk (positions)
+constexpr int GROUP = 256;         // attention workgroup span (positions): 4 chunks of 64
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 int cdiv(int a, int b) { return (a + b - 1) / b; }
@@ -48,14 +48,14 @@ struct Plan {
   seed_config cfg;
   int esize = 2;
   int H, NQ, NKV, HD, F, V, L, LD, QD, KVD, G;
-  int RB, n_rb_max, max_rows, bt_stride, blocks_per_seq, n_blocks, chunk_groups, S;
+  int RB, n_rb_max, max_rows, bt_stride, blocks_per_seq, n_blocks, n_groups_max;
   int dstride, tstride, log_cap;
   // weight arena
   size_t w_embed, w_final_norm, w_rope_cos, w_rope_sin, w_total;
   std::vector<size_t> w_attn_norm, w_mlp_norm, w_qkv, w_o, w_gu, w_down;
   size_t kv_total;
   // workspace
-  size_t o_h, o_ssq, o_q, o_attn, o_act, o_part, o_row_seq, o_row_pos, o_keys, o_counter, o_vtok;
+  size_t o_h, o_xg, o_ssq, o_q, o_attn, o_act, o_part, o_cnt, o_row_seq, o_row_pos, o_amax_val, o_amax_idx, o_vtok;
   size_t o_t, o_len, o_limit, o_active, o_nacc, o_bonus, o_rounds, o_counters, o_drafts, o_tokens,
       o_trace, o_log, o_bt, o_scratch, ws_total;
 };
@@ -78,7 +78,9 @@ seed_status validate(const seed_config* c) {
   if (c->max_draft < 0 || c->max_draft > 15) return fail(SEED_ERR_UNSUPPORTED, "max_draft must be in [0, 15]");
   if (c->max_batch * (c->max_draft + 1) > MAX_ROWS)
     return fail(SEED_ERR_UNSUPPORTED, "max_batch * (max_draft + 1) must be at most 64");
-  if (c->max_ctx < 2 || c->max_ctx > (1 << 22)) return fail(SEED_ERR_ARG, "max_ctx must be in [2, 2^22]");
+  if (c->max_ctx < 2) return fail(SEED_ERR_ARG, "max_ctx must be at least 2");
+  if (c->max_ctx > 3 * c->head_dim * GROUP)   // the attention combine keeps 32 weights per group in LDS
+    return fail(SEED_ERR_UNSUPPORTED, "max_ctx must be at most 768 * head_dim");
   if (!(c->rope_base > 0.f) || !(c->rms_eps >= 0.f)) return fail(SEED_ERR_ARG, "rope_base must be > 0 and rms_eps >= 0");
   return SEED_OK;
 }
@@ -91,13 +93,13 @@ Plan make_plan(const seed_config& c) {
   p.L = c.n_layers; p.LD = c.n_layers - c.n_dec_layers;
   p.QD = p.NQ * p.HD; p.KVD = p.NKV * p.HD; p.G = p.NQ / p.NKV;
   p.RB = std::max(1, 32 / p.G);
-  p.n_rb_max = cdiv(c.max_draft + 1, p.RB);
+  p.n_rb_max = cdiv(std::max(c.max_draft + 1, PREFILL_ROWS), p.RB);
   p.max_rows = std::max(PREFILL_ROWS, c.max_batch * (c.max_draft + 1));
   p.blocks_per_seq = cdiv(c.max_ctx, 16);
-  p.bt_stride = cdiv(p.blocks_per_seq, CHUNK / 16) * (CHUNK / 16);   // whole chunks, padded with block 0
+  p.bt_stride = cdiv(p.blocks_per_seq, GROUP / 16) * (GROUP / 16);   // whole groups, padded with block 0
   p.n_blocks = c.max_batch * p.blocks_per_seq + 1;                  // block 0 = permanent zero block
-  p.S = 1;
-  p.chunk_groups = cdiv(p.bt_stride * 16 / CHUNK, p.S);
+
+  p.n_groups_max = p.bt_stride * 16 / GROUP;
   p.dstride = c.max_draft + 1;
   p.tstride = c.max_ctx;
   p.log_cap = c.max_ctx;
@@ -124,15 +126,17 @@ Plan make_plan(const seed_config& c) {
   o = 0;
   const size_t R = p.max_rows, B = c.max_batch;
   p.o_h = take(R * p.H * 4);
+  p.o_xg = take(R * p.H * 4);
   p.o_ssq = take(R * (p.H / 16) * 4);
   p.o_q = take(R * p.QD * 4);
   p.o_attn = take(R * p.QD * 4);
   p.o_act = take(R * p.F * 4);
-  p.o_part = take(B * p.NKV * p.n_rb_max * (size_t)p.chunk_groups * 32 * (p.HD + 4) * 4);
+  p.o_part = take(B * p.NKV * p.n_rb_max * (size_t)p.n_groups_max * 32 * (p.HD + 4) * 4);
+  p.o_cnt = take(B * p.NKV * p.n_rb_max * 4);
   p.o_row_seq = take(R * 4);
   p.o_row_pos = take(R * 4);
-  p.o_keys = take(R * 8);
-  p.o_counter = take(64);
+  p.o_amax_val = take(R * (size_t)(p.V / 16) * 4);
+  p.o_amax_idx = take(R * (size_t)(p.V / 16) * 4);
   p.o_vtok = take(R * 4);
   p.o_t = take(B * 4);
   p.o_len = take(B * 4);
@@ -231,10 +235,20 @@ void timed(seed_ctx* c, int phase, int op, bool capturing, F&& fn) {
 // ---------------------------------------------------------------------------------------------
 // launch helpers
 // ---------------------------------------------------------------------------------------------
-void tile_policy(int N, int K, int& NT, int& KS) {
+// Waves per workgroup and how they split the work; a function of the weight shape only, so a
+// row's reduction order never depends on how many rows share the pass.
+void tile_policy(int N, int K, bool head, int& NT, int& KS) {
   (void)N;
   const int KT = K / 32;
-  KS = std::min(16, std::max(1, KT / 4));
+  if (head) {               // huge N: one n-tile per wave over the full K, 16 n-tiles per workgroup
+    KS = 1;
+    NT = 16;
+    return;
+  }
+#ifndef SEED_KT_PER_WAVE
+#define SEED_KT_PER_WAVE 4
+#endif
+  KS = std::min(16, std::max(1, KT / SEED_KT_PER_WAVE));
   NT = std::max(1, 16 / KS);
 }
 
@@ -269,6 +283,7 @@ LinArgs lin_base(seed_ctx* c, int M) {
   a.nssq = p.H / 16;
   a.eps = p.cfg.rms_eps;
   a.h = c->ws<float>(p.o_h);
+  a.xg = c->ws<float>(p.o_xg);
   a.ssq_out = c->ws<float>(p.o_ssq);
   a.act = c->ws<float>(p.o_act);
   a.q = c->ws<float>(p.o_q);
@@ -283,20 +298,21 @@ LinArgs lin_base(seed_ctx* c, int M) {
   a.n_heads = p.NQ;
   a.n_kv = p.NKV;
   a.head_dim = p.HD;
-  a.keys = c->ws<unsigned long long>(p.o_keys);
-  a.counter = c->ws<unsigned int>(p.o_counter);
+  a.amax_val = c->ws<float>(p.o_amax_val);
+  a.amax_idx = c->ws<int>(p.o_amax_idx);
+  a.amax_stride = p.V / 16;
   return a;
 }
 
 template <typename T>
 void linear(seed_ctx* c, LinArgs a, int pro, int epi, bool valu, int phase, int op, bool cap) {
-  tile_policy(a.N, a.K, a.NT, a.KS);
+  tile_policy(a.N, a.K, epi == EPI_HEAD, a.NT, a.KS);
   timed(c, phase, op, cap, [&] { launch_linear<T>(a, pro, epi, valu, c->s); });
 }
 
 // Layers [l0, l1) over M rows (B sequences x R rows each, consecutive positions per sequence).
 template <typename T>
-void run_layers(seed_ctx* c, int M, int B, int R, int l0, int l1, bool valu, int phase, bool flash,
+void run_layers(seed_ctx* c, int M, int B, int R, int l0, int l1, bool valu, int phase,
                 const int* bt_override, bool cap) {
   const Plan& p = c->p;
   float* h = c->ws<float>(p.o_h);
@@ -305,7 +321,7 @@ void run_layers(seed_ctx* c, int M, int B, int R, int l0, int l1, bool valu, int
     a.layer = li;
     // QKV + RoPE + KV write
     a.W = c->W + p.w_qkv[li]; a.N = p.QD + 2 * p.KVD; a.K = p.H;
-    a.X = h; a.ldx = p.H; a.gain = c->wf(p.w_attn_norm[li]);
+    a.X = c->ws<float>(p.o_xg); a.ldx = p.H;
     linear<T>(c, a, PRO_NORM, EPI_QKV, valu, phase, SEED_OP_QKV, cap);
     // attention
     AttnArgs at;
@@ -320,26 +336,27 @@ void run_layers(seed_ctx* c, int M, int B, int R, int l0, int l1, bool valu, int
     at.B = B; at.R = R;
     at.n_heads = p.NQ; at.n_kv = p.NKV; at.head_dim = p.HD; at.G = p.G;
     at.RB = p.RB; at.n_rb = cdiv(R, p.RB);
-    at.chunk_groups = p.chunk_groups; at.S = p.S;
+    at.n_groups_max = p.n_groups_max;
+    at.cnt = c->ws<int>(p.o_cnt);
     at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)p.HD));
     at.part = c->ws<float>(p.o_part);
     at.out = c->ws<float>(p.o_attn);
-    timed(c, phase, SEED_OP_ATTN, cap, [&] { launch_attention<T>(at, flash, c->s); });
-    if (!flash) timed(c, phase, SEED_OP_COMBINE, cap, [&] { launch_combine(at, c->s); });
+    timed(c, phase, SEED_OP_ATTN, cap, [&] { launch_attention<T>(at, c->s); });
     // O + residual
     a = lin_base(c, M);
     a.W = c->W + p.w_o[li]; a.N = p.H; a.K = p.QD;
-    a.X = c->ws<float>(p.o_attn); a.ldx = p.QD;
+    a.X = c->ws<float>(p.o_attn); a.ldx = p.QD; a.gain_next = c->wf(p.w_mlp_norm[li]);
     linear<T>(c, a, PRO_PLAIN, EPI_RESID, valu, phase, SEED_OP_O, cap);
     // gate/up + SwiGLU
     a = lin_base(c, M);
     a.W = c->W + p.w_gu[li]; a.N = 2 * p.F; a.K = p.H;
-    a.X = h; a.ldx = p.H; a.gain = c->wf(p.w_mlp_norm[li]);
+    a.X = c->ws<float>(p.o_xg); a.ldx = p.H;
     linear<T>(c, a, PRO_NORM, EPI_SWIGLU, valu, phase, SEED_OP_GATEUP, cap);
     // down + residual
     a = lin_base(c, M);
     a.W = c->W + p.w_down[li]; a.N = p.H; a.K = p.F;
     a.X = c->ws<float>(p.o_act); a.ldx = p.F;
+    a.gain_next = c->wf(li + 1 < p.L ? p.w_attn_norm[li + 1] : p.w_final_norm);
     linear<T>(c, a, PRO_PLAIN, EPI_RESID, valu, phase, SEED_OP_DOWN, cap);
   }
 }
@@ -350,13 +367,20 @@ void run_head(seed_ctx* c, int M, bool valu, int* tok_out, int tok_stride, float
   const Plan& p = c->p;
   LinArgs a = lin_base(c, M);
   a.W = c->W + p.w_embed; a.N = p.V; a.K = p.H;
-  a.X = c->ws<float>(p.o_h); a.ldx = p.H; a.gain = c->wf(p.w_final_norm);
+  a.X = c->ws<float>(p.o_xg); a.ldx = p.H;
   a.logits = logits; a.ld_logits = ld;
-  a.tok_out = tok_out; a.tok_stride = tok_stride;
   linear<T>(c, a, PRO_NORM, EPI_HEAD, valu, phase, SEED_OP_HEAD, cap);
+  int NT, KS;
+  tile_policy(a.N, a.K, true, NT, KS);
+  const int parts = cdiv(p.V / 16, NT);
+  timed(c, phase, SEED_OP_HEAD_ARGMAX, cap, [&] {
+    launch_argmax_finalize(a.amax_val, a.amax_idx, a.amax_stride, parts, M, tok_out, tok_stride, c->s);
+  });
 }
 
-SetupArgs setup_base(seed_ctx* c) {
+// Setup for a pass whose first layer is l0 (its RMSNorm gain forms x*g; the head's gain when the
+// pass has no layers).
+SetupArgs setup_base(seed_ctx* c, int l0) {
   const Plan& p = c->p;
   SetupArgs s;
   std::memset(&s, 0, sizeof(s));
@@ -373,6 +397,8 @@ SetupArgs setup_base(seed_ctx* c) {
   s.row_seq = c->ws<int>(p.o_row_seq);
   s.row_pos = c->ws<int>(p.o_row_pos);
   s.h = c->ws<float>(p.o_h);
+  s.xg = c->ws<float>(p.o_xg);
+  s.gain = c->wf(l0 < p.L ? p.w_attn_norm[l0] : p.w_final_norm);
   s.ssq = c->ws<float>(p.o_ssq);
   return s;
 }
@@ -384,10 +410,10 @@ void enqueue_draft(seed_ctx* c, int k, float* logits, bool cap) {
   const int B = c->B;
   const bool valu = (B == 1);
   for (int i = 1; i <= k; ++i) {
-    SetupArgs s = setup_base(c);
+    SetupArgs s = setup_base(c, p.LD);
     s.mode = SETUP_DRAFT; s.M = B; s.R = 1; s.step = i;
     timed(c, SEED_PHASE_DRAFT, SEED_OP_SETUP, cap, [&] { launch_setup<T>(s, c->s); });
-    run_layers<T>(c, B, B, 1, p.LD, p.L, valu, SEED_PHASE_DRAFT, false, nullptr, cap);
+    run_layers<T>(c, B, B, 1, p.LD, p.L, valu, SEED_PHASE_DRAFT, nullptr, cap);
     run_head<T>(c, B, valu, c->ws<int>(p.o_drafts) + i, p.dstride,
                 logits ? logits + (size_t)(i - 1) * p.V : nullptr, (long long)k * p.V, SEED_PHASE_DRAFT, cap);
   }
@@ -398,10 +424,10 @@ template <typename T>
 void enqueue_verify(seed_ctx* c, int k, int sim_accept, float* logits, bool cap) {
   const Plan& p = c->p;
   const int B = c->B, R = k + 1, M = B * R;
-  SetupArgs s = setup_base(c);
+  SetupArgs s = setup_base(c, 0);
   s.mode = SETUP_VERIFY; s.M = M; s.R = R; s.sim_accept = sim_accept;
   timed(c, SEED_PHASE_VERIFY, SEED_OP_SETUP, cap, [&] { launch_setup<T>(s, c->s); });
-  run_layers<T>(c, M, B, R, 0, p.L, false, SEED_PHASE_VERIFY, false, nullptr, cap);
+  run_layers<T>(c, M, B, R, 0, p.L, false, SEED_PHASE_VERIFY, nullptr, cap);
   run_head<T>(c, M, false, c->ws<int>(p.o_vtok), 1, logits, (long long)p.V, SEED_PHASE_VERIFY, cap);
   DevState st = dev_state(c);
   timed(c, SEED_PHASE_VERIFY, SEED_OP_ACCEPT, cap, [&] { launch_accept(st, B, k, c->s); });
@@ -613,10 +639,10 @@ seed_status do_prefill(seed_ctx* c, const std::vector<int>& tokens_packed) {
     const int n = c->lens[b] - 1;
     for (int s0 = 0; s0 < n; s0 += PREFILL_ROWS) {
       const int M = std::min(PREFILL_ROWS, n - s0);
-      SetupArgs s = setup_base(c);
+      SetupArgs s = setup_base(c, 0);
       s.mode = SETUP_PREFILL; s.M = M; s.R = M; s.pf_seq = b; s.pf_pos0 = s0;
       timed(c, SEED_PHASE_PREFILL, SEED_OP_SETUP, false, [&] { launch_setup<T>(s, c->s); });
-      run_layers<T>(c, M, 1, M, 0, p.L, false, SEED_PHASE_PREFILL, true,
+      run_layers<T>(c, M, 1, M, 0, p.L, false, SEED_PHASE_PREFILL,
                     c->ws<int>(p.o_bt) + (size_t)b * p.bt_stride, false);
     }
   }

@@ -1,0 +1,207 @@
+"""GPU tests of the runtime around the kernels: batches with ragged prompts and acceptance,
+graph replay, forced acceptance, EOS, long contexts that span several attention groups, the
+step-wise calls, and the error paths of the C ABI (state is left unchanged after an error)."""
+import numpy as np
+import pytest
+
+from gpu_common import decoder, oracle_model, say, top2_gap
+from oracle import seed as os_
+from paper_2609_36590_amd import binding, synth
+
+pytestmark = pytest.mark.gpu
+
+BF16_TINY = synth.C1_TINY.replace(name="tiny-bf16", dtype=synth.BF16)
+
+
+@pytest.fixture(scope="module")
+def batch_dec():
+    cfg = BF16_TINY
+    w = synth.make_weights(cfg, seed=3, enc_out_scale=0.1)
+    dec = decoder(cfg, w, max_batch=4, max_ctx=600, max_draft=6)
+    yield cfg, w, dec
+    dec.close()
+
+
+def _prompts(cfg, lens, seed=7):
+    rng = np.random.default_rng(seed)
+    return [rng.integers(0, cfg.vocab, size=n).astype(np.int32) for n in lens]
+
+
+def test_batch_equals_each_sequence_alone(batch_dec):
+    cfg, w, dec = batch_dec
+    prompts = _prompts(cfg, [5, 70, 33, 300])
+    say("[gpu] batch of 4 ragged prompts vs alone")
+    out_b, cnt_b, st = dec.generate(prompts, 4, 48, log_cap=64)
+    assert (cnt_b == 48).all()
+    log = st["n_accept_log"]
+    assert len({int(x) for x in log[log >= 0]}) >= 2, "acceptance should vary across rounds"
+    for i, p in enumerate(prompts):
+        out_1, _, _ = dec.generate([p], 4, 48)
+        np.testing.assert_array_equal(out_b[i], out_1[0])
+        out_g, _, _ = dec.generate([p], 0, 48)
+        np.testing.assert_array_equal(out_b[i], out_g[0])
+
+
+def test_graph_replay_equals_eager(batch_dec):
+    cfg, w, dec = batch_dec
+    prompts = _prompts(cfg, [40, 9], seed=8)
+    say("[gpu] graph vs eager")
+    a, _, sa = dec.generate(prompts, 3, 40, use_graph=False, log_cap=64)
+    b, _, sb = dec.generate(prompts, 3, 40, use_graph=True, log_cap=64)
+    np.testing.assert_array_equal(a, b)
+    np.testing.assert_array_equal(sa["n_accept_log"], sb["n_accept_log"])
+
+
+@pytest.mark.parametrize("a", [0, 1, 2, 3, 4])
+def test_forced_acceptance(batch_dec, a):
+    cfg, w, dec = batch_dec
+    prompts = _prompts(cfg, [30, 12], seed=9)
+    trace, _, _ = dec.generate(prompts, 0, 40)
+    say(f"[gpu] forced acceptance a={a}")
+    out, cnt, st = dec.generate(prompts, 4, 40, sim_accept=a, forced_trace=trace, log_cap=64)
+    np.testing.assert_array_equal(out, trace)
+    log = st["n_accept_log"]
+    for b in range(2):
+        live = log[:, b][log[:, b] >= 0]
+        # every round that ends inside the trace accepts exactly a drafts
+        assert (live[:-1] == a).all(), (a, live)
+    assert st["rounds"] == -(-40 // (a + 1))
+
+
+def test_eos_stops_each_sequence(batch_dec):
+    cfg, w, dec = batch_dec
+    prompts = _prompts(cfg, [20, 25], seed=10)
+    ref, _, _ = dec.generate(prompts, 0, 30)
+    eos = int(ref[0, 6])
+    out, cnt, _ = dec.generate(prompts, 4, 30, eos_id=eos)
+    for b in range(2):
+        hits = np.nonzero(ref[b] == eos)[0]
+        n = hits[0] + 1 if len(hits) else 30
+        assert cnt[b] == n
+        np.testing.assert_array_equal(out[b, :n], ref[b, :n])
+        assert (out[b, n:] == -1).all()
+
+
+def test_rounds_and_stepwise_calls_agree_with_generate(batch_dec):
+    cfg, w, dec = batch_dec
+    prompts = _prompts(cfg, [17, 64], seed=11)
+    ref, _, _ = dec.generate(prompts, 0, 60)
+    dec.prefill(prompts)
+    binding.seed_rounds(dec.ctx, 4, 6, True)
+    for b in range(2):
+        toks = dec.tokens(b)
+        n = len(toks) - len(prompts[b])
+        assert n >= 6
+        np.testing.assert_array_equal(toks[len(prompts[b]):], ref[b, :n])
+    # the step-wise calls: draft, then verify the device drafts
+    dec.prefill(prompts)
+    total = [0, 0]
+    for _ in range(5):
+        d, _ = dec.draft(3)
+        na, bo, _ = dec.verify(3)
+        for b in range(2):
+            total[b] += na[b] + 1
+    for b in range(2):
+        toks = dec.tokens(b)
+        np.testing.assert_array_equal(toks[len(prompts[b]):], ref[b, :total[b]])
+
+
+def test_long_context_spans_several_attention_groups():
+    """A 700-token context crosses two 256-position group boundaries (cross-group merge)."""
+    cfg = synth.C1_TINY
+    w = synth.make_weights(cfg, seed=4)
+    prompt = _prompts(cfg, [700], seed=12)[0]
+    m = oracle_model(cfg, w)
+    st = os_.prefill(m, prompt, 760)
+    drafts, qlog = os_.draft(st, 4)
+    vlog = os_.verify(st, drafts)
+    dec = decoder(cfg, w, max_batch=1, max_ctx=760, max_draft=4)
+    try:
+        dec.prefill([prompt])
+        d, q = dec.draft(4, logits=True)
+        _, _, v = dec.verify(4, drafts=drafts[1:][None].astype(np.int32), logits=True)
+        err_q = np.abs(q[0, 0] - qlog[0]).max()
+        err_v = np.abs(v[0] - vlog).max()
+        say(f"[gpu] long context: draft err {err_q:.2e}, verify err {err_v:.2e}")
+        assert err_q <= 1e-4 and err_v <= 1e-4
+        g0, _, _ = dec.generate([prompt], 0, 24)
+        g4, _, _ = dec.generate([prompt], 4, 24)
+        np.testing.assert_array_equal(g0, g4)
+        ref, _ = os_.generate(m, prompt, 4, 24)
+        gap_ok = all(top2_gap(vlog) > 2e-4)
+        if gap_ok:
+            assert g4[0, 0] == ref[0]
+    finally:
+        dec.close()
+
+
+def test_error_paths_leave_state_unchanged(batch_dec):
+    cfg, w, dec = batch_dec
+    lib = binding.load_library()
+    fresh = decoder(cfg, w, max_batch=2, max_ctx=80, max_draft=4)
+    try:
+        with pytest.raises(binding.SeedError) as e:
+            fresh.draft(2)
+        assert e.value.status == -2
+        prompts = _prompts(cfg, [10, 20], seed=13)
+        with pytest.raises(binding.SeedError) as e:
+            fresh.prefill(_prompts(cfg, [5, 5, 5]))
+        assert e.value.status == -3
+        with pytest.raises(binding.SeedError) as e:
+            fresh.prefill([np.array([1, 2, cfg.vocab], np.int32)])
+        assert e.value.status == -1
+        with pytest.raises(binding.SeedError) as e:
+            fresh.prefill([np.zeros(80, np.int32)])
+        assert e.value.status == -3
+        fresh.prefill(prompts)
+        before = [fresh.tokens(b) for b in range(2)]
+        with pytest.raises(binding.SeedError) as e:
+            fresh.draft(5)
+        assert e.value.status == -1
+        with pytest.raises(binding.SeedError) as e:
+            fresh.verify(3)
+        assert e.value.status == -2          # no drafts of length 3 since the last commit
+        with pytest.raises(binding.SeedError) as e:
+            fresh.verify(2, drafts=np.array([[1, -1], [0, 0]], np.int32))
+        assert e.value.status == -1
+        with pytest.raises(binding.SeedError) as e:
+            binding.seed_rounds(fresh.ctx, 4, 40, False)
+        assert e.value.status == -3
+        assert lib.seed_last_error()
+        for b in range(2):
+            np.testing.assert_array_equal(fresh.tokens(b), before[b])
+        # still usable, and the result equals a run that never saw the errors
+        out, _, _ = fresh.generate(prompts, 2, 20)
+        ref, _, _ = dec.generate(prompts, 2, 20)
+        np.testing.assert_array_equal(out, ref)
+        with pytest.raises(binding.SeedError) as e:
+            fresh.generate(prompts, 2, 70)
+        assert e.value.status == -3
+    finally:
+        fresh.close()
+
+
+def test_missing_weights_are_reported():
+    cfg = synth.C1_TINY
+    w = synth.make_weights(cfg, seed=0)
+    dec = binding.Decoder(cfg, max_batch=1, max_ctx=64, max_draft=2)
+    try:
+        part = {k: v for k, v in w.items() if k != "layers.1.w_up"}
+        dec.load_weights(part)
+        with pytest.raises(binding.SeedError) as e:
+            dec.prefill([np.arange(5, dtype=np.int32)])
+        assert e.value.status == -2 and "layers.1.w_up" in str(e.value)
+        with pytest.raises(binding.SeedError) as e:
+            dec.load_weights({"layers.1.w_up": w["layers.1.w_up"][:, :64]})
+        assert e.value.status == -1
+        dec.load_weights({"layers.1.w_up": w["layers.1.w_up"]})
+        dec.prefill([np.arange(5, dtype=np.int32)])
+        # host-side sources take the same path as device sources
+        host = binding.Decoder(cfg, max_batch=1, max_ctx=64, max_draft=2)
+        host.load_weights(w, on_device=False)
+        a, _, _ = dec.generate([np.arange(5, dtype=np.int32)], 2, 10)
+        b, _, _ = host.generate([np.arange(5, dtype=np.int32)], 2, 10)
+        np.testing.assert_array_equal(a, b)
+        host.close()
+    finally:
+        dec.close()
