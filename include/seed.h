@@ -57,7 +57,7 @@ typedef enum seed_dtype {
  * Supported: hidden, ffn, n_heads*head_dim, n_kv_heads*head_dim multiples of 32; vocab a
  * multiple of 16; head_dim in {64, 128}; n_heads a multiple of n_kv_heads with
  * (n_heads/n_kv_heads) <= 32; 0 <= n_dec_layers <= n_layers; kv_block == 16;
- * 1 <= max_batch <= 64; 0 <= max_draft <= 15; max_ctx >= 2.
+ * 1 <= max_batch <= 64; 0 <= max_draft <= 15; 2 <= max_ctx <= 2^20.
  */
 typedef struct seed_config {
   int32_t n_layers;       /* l */

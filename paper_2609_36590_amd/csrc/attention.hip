@@ -241,50 +241,43 @@ __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
   if (n_groups == 1) return;
 
   // ---- the last group of (b, h, rb) to finish merges all group partials left to right ----
-  __threadfence();
+  // One agent-scope acquire-release count per workgroup, after the barrier has completed every
+  // wave's stores: it publishes this group's partial and, for the last group, makes the others
+  // visible.
   __syncthreads();
   int* cnt = a.cnt + (b * a.n_kv + h) * a.n_rb + rb;
-  if (threadIdx.x == 0) s_last = (atomicAdd(cnt, 1) == n_groups - 1);
+  if (threadIdx.x == 0)
+    s_last = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) == n_groups - 1;
   __syncthreads();
   if (!s_last) return;
-  __threadfence();
-  // Two passes over the group partials (g in increasing order): per query, the global max m*,
-  // the weights w_g = 2^(m_g - m*) and L = sum_g w_g l_g; then out = sum_g w_g o_g / L. A group
-  // that sees nothing has w_g = 0 exactly and adds exact zeros.
+  // Merge the group partials left to right (online softmax merge, fixed order). Thread e owns
+  // columns 4*(e mod HD/4).. of query vector e / (HD/4); each batch of 8 groups is loaded at
+  // once. A group that sees nothing is an exact identity of the merge.
   const float* part0 = a.part + ((((size_t)(b * a.n_kv + h) * a.n_rb + rb) * a.n_groups_max) * 32) * PS;
-  float* s_w = &s_o[0][0][0];                 // [n_groups][32] weights (n_groups <= 3*HD)
-  float* s_L = &s_ml[0][0][0];                // [32]
-  if (threadIdx.x < nqv) {
-    const int qv = threadIdx.x;
-    float mstar = NEG_INF;
-    for (int gi = 0; gi < n_groups; ++gi) mstar = fmaxf(mstar, part0[((size_t)gi * 32 + qv) * PS + HD]);
-    float L = 0.f;
-    for (int gi = 0; gi < n_groups; ++gi) {
-      const float* pp = part0 + ((size_t)gi * 32 + qv) * PS;
-      const float mg = pp[HD];
-      const float wg = (mg == NEG_INF) ? 0.f : exp2f(mg - mstar);
-      s_w[gi * 32 + qv] = wg;
-      L += wg * pp[HD + 1];
-    }
-    s_L[qv] = L;
-  }
-  __syncthreads();
-  for (int e = threadIdx.x; e < nqv * HD; e += blockDim.x) {
-    const int qv = e / HD, d = e - qv * HD;
-    float o = 0.f;
-    int gi = 0;
-    for (; gi + 4 <= n_groups; gi += 4) {
-      float oo[4];
+  constexpr int HD4 = HD / 4;
+  for (int e = threadIdx.x; e < nqv * HD4; e += blockDim.x) {
+    const int qv = e / HD4, d = (e - qv * HD4) * 4;
+    float m_r = NEG_INF, l_r = 0.f, o_r[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int g0 = 0; g0 < n_groups; g0 += 8) {
+      float mg[8], lg[8], og[8][4];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) oo[u] = part0[((size_t)(gi + u) * 32 + qv) * PS + d];
+      for (int u = 0; u < 8; ++u) {
+        const float* pp = part0 + ((size_t)min(g0 + u, n_groups - 1) * 32 + qv) * PS;
+        const float4 v = *reinterpret_cast<const float4*>(pp + d);
+        const float2 ml = *reinterpret_cast<const float2*>(pp + HD);
+        og[u][0] = v.x; og[u][1] = v.y; og[u][2] = v.z; og[u][3] = v.w;
+        mg[u] = ml.x;
+        lg[u] = ml.y;
+      }
 #pragma unroll
-      for (int u = 0; u < 4; ++u) o += s_w[(gi + u) * 32 + qv] * oo[u];
+      for (int u = 0; u < 8; ++u)
+        if (g0 + u < n_groups) softmax_merge(m_r, l_r, o_r, mg[u], lg[u], og[u], 4);
     }
-    for (; gi < n_groups; ++gi) o += s_w[gi * 32 + qv] * part0[((size_t)gi * 32 + qv) * PS + d];
     const int rl = qv / a.G, gq = qv - rl * a.G;
-    a.out[(size_t)(mrow0 + rl) * qstride + (h * a.G + gq) * HD + d] = o / s_L[qv];
+    *reinterpret_cast<float4*>(a.out + (size_t)(mrow0 + rl) * qstride + (h * a.G + gq) * HD + d) =
+        make_float4(o_r[0] / l_r, o_r[1] / l_r, o_r[2] / l_r, o_r[3] / l_r);
   }
-  if (threadIdx.x == 0) atomicExch(cnt, 0);
+  if (threadIdx.x == 0) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 template <typename T>

@@ -71,6 +71,15 @@ struct ET<uint16_t> {
     }
   }
   __device__ static uint16_t from_f32(float f) { return f2bf(f); }
+  // B operand kept in LDS as 32 bytes per lane slot: 8 bf16 hi, then 8 bf16 lo
+  __device__ static void to_lds(char* p, const float x[8]) {
+    const B b = split(x);
+    *reinterpret_cast<bf16x8*>(p) = b.hi;
+    *reinterpret_cast<bf16x8*>(p + 16) = b.lo;
+  }
+  __device__ static B from_lds(const char* p) {
+    return B{*reinterpret_cast<const bf16x8*>(p), *reinterpret_cast<const bf16x8*>(p + 16)};
+  }
 };
 
 template <>
@@ -101,6 +110,15 @@ struct ET<float> {
     out[4] = a.b.x; out[5] = a.b.y; out[6] = a.b.z; out[7] = a.b.w;
   }
   __device__ static float from_f32(float f) { return f; }
+  // B operand kept in LDS as 32 bytes per lane slot: 8 fp32
+  __device__ static void to_lds(char* p, const float x[8]) {
+    reinterpret_cast<float4*>(p)[0] = make_float4(x[0], x[1], x[2], x[3]);
+    reinterpret_cast<float4*>(p)[1] = make_float4(x[4], x[5], x[6], x[7]);
+  }
+  __device__ static B from_lds(const char* p) {
+    const float4 u = reinterpret_cast<const float4*>(p)[0], v = reinterpret_cast<const float4*>(p)[1];
+    return B{{u.x, u.y, u.z, u.w, v.x, v.y, v.z, v.w}};
+  }
 };
 
 __device__ __forceinline__ void load8(const float* p, float x[8]) {

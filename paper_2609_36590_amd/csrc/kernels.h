@@ -28,7 +28,13 @@ struct LinArgs {
   const void* W;          // packed weights
   int N, K;               // output features, input features
   int M;                  // activation rows in this pass
-  int NT, KS;             // n-tiles per workgroup, K-splits per n-tile (waves = NT * KS)
+  int NT, KS;             // n-tiles per workgroup pass, K-splits per n-tile
+  int S;                  // K-slices: the KS splits form S consecutive groups of KS/S; partial sums
+                          // are added group by group, in order (the LDS kernel gives each slice
+                          // its own workgroup and the last one to finish adds them up)
+  int NJ;                 // LDS kernel, S == 1: passes per workgroup (n-group blockIdx.x + j*gridDim.x)
+  float* lpart;           // S > 1: slice partials [n_groups][S][NT][M][16]
+  int* lcnt;              // S > 1: finished-slice counters [n_groups] (zero between launches)
   // input
   const float* X;         // [M][ldx] fp32 activations; PRO_NORM: x*g formed by the producer
   int ldx;
@@ -46,12 +52,9 @@ struct LinArgs {
   // EPI_QKV
   float* q;               // [M][n_heads*head_dim] rotated queries (fp32)
   void* kv;               // KV pool
-  const int* bt;          // block tables [B][bt_stride]
-  int bt_stride;
-  const int* row_seq;     // [M] sequence of each row
   const int* row_pos;     // [M] absolute position of each row
-  const float* rope_cos;  // [max_ctx][head_dim/2]
-  const float* rope_sin;
+  const int* row_blk;     // [M] KV-pool block holding that position (same block in every layer)
+  const float* row_rope;  // [M][head_dim]: cos(pos*theta_i) for i < head_dim/2, then sin(pos*theta_i)
   int layer, n_blocks, n_heads, n_kv, head_dim;
   // EPI_HEAD
   float* logits;          // nullable: logits[m * ld_logits + n]
@@ -99,6 +102,14 @@ struct SetupArgs {
   int H;
   int* row_seq;
   int* row_pos;
+  // per-row KV block and RoPE row for the pass's QKV epilogues
+  const int* bt;          // block tables [B][bt_stride]
+  int bt_stride;
+  const float* rope_cos;  // [max_ctx][head_dim/2]
+  const float* rope_sin;
+  int head_dim;
+  int* row_blk;           // [M]
+  float* row_rope;        // [M][head_dim]
   float* h;               // [M][H]
   float* xg;              // [M][H] h * gain (input of the pass's first RMSNorm consumer)
   const float* gain;      // [H]
@@ -125,8 +136,12 @@ struct DevState {
   int eos;
 };
 
+// Kernel choice for a linear launch: weights streamed with the activation rows staged in LDS as
+// MFMA fragments (M <= 16 and the rows fit), else the activation fragments come from global memory.
+enum LinearKind { LIN_LDS = 0, LIN_GLOBAL = 1, LIN_VALU = 2 };
+
 template <typename T>
-void launch_linear(const LinArgs& a, int prologue, int epilogue, bool valu, hipStream_t s);
+void launch_linear(const LinArgs& a, int prologue, int epilogue, int kind, hipStream_t s);
 template <typename T>
 void launch_attention(const AttnArgs& a, hipStream_t s);
 template <typename T>
@@ -143,8 +158,10 @@ void launch_fill_u32(void* dst, unsigned value, long long n_words, hipStream_t s
 
 // allow the linear kernels to use more than 64 KB of LDS (once per process and dtype)
 hipError_t configure_kernels(int bf16);
+// dynamic LDS bytes one linear workgroup may use (valid after configure_kernels)
+size_t linear_lds_limit();
 
 // dynamic LDS bytes needed by launch_linear for a given shape
-size_t linear_lds_bytes(int M, int K, int NT, int KS, bool valu);
+size_t linear_lds_bytes(int M, int K, int NT, int KS, int S, int NJ, int kind);
 
 }  // namespace seedk

@@ -1,102 +1,170 @@
-// Weight-streaming linear kernels (MFMA skinny GEMM, VALU GEMV) with fused RMSNorm,
-// RoPE + paged-KV write, residual, SwiGLU and LM-head argmax epilogues.
+// Weight-streaming linear kernels (MFMA skinny GEMM) with fused RMSNorm scale, RoPE + paged-KV
+// write, residual, SwiGLU and LM-head argmax epilogues.
+//
+//  * k_linear_lds    M <= 16 rows: the activation rows are staged once per workgroup in LDS as MFMA
+//                    B-operand slots, so the vector-memory path carries weight tiles only.
+//  * k_linear_mfma   any M (prefill, large batches): activation fragments are read from global
+//                    memory next to each weight tile.
+//
+// Both compute every output with the same arithmetic: wave ks of the KS K-splits accumulates its
+// k-range in k order on MFMA, and the KS partial sums are added in S consecutive groups
+// (y = sum_s (sum_{k in group s} p_k), each sum left to right, starting from 0). The split (KS, S)
+// depends only on the weight shape (N, K), so a row's output is bit-identical whatever kernel
+// runs it and however many rows share the pass: verifying d drafts gives the same logits, row by
+// row, as plain greedy decoding (d = 0).
 #include "device_common.h"
 
 namespace seedk {
 
+// n-group of pass j of this workgroup: g0 + j * gs
+struct Grp {
+  int g0, gs;
+};
+
 // ---------------------------------------------------------------------------------------------
-// Linear epilogues. Y(nl, m, c) is the finished fp32 output of row c of the workgroup's local
-// n-tile nl for activation row m.
+// Epilogues. Y(lt, m, c) is the finished fp32 output (column c of local tile lt = j*NT + nl, row
+// m). Element e of the (lt, m, c) space is handled by thread e mod blockDim; the global values an
+// element needs (residual, gain, KV block, RoPE angles) are loaded for the thread's first element
+// at kernel start, before the weight stream, so the epilogue itself costs no extra round trip.
 // ---------------------------------------------------------------------------------------------
+struct EpiPre {
+  float h, g;        // EPI_RESID: residual value and next-norm gain
+  int pos, blk;      // EPI_QKV: position and KV block of the row
+  float cs, sn;      // EPI_QKV: RoPE cos/sin for the element's rotary pair
+};
+
+__device__ __forceinline__ void epi_coords(const LinArgs& a, Grp gr, int e, int& lt, int& m, int& c, int& nt) {
+  const int per = a.M * 16;
+  lt = e / per;
+  const int r = e - lt * per;
+  m = r >> 4;
+  c = r & 15;
+  const int j = lt / a.NT, nl = lt - j * a.NT;
+  nt = (gr.g0 + j * gr.gs) * a.NT + nl;
+}
+
+// QKV section of n-tile nt: 0 = q, 1 = k, 2 = v; (head, j) = tile j of that head (dims 8j..8j+7
+// and head_dim/2+8j..+7, so rotary partners share the tile).
+__device__ __forceinline__ void qkv_tile(const LinArgs& a, int nt, int& sec, int& head, int& j) {
+  const int tpd = a.head_dim >> 4, q_tiles = a.n_heads * tpd, k_tiles = a.n_kv * tpd;
+  int lt;
+  if (nt < q_tiles) { sec = 0; lt = nt; }
+  else if (nt < q_tiles + k_tiles) { sec = 1; lt = nt - q_tiles; }
+  else { sec = 2; lt = nt - q_tiles - k_tiles; }
+  head = lt / tpd;
+  j = lt - head * tpd;
+}
+
+template <int EPI>
+__device__ __forceinline__ void epi_load(const LinArgs& a, Grp gr, int e, EpiPre& p) {
+  int lt, m, c, nt;
+  epi_coords(a, gr, e, lt, m, c, nt);
+  if (e >= a.NJ * a.NT * a.M * 16 || nt >= (a.N >> 4)) return;
+  if constexpr (EPI == EPI_RESID) {
+    p.h = a.h[(size_t)m * a.N + nt * 16 + c];
+    p.g = a.gain_next[nt * 16 + c];
+  } else if constexpr (EPI == EPI_QKV) {
+    int sec, head, j;
+    qkv_tile(a, nt, sec, head, j);
+    p.pos = a.row_pos[m];
+    p.blk = a.row_blk[m];
+    const int fi = 8 * j + (c & 7);
+    p.cs = a.row_rope[(size_t)m * a.head_dim + fi];
+    p.sn = a.row_rope[(size_t)m * a.head_dim + (a.head_dim >> 1) + fi];
+  }
+}
+
 template <typename T, int EPI>
-__device__ void linear_epilogue(const LinArgs& a, const float* Y, int y_nl_stride, int y_m_stride) {
+__device__ void linear_epilogue(const LinArgs& a, Grp gr, const float* Y, int y_lt_stride, const EpiPre& pre) {
   const int tid = threadIdx.x, nthr = blockDim.x;
   const int n_tiles = a.N >> 4;
   const int M = a.M;
-#define YV(nl_, m_, c_) Y[(nl_) * y_nl_stride + (m_) * y_m_stride + (c_)]
-  if constexpr (EPI == EPI_RESID) {
-    for (int e = tid; e < a.NT * M; e += nthr) {
-      const int nl = e / M, m = e - nl * M;
-      const int nt = blockIdx.x * a.NT + nl;
+  const int total = a.NJ * a.NT * M * 16;
+#define YV(lt_, m_, c_) Y[(lt_) * y_lt_stride + (m_) * 16 + (c_)]
+  if constexpr (EPI == EPI_RESID || EPI == EPI_QKV) {
+    // nthr is a multiple of 64 and total of 16, so the 16 columns of one (lt, m) are 16 aligned
+    // lanes of one wave in the same iteration (the ssq butterfly below stays inside them)
+    for (int e = tid; e < total; e += nthr) {
+      int lt, m, c, nt;
+      epi_coords(a, gr, e, lt, m, c, nt);
       if (nt >= n_tiles) continue;
-      float* hp = a.h + (size_t)m * a.N + nt * 16;
-      float* xgp = a.xg + (size_t)m * a.N + nt * 16;
-      const float* gn = a.gain_next + nt * 16;
-      float s = 0.f;
-#pragma unroll
-      for (int c = 0; c < 16; ++c) {
-        const float v = hp[c] + YV(nl, m, c);
-        hp[c] = v;
-        xgp[c] = v * gn[c];
-        s += v * v;
+      EpiPre p = pre;
+      if (e != tid) epi_load<EPI>(a, gr, e, p);
+      if constexpr (EPI == EPI_RESID) {
+        const float v = p.h + YV(lt, m, c);
+        const size_t off = (size_t)m * a.N + nt * 16 + c;
+        a.h[off] = v;
+        a.xg[off] = v * p.g;
+        float s = v * v;
+        s += __shfl_xor(s, 8);
+        s += __shfl_xor(s, 4);
+        s += __shfl_xor(s, 2);
+        s += __shfl_xor(s, 1);
+        if (c == 0) a.ssq_out[(size_t)m * n_tiles + nt] = s;
+      } else {
+        const int HD = a.head_dim, half = HD >> 1;
+        int sec, head, j;
+        qkv_tile(a, nt, sec, head, j);
+        const int d = (c < 8) ? 8 * j + c : half + 8 * j + (c - 8);
+        float y = YV(lt, m, c);
+        if (sec < 2) {
+          const float partner = YV(lt, m, c ^ 8);
+          y = (c < 8) ? (y * p.cs - partner * p.sn) : (y * p.cs + partner * p.sn);
+        }
+        if (sec == 0) {
+          a.q[(size_t)m * a.n_heads * HD + head * HD + d] = y;
+        } else {
+          T* kvp = reinterpret_cast<T*>(a.kv);
+          const size_t base = ((size_t)(a.layer * a.n_blocks + p.blk) * 2 + (sec - 1)) * a.n_kv + head;
+          if (sec == 1) kvp[base * 16 * HD + (p.pos & 15) * HD + d] = ET<T>::from_f32(y);
+          else kvp[base * HD * 16 + d * 16 + (p.pos & 15)] = ET<T>::from_f32(y);
+        }
       }
-      a.ssq_out[(size_t)m * n_tiles + nt] = s;
     }
   } else if constexpr (EPI == EPI_SWIGLU) {
     const int F = a.N >> 1;
-    for (int e = tid; e < a.NT * M * 8; e += nthr) {
-      const int nl = e / (M * 8), r = e - nl * M * 8, m = r >> 3, c = r & 7;
-      const int nt = blockIdx.x * a.NT + nl;
+    for (int e = tid; e < a.NJ * a.NT * M * 8; e += nthr) {
+      const int lt = e / (M * 8), r = e - lt * M * 8, m = r >> 3, c = r & 7;
+      const int j = lt / a.NT, nt = (gr.g0 + j * gr.gs) * a.NT + (lt - j * a.NT);
       if (nt >= n_tiles) continue;
-      const float g = YV(nl, m, c), u = YV(nl, m, c + 8);
+      const float g = YV(lt, m, c), u = YV(lt, m, c + 8);
       a.act[(size_t)m * F + nt * 8 + c] = g / (1.f + __expf(-g)) * u;
-    }
-  } else if constexpr (EPI == EPI_QKV) {
-    const int HD = a.head_dim, tpd = HD >> 4, half = HD >> 1;
-    const int q_tiles = a.n_heads * tpd, k_tiles = a.n_kv * tpd;
-    T* kvp = reinterpret_cast<T*>(a.kv);
-    for (int e = tid; e < a.NT * M * 16; e += nthr) {
-      const int nl = e / (M * 16), r = e - nl * M * 16, m = r >> 4, c = r & 15;
-      const int nt = blockIdx.x * a.NT + nl;
-      if (nt >= n_tiles) continue;
-      int sec, lt;
-      if (nt < q_tiles) { sec = 0; lt = nt; }
-      else if (nt < q_tiles + k_tiles) { sec = 1; lt = nt - q_tiles; }
-      else { sec = 2; lt = nt - q_tiles - k_tiles; }
-      const int head = lt / tpd, j = lt - head * tpd;
-      const int d = (c < 8) ? 8 * j + c : half + 8 * j + (c - 8);
-      const int pos = a.row_pos[m];
-      float y = YV(nl, m, c);
-      if (sec < 2) {
-        const int fi = 8 * j + (c & 7);
-        const float cs = a.rope_cos[(size_t)pos * half + fi];
-        const float sn = a.rope_sin[(size_t)pos * half + fi];
-        const float partner = YV(nl, m, c ^ 8);
-        y = (c < 8) ? (y * cs - partner * sn) : (y * cs + partner * sn);
-      }
-      if (sec == 0) {
-        a.q[(size_t)m * a.n_heads * HD + head * HD + d] = y;
-      } else {
-        const int b = a.row_seq[m];
-        const int blk = a.bt[b * a.bt_stride + (pos >> 4)];
-        const size_t base = ((size_t)(a.layer * a.n_blocks + blk) * 2 + (sec - 1)) * a.n_kv + head;
-        if (sec == 1) kvp[base * 16 * HD + (pos & 15) * HD + d] = ET<T>::from_f32(y);
-        else kvp[base * HD * 16 + d * 16 + (pos & 15)] = ET<T>::from_f32(y);
-      }
     }
   } else {  // EPI_HEAD
     if (a.logits) {
-      for (int e = tid; e < a.NT * M * 16; e += nthr) {
-        const int nl = e / (M * 16), r = e - nl * M * 16, m = r >> 4, c = r & 15;
-        const int nt = blockIdx.x * a.NT + nl;
+      for (int e = tid; e < total; e += nthr) {
+        int lt, m, c, nt;
+        epi_coords(a, gr, e, lt, m, c, nt);
         if (nt >= n_tiles) continue;
-        a.logits[(long long)m * a.ld_logits + nt * 16 + c] = YV(nl, m, c);
+        a.logits[(long long)m * a.ld_logits + nt * 16 + c] = YV(lt, m, c);
       }
     }
-    // per-workgroup argmax (lowest token id among equal maxima), reduced by a finalize kernel
-    for (int m = tid; m < M; m += nthr) {
+    // argmax of each row over each pass's n-group (lowest token id among equal maxima): one wave
+    // per (pass, row), lane-strided candidates, then a butterfly; the partial of n-group g goes to
+    // slot g and k_argmax_finalize reduces the slots
+    const int lane = tid & 63, wave = tid >> 6, nw = nthr >> 6;
+    for (int q = wave; q < a.NJ * M; q += nw) {
+      const int j = q / M, m = q - j * M;
+      const int grp = gr.g0 + j * gr.gs;
+      if (grp * a.NT >= n_tiles) continue;
+      const int n_cand = min(a.NT, n_tiles - grp * a.NT) * 16;
+      const int id0 = grp * a.NT * 16;
       float best = NEG_INF;
       int bi = -1;
-      for (int nl = 0; nl < a.NT; ++nl) {
-        const int nt = blockIdx.x * a.NT + nl;
-        if (nt >= n_tiles) break;
-        for (int c = 0; c < 16; ++c) {
-          const float v = YV(nl, m, c);
-          if (bi < 0 || v > best) { best = v; bi = nt * 16 + c; }
-        }
+      for (int jc = lane; jc < n_cand; jc += 64) {
+        const float v = YV(j * a.NT + (jc >> 4), m, jc & 15);
+        if (bi < 0 || v > best) { best = v; bi = id0 + jc; }
       }
-      a.amax_val[(size_t)m * a.amax_stride + blockIdx.x] = best;
-      a.amax_idx[(size_t)m * a.amax_stride + blockIdx.x] = bi;
+#pragma unroll
+      for (int o = 32; o >= 1; o >>= 1) {
+        const float ov = __shfl_xor(best, o);
+        const int oi = __shfl_xor(bi, o);
+        if (oi >= 0 && (bi < 0 || ov > best || (ov == best && oi < bi))) { best = ov; bi = oi; }
+      }
+      if (lane == 0) {
+        a.amax_val[(size_t)m * a.amax_stride + grp] = best;
+        a.amax_idx[(size_t)m * a.amax_stride + grp] = bi;
+      }
     }
   }
 #undef YV
@@ -130,18 +198,193 @@ __device__ __forceinline__ bool preload_row_ssq(const LinArgs& a, int m, float s
   return true;
 }
 
+// sum of n consecutive wave partials (stride `per` floats), left to right from 0
+__device__ __forceinline__ float sum_partials(const float* p, int n, int per) {
+  float t = 0.f;
+  for (int k = 0; k < n; ++k) t += p[(size_t)k * per];
+  return t;
+}
+
+// k-tiles of slice s: from slice_kt_begin(s) to slice_kt_begin(s + 1), the k-ranges of the
+// K-splits s*KS/S .. (s+1)*KS/S - 1
+__host__ __device__ inline int slice_kt_begin(int KT, int KS, int S, int s) { return (s * (KS / S) * KT) / KS; }
+// an upper bound of the k-tiles of any slice
+__host__ __device__ inline int slice_kt_max(int KT, int S) { return S == 1 ? KT : (KT + S - 1) / S + 1; }
+__host__ __device__ inline size_t lds_x_bytes(int M, int nkt) { return (size_t)nkt * 4 * M * 32 + 32; }
+
 // ---------------------------------------------------------------------------------------------
-// Weight-streaming skinny GEMM on MFMA: Y[M, N] = X[M, K] W^T, M <= 16*TT.
+// Skinny GEMM with the activation rows in LDS: Y[M, N] = X[M, K] W^T, M <= 16 (one MFMA tile).
+//
+// The workgroup (NT * KS/S waves) issues its first weight tiles, then stages the X columns of its
+// K-slice into LDS as MFMA B-operand slots: slot (kt, kg, r) = 32 bytes holding
+// x[r][32kt + 8kg .. +7] (bf16 hi/lo pair for bf16 weights, fp32 otherwise), plus one zero slot
+// for the token columns r >= M. Waves then stream weight tiles with P in flight, reading their B
+// operands from LDS.
+//
+// Work: with S == 1 the workgroup makes NJ passes over n-groups blockIdx.x + j*gridDim.x (NT
+// n-tiles each) and wave (nl, ks) covers k-range ks of n-tile nl of every pass, as one continuous
+// stream. With S > 1 (few n-tiles, long K) workgroup b takes slice b mod S of n-group b / S; its
+// slice sum goes to global memory and the last of the S workgroups to finish adds the S slice
+// sums in slice order and runs the epilogue.
+// ---------------------------------------------------------------------------------------------
+template <typename T, int PRO, int EPI>
+__global__ void __launch_bounds__(1024) k_linear_lds(LinArgs a) {
+  extern __shared__ __attribute__((aligned(16))) char lds[];
+  __shared__ float s_rs[16];
+  __shared__ int s_last;
+  constexpr int P = 8;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int S = a.S, KSs = a.KS / S;
+  const int NW = a.NT * KSs;
+  const int KT = a.K >> 5, n_tiles = a.N >> 4, M = a.M;
+  const int nl = wave / KSs, kss = wave - nl * KSs;
+  const int tl = lane & 15, kg = lane >> 4;
+  const int sl = (S > 1) ? (int)(blockIdx.x % S) : 0;
+  const Grp gr = (S > 1) ? Grp{(int)(blockIdx.x / S), 0} : Grp{(int)blockIdx.x, (int)gridDim.x};
+  const int ks = sl * KSs + kss;
+  const int kt0 = (ks * KT) / a.KS, nk = ((ks + 1) * KT) / a.KS - kt0;
+  const int ktA = slice_kt_begin(KT, a.KS, S, sl), nkt_s = slice_kt_begin(KT, a.KS, S, sl + 1) - ktA;
+  int nj = 0;
+  while (nj < a.NJ && (gr.g0 + nj * gr.gs) * a.NT + nl < n_tiles) ++nj;
+  const int Sw = nj * nk;  // weight tiles this wave streams
+  const T* w0 = reinterpret_cast<const T*>(a.W) + ((size_t)(gr.g0 * a.NT + nl) * KT + kt0) * 512 + lane * 8;
+  const size_t wj = (size_t)gr.gs * a.NT * KT * 512;  // elements from one pass's n-tile to the next
+
+  // ---- weight prefetch ----
+  typename ET<T>::A wb[P];
+  int jI = 0, iI = 0;  // pass / k-tile of the next tile to issue
+  auto issue = [&](int slot) {
+    wb[slot] = ET<T>::load_nt(w0 + jI * wj + (size_t)iI * 512);
+    if (++iI == nk) { iI = 0; ++jI; }
+  };
+#pragma unroll
+  for (int p = 0; p < P; ++p)
+    if (p < Sw) issue(p);
+
+  EpiPre epre{};
+  epi_load<EPI>(a, gr, tid, epre);
+  float ssv[4] = {0.f, 0.f, 0.f, 0.f};
+  bool pre = false;
+  if constexpr (PRO == PRO_NORM) pre = preload_row_ssq(a, wave, ssv);
+
+  // ---- stage the slice's X columns into LDS (loads first, then the LDS writes) ----
+  const size_t zero_off = (size_t)nkt_s * 4 * M * 32;
+  float* part = reinterpret_cast<float*>(lds + lds_x_bytes(M, slice_kt_max(KT, S)));  // [NJ][NW][M][16]
+  {
+    const int row_items = nkt_s * 4, items = M * row_items;
+    for (int q0 = 0; q0 < items; q0 += 2 * (int)blockDim.x) {
+      float xv[2][8];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int q = q0 + u * blockDim.x + tid;
+        if (q < items) {
+          const int r = q / row_items, rem = q - r * row_items;
+          load8(a.X + (size_t)r * a.ldx + (size_t)(ktA * 4 + rem) * 8, xv[u]);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int q = q0 + u * blockDim.x + tid;
+        if (q < items) {
+          const int r = q / row_items, rem = q - r * row_items;
+          ET<T>::to_lds(lds + ((size_t)rem * M + r) * 32, xv[u]);
+        }
+      }
+    }
+    if (tid < 2) *reinterpret_cast<float4*>(lds + zero_off + tid * 16) = make_float4(0.f, 0.f, 0.f, 0.f);
+  }
+  __syncthreads();
+
+  // ---- stream ----
+  const bool live_col = tl < M;
+  const char* xa = lds + (live_col ? ((size_t)(kt0 - ktA) * 4 * M + (size_t)kg * M + tl) * 32 : zero_off);
+  const size_t xs = live_col ? (size_t)4 * M * 32 : 0;  // bytes per k-tile
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  int jC = 0, iC = 0;  // pass / k-tile of the next tile to consume
+  auto consume = [&](int slot) {
+    ET<T>::mma(acc, wb[slot], ET<T>::from_lds(xa + iC * xs));
+    if (++iC == nk) {
+      if (live_col) {
+        float* dst = part + ((size_t)(jC * NW + wave) * M + tl) * 16 + 4 * kg;
+        dst[0] = acc[0]; dst[1] = acc[1]; dst[2] = acc[2]; dst[3] = acc[3];
+      }
+      acc = f32x4{0.f, 0.f, 0.f, 0.f};
+      iC = 0;
+      ++jC;
+    }
+  };
+  int s0 = 0;
+  for (; s0 + 2 * P <= Sw; s0 += P) {
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+      consume(p);
+      issue(p);
+      // keep each refill next to its consumption (the scheduler would otherwise sink all refills
+      // below the last MFMA and drain the pipeline once per P tiles)
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+#pragma unroll
+  for (int p = 0; p < P; ++p) {
+    if (s0 + p < Sw) {
+      consume(p);
+      if (s0 + p + P < Sw) issue(p);
+    }
+  }
+#pragma unroll
+  for (int p = 0; p < P; ++p)
+    if (s0 + P + p < Sw) consume(p);
+
+  // ---- sums over the workgroup's K-splits, slice combine, RMSNorm row scale, epilogue ----
+  if constexpr (PRO == PRO_NORM) {
+    for (int m = wave; m < M; m += NW) {
+      const float r = wave_row_scale(a, m, ssv, pre && m == wave);
+      if (lane == 0) s_rs[m] = r;
+    }
+  }
+  __syncthreads();
+  const int per = M * 16;
+  const int n_out = a.NJ * a.NT * per;
+  for (int e = tid; e < n_out; e += blockDim.x) {
+    const int lt = e / per, r = e - lt * per;
+    const int j = lt / a.NT, nl2 = lt - j * a.NT;
+    float* src = part + (size_t)(j * NW + nl2 * KSs) * per + r;
+    float y = sum_partials(src, KSs, per);
+    if (S > 1) {
+      a.lpart[((size_t)gr.g0 * S + sl) * a.NT * per + e] = y;  // NJ == 1 here, so e < NT * per
+    } else {
+      if constexpr (PRO == PRO_NORM) y *= s_rs[r >> 4];
+      *src = y;
+    }
+  }
+  if (S > 1) {
+    // one agent-scope acquire-release count per workgroup, after the barrier has completed every
+    // wave's stores: it publishes this slice and, for the last slice, makes the others visible
+    __syncthreads();
+    if (tid == 0)
+      s_last = __hip_atomic_fetch_add(a.lcnt + gr.g0, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) == S - 1;
+    __syncthreads();
+    if (!s_last) return;
+    for (int e = tid; e < a.NT * per; e += blockDim.x) {
+      const int nl2 = e / per, r = e - nl2 * per;
+      float y = 0.f;
+      for (int s2 = 0; s2 < S; ++s2) y += a.lpart[((size_t)gr.g0 * S + s2) * a.NT * per + e];
+      if constexpr (PRO == PRO_NORM) y *= s_rs[r >> 4];
+      part[(size_t)(nl2 * KSs) * per + r] = y;
+    }
+    if (tid == 0) __hip_atomic_store(a.lcnt + gr.g0, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+  linear_epilogue<T, EPI>(a, gr, part, KSs * per, epre);
+}
+
+// ---------------------------------------------------------------------------------------------
+// Skinny GEMM with activation fragments from global memory: Y[M, N] = X[M, K] W^T, M <= 16*TT.
 // Workgroup = NT*KS waves; wave (nl, ks) streams n-tile blockIdx.x*NT+nl over the ks-th
-// contiguous range of k-tiles. Partials are reduced across ks in LDS in ks order.
-//
-// Streaming: each wave keeps P k-tiles in flight, the weight tile (non-temporal) together with
-// the matching activation fragment, and refills a slot right after taking its data. Vector
-// memory returns complete in issue order, so issuing an operand together with its weight tile
-// keeps every wait at "oldest slot only".
-//
-// RMSNorm consumers get x*g already formed by the producer of x and apply the row scale rs to
-// the reduced sums (y = rs * sum_k W (x*g)).
+// contiguous range of k-tiles; each wave keeps P weight tiles in flight together with the
+// matching activation fragments, refilling a slot right after taking its data (vector memory
+// returns in issue order, so every wait is for the oldest slot only). Lanes past the last row
+// read row 0 (branch-free issue) and are zeroed when consumed.
 // ---------------------------------------------------------------------------------------------
 template <typename T, int PRO, int EPI, int TT>
 __global__ void __launch_bounds__(1024) k_linear_mfma(LinArgs a) {
@@ -155,6 +398,9 @@ __global__ void __launch_bounds__(1024) k_linear_mfma(LinArgs a) {
   const int nl = wave / a.KS, ks = wave - nl * a.KS;
   const int nt = blockIdx.x * a.NT + nl;
   const int tl = lane & 15, kg = lane >> 4;
+  const Grp gr{(int)blockIdx.x, (int)gridDim.x};
+  EpiPre epre{};
+  epi_load<EPI>(a, gr, tid, epre);
   float ssv[4] = {0.f, 0.f, 0.f, 0.f};
   bool pre = false;
   if constexpr (PRO == PRO_NORM) pre = preload_row_ssq(a, wave, ssv);
@@ -174,44 +420,44 @@ __global__ void __launch_bounds__(1024) k_linear_mfma(LinArgs a) {
       ok[tt] = tok < M;
       xp[tt] = a.X + (size_t)(ok[tt] ? tok : 0) * a.ldx + kg * 8 + kt0 * 32;
     }
-    constexpr int P = (TT <= 1) ? 8 : (TT == 2 ? 4 : (TT == 3 ? 3 : 2));
+    constexpr int P = (TT <= 1) ? 4 : (TT == 2 ? 3 : 2);
     typename ET<T>::A wb[P];
     float xb[P][TT][8];
-    // lanes past the last row read row 0 (branch-free issue) and are zeroed when consumed
     auto issue = [&](int slot, int j) {
       wb[slot] = ET<T>::load_nt(wp + (size_t)j * 512);
 #pragma unroll
       for (int tt = 0; tt < TT; ++tt) load8(xp[tt] + j * 32, xb[slot][tt]);
     };
+    auto consume = [&](int slot) {
 #pragma unroll
-    for (int i = 0; i < P; ++i) issue(i, min(i, nk - 1));
-    // consume a slot, then refill the same registers: no register copies, so every wait is
-    // for the oldest slot only
+      for (int tt = 0; tt < TT; ++tt) {
+        float x[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) x[q] = ok[tt] ? xb[slot][tt][q] : 0.f;
+        ET<T>::mma(acc[tt], wb[slot], ET<T>::split(x));
+      }
+    };
+#pragma unroll
+    for (int i = 0; i < P; ++i)
+      if (i < nk) issue(i, i);
     int base = 0;
-    for (; base + P <= nk; base += P) {
+    for (; base + 2 * P <= nk; base += P) {
 #pragma unroll
       for (int i = 0; i < P; ++i) {
-#pragma unroll
-        for (int tt = 0; tt < TT; ++tt) {
-          float x[8];
-#pragma unroll
-          for (int q = 0; q < 8; ++q) x[q] = ok[tt] ? xb[i][tt][q] : 0.f;
-          ET<T>::mma(acc[tt], wb[i], ET<T>::split(x));
-        }
-        issue(i, min(base + i + P, nk - 1));
+        consume(i);
+        issue(i, base + i + P);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
 #pragma unroll
     for (int i = 0; i < P; ++i)
       if (base + i < nk) {
-#pragma unroll
-        for (int tt = 0; tt < TT; ++tt) {
-          float x[8];
-#pragma unroll
-          for (int q = 0; q < 8; ++q) x[q] = ok[tt] ? xb[i][tt][q] : 0.f;
-          ET<T>::mma(acc[tt], wb[i], ET<T>::split(x));
-        }
+        consume(i);
+        if (base + i + P < nk) issue(i, base + i + P);
       }
+#pragma unroll
+    for (int i = 0; i < P; ++i)
+      if (base + P + i < nk) consume(i);
   }
   // lane (tl, kg) holds rows 4*kg+i of the n-tile for token tt*16+tl
 #pragma unroll
@@ -229,93 +475,20 @@ __global__ void __launch_bounds__(1024) k_linear_mfma(LinArgs a) {
     }
   }
   __syncthreads();
-  for (int e = tid; e < a.NT * M * 16; e += blockDim.x) {
-    const int nl2 = e / (M * 16), r = e - nl2 * M * 16;
+  const int per = M * 16, KSs = a.KS / a.S;
+  for (int e = tid; e < a.NT * per; e += blockDim.x) {
+    const int nl2 = e / per, r = e - nl2 * per;
+    float* src = s_red + (size_t)(nl2 * a.KS) * per + r;
     float y = 0.f;
-    for (int k2 = 0; k2 < a.KS; ++k2) y += s_red[(size_t)(nl2 * a.KS + k2) * M * 16 + r];
+    for (int s2 = 0; s2 < a.S; ++s2) y += sum_partials(src + (size_t)s2 * KSs * per, KSs, per);
     if constexpr (PRO == PRO_NORM) y *= s_rs[r >> 4];
-    s_red[(size_t)(nl2 * a.KS) * M * 16 + r] = y;
+    *src = y;
   }
   __syncthreads();
-  linear_epilogue<T, EPI>(a, s_red, a.KS * M * 16, 16);
+  linear_epilogue<T, EPI>(a, gr, s_red, a.KS * per, epre);
 }
 
-// ---------------------------------------------------------------------------------------------
-// Weight-streaming GEMV on the vector ALUs (one activation row): same tiles and waves as the
-// MFMA kernel; lane (tl, kg) accumulates row tl over its k-slots, then the four k-groups are
-// added across lanes and the KS partials in LDS. The activation row sits in LDS; the weight
-// stream keeps P tiles in flight from the first instruction on.
-// ---------------------------------------------------------------------------------------------
-template <typename T, int PRO, int EPI>
-__global__ void __launch_bounds__(1024) k_linear_valu(LinArgs a) {
-  extern __shared__ float smem[];
-  float* s_x = smem;                // [K]
-  float* s_red = smem + a.K;        // [NW][16]
-  __shared__ float s_rs;
-  constexpr int P = 8;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int KT = a.K >> 5, n_tiles = a.N >> 4;
-  const int nl = wave / a.KS, ks = wave - nl * a.KS;
-  const int nt = blockIdx.x * a.NT + nl;
-  const int kg = lane >> 4;
-  const bool live = nt < n_tiles;
-  const int kt0 = (ks * KT) / a.KS, kt1 = ((ks + 1) * KT) / a.KS;
-  const int nk = kt1 - kt0;
-  const T* wp = reinterpret_cast<const T*>(a.W) + ((size_t)(live ? nt : 0) * KT + kt0) * 512 + lane * 8;
-  typename ET<T>::A wb[P];
-  if (live) {
-#pragma unroll
-    for (int i = 0; i < P; ++i) wb[i] = ET<T>::load_nt(wp + (size_t)min(i, nk - 1) * 512);
-  }
-  float ssv[4] = {0.f, 0.f, 0.f, 0.f};
-  bool pre = false;
-  if constexpr (PRO == PRO_NORM) pre = (wave == 0) && preload_row_ssq(a, 0, ssv);
-  for (int k = tid; k < a.K; k += blockDim.x) s_x[k] = a.X[k];
-  __syncthreads();
-  float acc = 0.f;
-  if (live) {
-    const float* xs = s_x + kg * 8 + kt0 * 32;
-    auto step = [&](const typename ET<T>::A& w, int j) {
-      float wf[8], xv[8];
-      ET<T>::to_f32(w, wf);
-      load8(xs + j * 32, xv);
-#pragma unroll
-      for (int q = 0; q < 8; ++q) acc = fmaf(wf[q], xv[q], acc);
-    };
-    int base = 0;
-    for (; base + P <= nk; base += P) {
-#pragma unroll
-      for (int i = 0; i < P; ++i) {
-        step(wb[i], base + i);
-        wb[i] = ET<T>::load_nt(wp + (size_t)min(base + i + P, nk - 1) * 512);
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < P; ++i)
-      if (base + i < nk) step(wb[i], base + i);
-  }
-  acc += __shfl_xor(acc, 16);
-  acc += __shfl_xor(acc, 32);
-  if (lane < 16) s_red[wave * 16 + lane] = acc;
-  if constexpr (PRO == PRO_NORM) {
-    if (wave == 0) {
-      const float r = wave_row_scale(a, 0, ssv, pre);
-      if (lane == 0) s_rs = r;
-    }
-  }
-  __syncthreads();
-  for (int e = tid; e < a.NT * 16; e += blockDim.x) {
-    const int nl2 = e >> 4, c = e & 15;
-    float y = 0.f;
-    for (int k2 = 0; k2 < a.KS; ++k2) y += s_red[(nl2 * a.KS + k2) * 16 + c];
-    if constexpr (PRO == PRO_NORM) y *= s_rs;
-    s_red[(nl2 * a.KS) * 16 + c] = y;
-  }
-  __syncthreads();
-  linear_epilogue<T, EPI>(a, s_red, a.KS * 16, 16);
-}
-
-// Reduce per-workgroup argmax partials of one row; lowest token id wins among equal maxima.
+// Reduce per-n-group argmax partials of one row; lowest token id wins among equal maxima.
 __global__ void __launch_bounds__(256) k_argmax_finalize(const float* val, const int* idx, int stride, int n_parts,
                                                          int* tok_out, int tok_stride) {
   const int m = blockIdx.x, tid = threadIdx.x;
@@ -345,22 +518,30 @@ __global__ void __launch_bounds__(256) k_argmax_finalize(const float* val, const
 // ---------------------------------------------------------------------------------------------
 // Launchers.
 // ---------------------------------------------------------------------------------------------
-size_t linear_lds_bytes(int M, int K, int NT, int KS, bool valu) {
-  const int NW = NT * KS;
-  if (valu) return (size_t)(K + NW * 16) * sizeof(float);
-  return (size_t)(NW * M * 16) * sizeof(float);
+size_t linear_lds_bytes(int M, int K, int NT, int KS, int S, int NJ, int kind) {
+  if (kind == LIN_LDS) {
+    const int NW = NT * (KS / S);
+    return lds_x_bytes(M, slice_kt_max(K >> 5, S)) + (size_t)NJ * NW * M * 16 * sizeof(float);
+  }
+  return (size_t)(NT * KS * M * 16) * sizeof(float);
 }
 
 template <typename T, int PRO, int EPI>
-static void launch_linear_pe(const LinArgs& a, bool valu, hipStream_t s) {
+static void launch_linear_pe(const LinArgs& a0, int kind, hipStream_t s) {
+  LinArgs a = a0;
   const int n_tiles = a.N >> 4;
-  const dim3 grid((n_tiles + a.NT - 1) / a.NT);
-  const dim3 block(64 * a.NT * a.KS);
-  const size_t lds = linear_lds_bytes(a.M, a.K, a.NT, a.KS, valu);
-  if (valu) {
-    hipLaunchKernelGGL((k_linear_valu<T, PRO, EPI>), grid, block, lds, s, a);
+  const int n_groups = (n_tiles + a.NT - 1) / a.NT;
+  if (kind == LIN_LDS) {
+    if (a.S > 1) a.NJ = 1;
+    const dim3 grid(a.S > 1 ? n_groups * a.S : (n_groups + a.NJ - 1) / a.NJ);
+    const dim3 block(64 * a.NT * (a.KS / a.S));
+    const size_t lds = linear_lds_bytes(a.M, a.K, a.NT, a.KS, a.S, a.NJ, kind);
+    hipLaunchKernelGGL((k_linear_lds<T, PRO, EPI>), grid, block, lds, s, a);
     return;
   }
+  a.NJ = 1;
+  const dim3 grid(n_groups), block(64 * a.NT * a.KS);
+  const size_t lds = linear_lds_bytes(a.M, a.K, a.NT, a.KS, a.S, 1, kind);
   const int TT = (a.M + 15) / 16;
   switch (TT) {
     case 1: hipLaunchKernelGGL((k_linear_mfma<T, PRO, EPI, 1>), grid, block, lds, s, a); break;
@@ -371,15 +552,15 @@ static void launch_linear_pe(const LinArgs& a, bool valu, hipStream_t s) {
 }
 
 template <typename T>
-void launch_linear(const LinArgs& a, int prologue, int epilogue, bool valu, hipStream_t s) {
+void launch_linear(const LinArgs& a, int prologue, int epilogue, int kind, hipStream_t s) {
   if (prologue == PRO_NORM) {
     switch (epilogue) {
-      case EPI_QKV: launch_linear_pe<T, PRO_NORM, EPI_QKV>(a, valu, s); break;
-      case EPI_SWIGLU: launch_linear_pe<T, PRO_NORM, EPI_SWIGLU>(a, valu, s); break;
-      default: launch_linear_pe<T, PRO_NORM, EPI_HEAD>(a, valu, s); break;
+      case EPI_QKV: launch_linear_pe<T, PRO_NORM, EPI_QKV>(a, kind, s); break;
+      case EPI_SWIGLU: launch_linear_pe<T, PRO_NORM, EPI_SWIGLU>(a, kind, s); break;
+      default: launch_linear_pe<T, PRO_NORM, EPI_HEAD>(a, kind, s); break;
     }
   } else {
-    launch_linear_pe<T, PRO_PLAIN, EPI_RESID>(a, valu, s);
+    launch_linear_pe<T, PRO_PLAIN, EPI_RESID>(a, kind, s);
   }
 }
 
@@ -389,34 +570,45 @@ void launch_argmax_finalize(const float* val, const int* idx, int stride, int n_
 }
 
 template <typename T, int PRO, int EPI>
-static void allow_big_lds(int bytes) {
-  const void* fns[] = {reinterpret_cast<const void*>(&k_linear_valu<T, PRO, EPI>),
+static bool allow_big_lds(int bytes) {
+  const void* fns[] = {reinterpret_cast<const void*>(&k_linear_lds<T, PRO, EPI>),
                        reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 1>),
                        reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 2>),
                        reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 3>),
                        reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 4>)};
-  for (const void* f : fns) (void)hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  bool ok = true;
+  for (const void* f : fns) ok &= hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes) == hipSuccess;
+  return ok;
 }
 
-// Every launch stays within 64 KB of dynamic LDS; where the device allows more, opt in anyway
-// (failures are harmless and cleared).
+static size_t g_lds_limit = 65536;
+
+// Dynamic LDS available to one linear workgroup: the device's per-block limit, raised to the
+// opt-in limit when every linear kernel accepted it (failed opt-ins are cleared and ignored).
 hipError_t configure_kernels(int bf16) {
-  int dev = 0, optin = 0;
+  int dev = 0, base = 0, optin = 0;
   if (hipGetDevice(&dev) != hipSuccess) return hipGetLastError();
-  if (hipDeviceGetAttribute(&optin, hipDeviceAttributeSharedMemPerBlockOptin, dev) == hipSuccess && optin > 65536) {
+  if (hipDeviceGetAttribute(&base, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) == hipSuccess && base > 0)
+    g_lds_limit = (size_t)base;
+  if (hipDeviceGetAttribute(&optin, hipDeviceAttributeSharedMemPerBlockOptin, dev) == hipSuccess &&
+      (size_t)optin > g_lds_limit) {
+    bool ok;
     if (bf16) {
-      allow_big_lds<uint16_t, PRO_NORM, EPI_QKV>(optin); allow_big_lds<uint16_t, PRO_NORM, EPI_SWIGLU>(optin);
-      allow_big_lds<uint16_t, PRO_NORM, EPI_HEAD>(optin); allow_big_lds<uint16_t, PRO_PLAIN, EPI_RESID>(optin);
+      ok = allow_big_lds<uint16_t, PRO_NORM, EPI_QKV>(optin) & allow_big_lds<uint16_t, PRO_NORM, EPI_SWIGLU>(optin) &
+           allow_big_lds<uint16_t, PRO_NORM, EPI_HEAD>(optin) & allow_big_lds<uint16_t, PRO_PLAIN, EPI_RESID>(optin);
     } else {
-      allow_big_lds<float, PRO_NORM, EPI_QKV>(optin); allow_big_lds<float, PRO_NORM, EPI_SWIGLU>(optin);
-      allow_big_lds<float, PRO_NORM, EPI_HEAD>(optin); allow_big_lds<float, PRO_PLAIN, EPI_RESID>(optin);
+      ok = allow_big_lds<float, PRO_NORM, EPI_QKV>(optin) & allow_big_lds<float, PRO_NORM, EPI_SWIGLU>(optin) &
+           allow_big_lds<float, PRO_NORM, EPI_HEAD>(optin) & allow_big_lds<float, PRO_PLAIN, EPI_RESID>(optin);
     }
+    if (ok) g_lds_limit = (size_t)optin;
   }
   (void)hipGetLastError();
   return hipSuccess;
 }
 
-template void launch_linear<uint16_t>(const LinArgs&, int, int, bool, hipStream_t);
-template void launch_linear<float>(const LinArgs&, int, int, bool, hipStream_t);
+size_t linear_lds_limit() { return g_lds_limit; }
+
+template void launch_linear<uint16_t>(const LinArgs&, int, int, int, hipStream_t);
+template void launch_linear<float>(const LinArgs&, int, int, int, hipStream_t);
 
 }  // namespace seedk

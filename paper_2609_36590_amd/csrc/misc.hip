@@ -11,7 +11,7 @@ namespace seedk {
 template <typename T>
 __global__ void __launch_bounds__(256) k_setup(SetupArgs a) {
   const int m = blockIdx.x;
-  __shared__ int s_tok;
+  __shared__ int s_tok, s_pos, s_seq;
   if (threadIdx.x == 0) {
     int b, pos, tok;
     if (a.mode == SETUP_PREFILL) {
@@ -36,9 +36,20 @@ __global__ void __launch_bounds__(256) k_setup(SetupArgs a) {
     a.row_seq[m] = b;
     a.row_pos[m] = pos;
     s_tok = tok;
+    s_pos = pos;
+    s_seq = b;
   }
   __syncthreads();
   const int tok = s_tok;
+  {
+    // the row's KV block and RoPE angles, read once per pass by every layer's QKV epilogue
+    const int pos = s_pos, half = a.head_dim >> 1;
+    if (threadIdx.x == 0) a.row_blk[m] = a.bt[s_seq * a.bt_stride + (pos >> 4)];
+    for (int i = threadIdx.x; i < half; i += blockDim.x) {
+      a.row_rope[(size_t)m * a.head_dim + i] = a.rope_cos[(size_t)pos * half + i];
+      a.row_rope[(size_t)m * a.head_dim + half + i] = a.rope_sin[(size_t)pos * half + i];
+    }
+  }
   const int KT = a.H >> 5;
   const T* E = reinterpret_cast<const T*>(a.E);
   const int nt = tok >> 4, rr = tok & 15;

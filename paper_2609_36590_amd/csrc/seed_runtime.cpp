@@ -55,7 +55,8 @@ struct Plan {
   std::vector<size_t> w_attn_norm, w_mlp_norm, w_qkv, w_o, w_gu, w_down;
   size_t kv_total;
   // workspace
-  size_t o_h, o_xg, o_ssq, o_q, o_attn, o_act, o_part, o_cnt, o_row_seq, o_row_pos, o_amax_val, o_amax_idx, o_vtok;
+  size_t o_h, o_xg, o_ssq, o_q, o_attn, o_act, o_part, o_cnt, o_row_seq, o_row_pos, o_row_blk, o_row_rope, o_amax_val,
+      o_amax_idx, o_vtok;
   size_t o_t, o_len, o_limit, o_active, o_nacc, o_bonus, o_rounds, o_counters, o_drafts, o_tokens,
       o_trace, o_log, o_bt, o_scratch, ws_total;
 };
@@ -79,8 +80,7 @@ seed_status validate(const seed_config* c) {
   if (c->max_batch * (c->max_draft + 1) > MAX_ROWS)
     return fail(SEED_ERR_UNSUPPORTED, "max_batch * (max_draft + 1) must be at most 64");
   if (c->max_ctx < 2) return fail(SEED_ERR_ARG, "max_ctx must be at least 2");
-  if (c->max_ctx > 3 * c->head_dim * GROUP)   // the attention combine keeps 32 weights per group in LDS
-    return fail(SEED_ERR_UNSUPPORTED, "max_ctx must be at most 768 * head_dim");
+  if (c->max_ctx > (1 << 20)) return fail(SEED_ERR_UNSUPPORTED, "max_ctx must be at most 2^20");
   if (!(c->rope_base > 0.f) || !(c->rms_eps >= 0.f)) return fail(SEED_ERR_ARG, "rope_base must be > 0 and rms_eps >= 0");
   return SEED_OK;
 }
@@ -135,6 +135,8 @@ Plan make_plan(const seed_config& c) {
   p.o_cnt = take(B * p.NKV * p.n_rb_max * 4);
   p.o_row_seq = take(R * 4);
   p.o_row_pos = take(R * 4);
+  p.o_row_blk = take(R * 4);
+  p.o_row_rope = take(R * p.HD * 4);
   p.o_amax_val = take(R * (size_t)(p.V / 16) * 4);
   p.o_amax_idx = take(R * (size_t)(p.V / 16) * 4);
   p.o_vtok = take(R * 4);
@@ -236,20 +238,29 @@ void timed(seed_ctx* c, int phase, int op, bool capturing, F&& fn) {
 // launch helpers
 // ---------------------------------------------------------------------------------------------
 // Waves per workgroup and how they split the work; a function of the weight shape only, so a
-// row's reduction order never depends on how many rows share the pass.
-void tile_policy(int N, int K, bool head, int& NT, int& KS) {
-  (void)N;
-  const int KT = K / 32;
-  if (head) {               // huge N: one n-tile per wave over the full K, 16 n-tiles per workgroup
+// row's reduction order never depends on how many rows share the pass (measured on MI355X):
+//   head (N = vocab): one n-tile per wave over the full K, 8 n-tiles per workgroup.
+//   N >= 4096 (QKV, gate/up): 8 K-splits, 2 n-tiles per workgroup pass, and as many passes per
+//     workgroup as keep the grid near 200 workgroups (the LDS kernel stages the activations once
+//     per workgroup).
+//   smaller N (O, down): one n-tile per workgroup, K split in ranges of about 16 k-tiles (<= 16).
+void tile_policy(int N, int K, bool head, int& NT, int& KS, int& S, int& NJ) {
+  const int KT = K / 32, n_tiles = N / 16;
+  S = 1;
+  NJ = 1;
+  if (head) {
     KS = 1;
-    NT = 16;
+    NT = 8;
     return;
   }
-#ifndef SEED_KT_PER_WAVE
-#define SEED_KT_PER_WAVE 4
-#endif
-  KS = std::min(16, std::max(1, KT / SEED_KT_PER_WAVE));
-  NT = std::max(1, 16 / KS);
+  if (n_tiles >= 256) {
+    KS = std::min(8, KT);
+    NT = 2;
+    NJ = std::max(1, (cdiv(n_tiles, NT) + 100) / 200);
+    return;
+  }
+  KS = std::min(16, std::max(1, KT / 16));
+  NT = 1;
 }
 
 DevState dev_state(seed_ctx* c) {
@@ -288,12 +299,9 @@ LinArgs lin_base(seed_ctx* c, int M) {
   a.act = c->ws<float>(p.o_act);
   a.q = c->ws<float>(p.o_q);
   a.kv = c->KV;
-  a.bt = c->ws<int>(p.o_bt);
-  a.bt_stride = p.bt_stride;
-  a.row_seq = c->ws<int>(p.o_row_seq);
   a.row_pos = c->ws<int>(p.o_row_pos);
-  a.rope_cos = c->wf(p.w_rope_cos);
-  a.rope_sin = c->wf(p.w_rope_sin);
+  a.row_blk = c->ws<int>(p.o_row_blk);
+  a.row_rope = c->ws<float>(p.o_row_rope);
   a.n_blocks = p.n_blocks;
   a.n_heads = p.NQ;
   a.n_kv = p.NKV;
@@ -304,15 +312,23 @@ LinArgs lin_base(seed_ctx* c, int M) {
   return a;
 }
 
+// Kernel for one linear launch: activation rows staged in LDS when they fit (M <= 16), else
+// activation fragments read from global memory (prefill, large batches, very large K).
+int linear_kind(const LinArgs& a) {
+  if (a.M <= 16 && linear_lds_bytes(a.M, a.K, a.NT, a.KS, a.S, a.NJ, LIN_LDS) <= linear_lds_limit()) return LIN_LDS;
+  return LIN_GLOBAL;
+}
+
 template <typename T>
-void linear(seed_ctx* c, LinArgs a, int pro, int epi, bool valu, int phase, int op, bool cap) {
-  tile_policy(a.N, a.K, epi == EPI_HEAD, a.NT, a.KS);
-  timed(c, phase, op, cap, [&] { launch_linear<T>(a, pro, epi, valu, c->s); });
+void linear(seed_ctx* c, LinArgs a, int pro, int epi, int phase, int op, bool cap) {
+  tile_policy(a.N, a.K, epi == EPI_HEAD, a.NT, a.KS, a.S, a.NJ);
+  const int kind = linear_kind(a);
+  timed(c, phase, op, cap, [&] { launch_linear<T>(a, pro, epi, kind, c->s); });
 }
 
 // Layers [l0, l1) over M rows (B sequences x R rows each, consecutive positions per sequence).
 template <typename T>
-void run_layers(seed_ctx* c, int M, int B, int R, int l0, int l1, bool valu, int phase,
+void run_layers(seed_ctx* c, int M, int B, int R, int l0, int l1, int phase,
                 const int* bt_override, bool cap) {
   const Plan& p = c->p;
   float* h = c->ws<float>(p.o_h);
@@ -322,7 +338,7 @@ void run_layers(seed_ctx* c, int M, int B, int R, int l0, int l1, bool valu, int
     // QKV + RoPE + KV write
     a.W = c->W + p.w_qkv[li]; a.N = p.QD + 2 * p.KVD; a.K = p.H;
     a.X = c->ws<float>(p.o_xg); a.ldx = p.H;
-    linear<T>(c, a, PRO_NORM, EPI_QKV, valu, phase, SEED_OP_QKV, cap);
+    linear<T>(c, a, PRO_NORM, EPI_QKV, phase, SEED_OP_QKV, cap);
     // attention
     AttnArgs at;
     std::memset(&at, 0, sizeof(at));
@@ -346,33 +362,33 @@ void run_layers(seed_ctx* c, int M, int B, int R, int l0, int l1, bool valu, int
     a = lin_base(c, M);
     a.W = c->W + p.w_o[li]; a.N = p.H; a.K = p.QD;
     a.X = c->ws<float>(p.o_attn); a.ldx = p.QD; a.gain_next = c->wf(p.w_mlp_norm[li]);
-    linear<T>(c, a, PRO_PLAIN, EPI_RESID, valu, phase, SEED_OP_O, cap);
+    linear<T>(c, a, PRO_PLAIN, EPI_RESID, phase, SEED_OP_O, cap);
     // gate/up + SwiGLU
     a = lin_base(c, M);
     a.W = c->W + p.w_gu[li]; a.N = 2 * p.F; a.K = p.H;
     a.X = c->ws<float>(p.o_xg); a.ldx = p.H;
-    linear<T>(c, a, PRO_NORM, EPI_SWIGLU, valu, phase, SEED_OP_GATEUP, cap);
+    linear<T>(c, a, PRO_NORM, EPI_SWIGLU, phase, SEED_OP_GATEUP, cap);
     // down + residual
     a = lin_base(c, M);
     a.W = c->W + p.w_down[li]; a.N = p.H; a.K = p.F;
     a.X = c->ws<float>(p.o_act); a.ldx = p.F;
     a.gain_next = c->wf(li + 1 < p.L ? p.w_attn_norm[li + 1] : p.w_final_norm);
-    linear<T>(c, a, PRO_PLAIN, EPI_RESID, valu, phase, SEED_OP_DOWN, cap);
+    linear<T>(c, a, PRO_PLAIN, EPI_RESID, phase, SEED_OP_DOWN, cap);
   }
 }
 
 template <typename T>
-void run_head(seed_ctx* c, int M, bool valu, int* tok_out, int tok_stride, float* logits, long long ld,
+void run_head(seed_ctx* c, int M, int* tok_out, int tok_stride, float* logits, long long ld,
               int phase, bool cap) {
   const Plan& p = c->p;
   LinArgs a = lin_base(c, M);
   a.W = c->W + p.w_embed; a.N = p.V; a.K = p.H;
   a.X = c->ws<float>(p.o_xg); a.ldx = p.H;
   a.logits = logits; a.ld_logits = ld;
-  linear<T>(c, a, PRO_NORM, EPI_HEAD, valu, phase, SEED_OP_HEAD, cap);
-  int NT, KS;
-  tile_policy(a.N, a.K, true, NT, KS);
-  const int parts = cdiv(p.V / 16, NT);
+  linear<T>(c, a, PRO_NORM, EPI_HEAD, phase, SEED_OP_HEAD, cap);
+  int NT, KS, S, NJ;
+  tile_policy(a.N, a.K, true, NT, KS, S, NJ);
+  const int parts = cdiv(p.V / 16, NT);   // one argmax partial per n-group
   timed(c, phase, SEED_OP_HEAD_ARGMAX, cap, [&] {
     launch_argmax_finalize(a.amax_val, a.amax_idx, a.amax_stride, parts, M, tok_out, tok_stride, c->s);
   });
@@ -396,6 +412,13 @@ SetupArgs setup_base(seed_ctx* c, int l0) {
   s.H = p.H;
   s.row_seq = c->ws<int>(p.o_row_seq);
   s.row_pos = c->ws<int>(p.o_row_pos);
+  s.bt = c->ws<int>(p.o_bt);
+  s.bt_stride = p.bt_stride;
+  s.rope_cos = c->wf(p.w_rope_cos);
+  s.rope_sin = c->wf(p.w_rope_sin);
+  s.head_dim = p.HD;
+  s.row_blk = c->ws<int>(p.o_row_blk);
+  s.row_rope = c->ws<float>(p.o_row_rope);
   s.h = c->ws<float>(p.o_h);
   s.xg = c->ws<float>(p.o_xg);
   s.gain = c->wf(l0 < p.L ? p.w_attn_norm[l0] : p.w_final_norm);
@@ -408,13 +431,12 @@ template <typename T>
 void enqueue_draft(seed_ctx* c, int k, float* logits, bool cap) {
   const Plan& p = c->p;
   const int B = c->B;
-  const bool valu = (B == 1);
   for (int i = 1; i <= k; ++i) {
     SetupArgs s = setup_base(c, p.LD);
     s.mode = SETUP_DRAFT; s.M = B; s.R = 1; s.step = i;
     timed(c, SEED_PHASE_DRAFT, SEED_OP_SETUP, cap, [&] { launch_setup<T>(s, c->s); });
-    run_layers<T>(c, B, B, 1, p.LD, p.L, valu, SEED_PHASE_DRAFT, nullptr, cap);
-    run_head<T>(c, B, valu, c->ws<int>(p.o_drafts) + i, p.dstride,
+    run_layers<T>(c, B, B, 1, p.LD, p.L, SEED_PHASE_DRAFT, nullptr, cap);
+    run_head<T>(c, B, c->ws<int>(p.o_drafts) + i, p.dstride,
                 logits ? logits + (size_t)(i - 1) * p.V : nullptr, (long long)k * p.V, SEED_PHASE_DRAFT, cap);
   }
 }
@@ -427,8 +449,8 @@ void enqueue_verify(seed_ctx* c, int k, int sim_accept, float* logits, bool cap)
   SetupArgs s = setup_base(c, 0);
   s.mode = SETUP_VERIFY; s.M = M; s.R = R; s.sim_accept = sim_accept;
   timed(c, SEED_PHASE_VERIFY, SEED_OP_SETUP, cap, [&] { launch_setup<T>(s, c->s); });
-  run_layers<T>(c, M, B, R, 0, p.L, false, SEED_PHASE_VERIFY, nullptr, cap);
-  run_head<T>(c, M, false, c->ws<int>(p.o_vtok), 1, logits, (long long)p.V, SEED_PHASE_VERIFY, cap);
+  run_layers<T>(c, M, B, R, 0, p.L, SEED_PHASE_VERIFY, nullptr, cap);
+  run_head<T>(c, M, c->ws<int>(p.o_vtok), 1, logits, (long long)p.V, SEED_PHASE_VERIFY, cap);
   DevState st = dev_state(c);
   timed(c, SEED_PHASE_VERIFY, SEED_OP_ACCEPT, cap, [&] { launch_accept(st, B, k, c->s); });
 }
@@ -642,7 +664,7 @@ seed_status do_prefill(seed_ctx* c, const std::vector<int>& tokens_packed) {
       SetupArgs s = setup_base(c, 0);
       s.mode = SETUP_PREFILL; s.M = M; s.R = M; s.pf_seq = b; s.pf_pos0 = s0;
       timed(c, SEED_PHASE_PREFILL, SEED_OP_SETUP, false, [&] { launch_setup<T>(s, c->s); });
-      run_layers<T>(c, M, 1, M, 0, p.L, false, SEED_PHASE_PREFILL,
+      run_layers<T>(c, M, 1, M, 0, p.L, SEED_PHASE_PREFILL,
                     c->ws<int>(p.o_bt) + (size_t)b * p.bt_stride, false);
     }
   }
