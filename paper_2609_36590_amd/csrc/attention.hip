@@ -1,17 +1,19 @@
 // Paged split-KV attention on MFMA for the verify, draft and prefill passes.
 //
-// One workgroup = 4 waves = one group of 256 absolute positions (4 chunks of 64) for one
-// (sequence b, KV head h, row-block rb). The queries of a row-block (G query heads x RB rows,
+// k_attention: one workgroup = 4 waves = one group of 256 absolute positions (4 chunks of 64) for
+// one (sequence b, KV head h, row-block rb). The queries of a row-block (G query heads x RB rows,
 // <= 32) are the MFMA B operand. Per chunk, a wave computes S^T = K Q^T with the paged K block
 // rows as the A operand, masks positions later than each query's own, takes the chunk softmax in
-// base 2, and forms O^T = V^T P^T with the transposed V block as the A operand. All K/V loads of
-// the chunk are issued before any arithmetic, so a wave waits for one memory round trip.
+// base 2, and forms O^T = V^T P^T with the transposed V block as the A operand. The wave issues
+// its block-table reads together with the row positions, then all K/V loads of its chunk and the
+// query loads, so it waits for two memory round trips. The group's 4 chunks are merged left to
+// right in LDS and written as one partial (o, m, l), or as the final output when the rows see a
+// single group.
 //
-// Merge order is a fixed function of absolute positions: chunks are merged left to right inside
-// the group (LDS), and the last workgroup of (b, h, rb) to finish merges the group partials left
-// to right. A chunk or group with no visible position is an exact identity of the merge, so a
-// query's result depends only on the positions it attends to, not on how many rows share the
-// pass (verify rows vs plain greedy decoding give bit-identical outputs).
+// k_attn_combine merges the group partials of each query left to right. A chunk or group with no
+// visible position is an exact identity of the merge, so a query's result depends only on the
+// positions it attends to, not on how many rows share the pass (verify rows vs plain greedy
+// decoding give bit-identical outputs).
 //
 // Position tile pt (16 positions) of chunk base P0, MFMA row r <-> position
 //   P0 + 32*(pt>>1) + 8*(r>>2) + (r&3) + 4*(pt&1),
@@ -19,20 +21,21 @@
 // exactly the k-slot layout O^T needs for P^T: no cross-lane shuffle of P.
 #include "device_common.h"
 
+#include <algorithm>
+
 namespace seedk {
 
 static constexpr int ATT_CHUNK = 64;
 static constexpr int ATT_WAVES = 4;
 static constexpr int ATT_GROUP = ATT_CHUNK * ATT_WAVES;
 
-template <typename T, int HD>
+template <typename T, int HD, int QT>
 __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
   constexpr int DS = HD / 32;    // 32-dim steps of S^T
   constexpr int DT = HD / 16;    // 16-dim tiles of O^T
   constexpr int PS = HD + 4;     // floats per query vector in a group partial
   __shared__ float s_o[ATT_WAVES - 1][32][HD];
   __shared__ float s_ml[ATT_WAVES - 1][32][2];
-  __shared__ int s_last;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, tl = lane & 15, kg = lane >> 4;
   const int g = blockIdx.x;
   const int h = blockIdx.y % a.n_kv, rb = blockIdx.y / a.n_kv;
@@ -42,70 +45,85 @@ __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
   const int nr = min(a.RB, a.R - r0);
   const int nqv = nr * a.G;
   const int mrow0 = b * a.R + r0;
-  const int maxpos = a.row_pos[mrow0 + nr - 1];
-  const int n_groups = maxpos / ATT_GROUP + 1;
-  if (g >= n_groups) return;
-  const int QT = nqv > 16 ? 2 : 1;
   const int qstride = a.n_heads * HD;
   const int P0 = (g * ATT_WAVES + wave) * ATT_CHUNK;
-  const bool live = P0 <= maxpos;
-
   const T* kvp = reinterpret_cast<const T*>(a.kv);
-  const int* btp = a.bt + b * a.bt_stride;
+  const int* btp = a.bt + b * a.bt_stride;   // the grid covers exactly bt_stride * 16 positions
   const size_t layer_base = (size_t)a.layer * a.n_blocks;
 
-  // ---- issue the chunk's K and V loads first ----
+  // ---- round trip 1: the last row's position and this wave's block-table entries ----
+  const int maxpos = a.row_pos[mrow0 + nr - 1];
+  int kblk[4], vblk[2];
+#pragma unroll
+  for (int pt = 0; pt < 4; ++pt) kblk[pt] = btp[(P0 + 32 * (pt >> 1) + 8 * (tl >> 2) + (tl & 3) + 4 * (pt & 1)) >> 4];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) vblk[s] = btp[(P0 + 32 * s + 8 * kg) >> 4];
+  // queries (lane column qv = qt*16 + tl, k-slots d = ds*32 + kg*8 + j) and their positions:
+  // loaded branch-free from a valid row, masked when converted
+  float qraw[QT][DS][8];
+  int qpos[QT];
+  bool qok[QT];
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt) {
+    const int qv = qt * 16 + tl;
+    qok[qt] = qv < nqv;
+    const int rl = qok[qt] ? qv / a.G : 0, gq = qok[qt] ? qv - rl * a.G : 0;
+    qpos[qt] = a.row_pos[mrow0 + rl];
+    const float* qp = a.q + (size_t)(mrow0 + rl) * qstride + (h * a.G + gq) * HD + kg * 8;
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds) load8(qp + ds * 32, qraw[qt][ds]);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  const int n_groups = maxpos / ATT_GROUP + 1;
+  if (g >= n_groups) return;
+  const bool live = P0 <= maxpos;
+
+  // ---- round trip 2: the chunk's K and V, then the queries ----
   typename ET<T>::A kf[4][DS];
   typename ET<T>::A vf[2][DT];
   if (live) {
 #pragma unroll
     for (int pt = 0; pt < 4; ++pt) {
       const int pos = P0 + 32 * (pt >> 1) + 8 * (tl >> 2) + (tl & 3) + 4 * (pt & 1);
-      const int blk = btp[pos >> 4];
-      const T* kp = kvp + (((layer_base + blk) * 2 + 0) * a.n_kv + h) * 16 * HD + (pos & 15) * HD + kg * 8;
+      const T* kp = kvp + (((layer_base + kblk[pt]) * 2 + 0) * a.n_kv + h) * 16 * HD + (pos & 15) * HD + kg * 8;
 #pragma unroll
       for (int ds = 0; ds < DS; ++ds) kf[pt][ds] = ET<T>::load(kp + ds * 32);
     }
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
       const int pos = P0 + 32 * s + 8 * kg;
-      const int blk = btp[pos >> 4];
-      const T* vp = kvp + (((layer_base + blk) * 2 + 1) * a.n_kv + h) * HD * 16 + tl * 16 + (pos & 15);
+      const T* vp = kvp + (((layer_base + vblk[s]) * 2 + 1) * a.n_kv + h) * HD * 16 + tl * 16 + (pos & 15);
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) vf[s][dt] = ET<T>::load(vp + dt * 16 * 16);
     }
   }
+  // keep every K/V load here, ahead of all arithmetic: left to itself the scheduler trades them
+  // for registers and sinks them into the MFMA sequence, one round trip at a time
+  __builtin_amdgcn_sched_barrier(0);
 
-  // ---- queries: lane column qv = qt*16 + tl, k-slots d = ds*32 + kg*8 + j, scaled by log2(e)/sqrt(d)
-  typename ET<T>::B qf[2][DS];
-  int qpos[2];
+  // ---- queries scaled by log2(e)/sqrt(d), as bf16 hi/lo B operands ----
+  typename ET<T>::B qf[QT][DS];
 #pragma unroll
-  for (int qt = 0; qt < 2; ++qt) {
-    const int qv = qt * 16 + tl;
-    const bool ok = live && qt < QT && qv < nqv;
-    const int rl = qv / a.G, gq = qv - rl * a.G;
-    const int m = mrow0 + (ok ? rl : 0);
-    qpos[qt] = ok ? a.row_pos[m] : -1;
-    const float* qp = a.q + (size_t)m * qstride + (h * a.G + gq) * HD;
+  for (int qt = 0; qt < QT; ++qt) {
+    if (!(live && qok[qt])) qpos[qt] = -1;
 #pragma unroll
     for (int ds = 0; ds < DS; ++ds) {
       float x[8];
-      if (ok) {
-        load8(qp + ds * 32 + kg * 8, x);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) x[j] *= a.scale_log2;
-      } else {
-#pragma unroll
-        for (int j = 0; j < 8; ++j) x[j] = 0.f;
-      }
+      for (int j = 0; j < 8; ++j) x[j] = (live && qok[qt]) ? qraw[qt][ds][j] * a.scale_log2 : 0.f;
       qf[qt][ds] = ET<T>::split(x);
     }
   }
 
-  float m_c[2] = {NEG_INF, NEG_INF}, l_c[2] = {0.f, 0.f};
-  float o_c[2][DT][4];
+  float m_c[QT], l_c[QT];
+  float o_c[QT][DT][4];
 #pragma unroll
-  for (int qt = 0; qt < 2; ++qt)
+  for (int qt = 0; qt < QT; ++qt) {
+    m_c[qt] = NEG_INF;
+    l_c[qt] = 0.f;
+  }
+#pragma unroll
+  for (int qt = 0; qt < QT; ++qt)
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
@@ -113,21 +131,20 @@ __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
 
   if (live) {
     // ---- S^T = K Q^T ----
-    f32x4 sacc[4][2];
+    f32x4 sacc[4][QT];
 #pragma unroll
     for (int pt = 0; pt < 4; ++pt) {
-      sacc[pt][0] = f32x4{0.f, 0.f, 0.f, 0.f};
-      sacc[pt][1] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int ds = 0; ds < DS; ++ds) {
-        ET<T>::mma(sacc[pt][0], kf[pt][ds], qf[0][ds]);
-        if (QT > 1) ET<T>::mma(sacc[pt][1], kf[pt][ds], qf[1][ds]);
-      }
+      for (int qt = 0; qt < QT; ++qt) sacc[pt][qt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ds = 0; ds < DS; ++ds)
+#pragma unroll
+        for (int qt = 0; qt < QT; ++qt) ET<T>::mma(sacc[pt][qt], kf[pt][ds], qf[qt][ds]);
     }
     // ---- mask + chunk softmax (base 2) ----
-    float p[2][4][4];
+    float p[QT][4][4];
 #pragma unroll
-    for (int qt = 0; qt < 2; ++qt) {
+    for (int qt = 0; qt < QT; ++qt) {
       float mx = NEG_INF;
 #pragma unroll
       for (int pt = 0; pt < 4; ++pt)
@@ -155,9 +172,9 @@ __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
       l_c[qt] = sum;
     }
     // ---- O^T = V^T P^T ----
-    typename ET<T>::B pf[2][2];
+    typename ET<T>::B pf[QT][2];
 #pragma unroll
-    for (int qt = 0; qt < 2; ++qt)
+    for (int qt = 0; qt < QT; ++qt)
 #pragma unroll
       for (int s = 0; s < 2; ++s) {
         float x[8];
@@ -169,27 +186,23 @@ __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
         pf[qt][s] = ET<T>::split(x);
       }
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-      f32x4 oacc0 = {0.f, 0.f, 0.f, 0.f}, oacc1 = {0.f, 0.f, 0.f, 0.f};
+    for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        ET<T>::mma(oacc0, vf[s][dt], pf[0][s]);
-        if (QT > 1) ET<T>::mma(oacc1, vf[s][dt], pf[1][s]);
-      }
+      for (int qt = 0; qt < QT; ++qt) {
+        f32x4 oacc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        o_c[0][dt][i] = oacc0[i];
-        o_c[1][dt][i] = oacc1[i];
+        for (int s = 0; s < 2; ++s) ET<T>::mma(oacc, vf[s][dt], pf[qt][s]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o_c[qt][dt][i] = oacc[i];
       }
-    }
   }
 
   // ---- merge the group's 4 chunks left to right (wave 0 holds chunk 0) ----
   if (wave > 0) {
 #pragma unroll
-    for (int qt = 0; qt < 2; ++qt) {
+    for (int qt = 0; qt < QT; ++qt) {
       const int qv = qt * 16 + tl;
-      if (qt >= QT || qv >= nqv) continue;
+      if (qv >= nqv) continue;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
         *reinterpret_cast<float4*>(&s_o[wave - 1][qv][dt * 16 + 4 * kg]) =
@@ -204,9 +217,9 @@ __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
   float* part = a.part + ((((size_t)(b * a.n_kv + h) * a.n_rb + rb) * a.n_groups_max + g) * 32) * PS;
   if (wave == 0) {
 #pragma unroll
-    for (int qt = 0; qt < 2; ++qt) {
+    for (int qt = 0; qt < QT; ++qt) {
       const int qv = qt * 16 + tl;
-      if (qt >= QT || qv >= nqv) continue;
+      if (qv >= nqv) continue;
       for (int w = 0; w < ATT_WAVES - 1; ++w) {
         float oc[DT * 4];
 #pragma unroll
@@ -238,53 +251,69 @@ __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
       }
     }
   }
-  if (n_groups == 1) return;
+}
 
-  // ---- the last group of (b, h, rb) to finish merges all group partials left to right ----
-  // One agent-scope acquire-release count per workgroup, after the barrier has completed every
-  // wave's stores: it publishes this group's partial and, for the last group, makes the others
-  // visible.
-  __syncthreads();
-  int* cnt = a.cnt + (b * a.n_kv + h) * a.n_rb + rb;
-  if (threadIdx.x == 0)
-    s_last = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) == n_groups - 1;
-  __syncthreads();
-  if (!s_last) return;
-  // Merge the group partials left to right (online softmax merge, fixed order). Thread e owns
-  // columns 4*(e mod HD/4).. of query vector e / (HD/4); each batch of 8 groups is loaded at
-  // once. A group that sees nothing is an exact identity of the merge.
-  const float* part0 = a.part + ((((size_t)(b * a.n_kv + h) * a.n_rb + rb) * a.n_groups_max) * 32) * PS;
-  constexpr int HD4 = HD / 4;
-  for (int e = threadIdx.x; e < nqv * HD4; e += blockDim.x) {
-    const int qv = e / HD4, d = (e - qv * HD4) * 4;
-    float m_r = NEG_INF, l_r = 0.f, o_r[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int g0 = 0; g0 < n_groups; g0 += 8) {
-      float mg[8], lg[8], og[8][4];
+// Merge the group partials of each query left to right (online softmax merge, fixed order).
+// Thread e owns columns 4*(e mod HD/4).. of query vector e / (HD/4). The first 8 groups are
+// loaded before the group count is known (the partial buffer holds n_groups_max groups), so a
+// short context costs one round trip after the position read.
+template <int HD>
+__global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
+  constexpr int PS = HD + 4, HD4 = HD / 4;
+  const int h = blockIdx.y % a.n_kv, rb = blockIdx.y / a.n_kv;
+  const int b = blockIdx.z;
+  const int r0 = rb * a.RB;
+  if (r0 >= a.R) return;
+  const int nr = min(a.RB, a.R - r0);
+  const int nqv = nr * a.G;
+  const int mrow0 = b * a.R + r0;
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= nqv * HD4) return;
+  const int qv = e / HD4, d = (e - qv * HD4) * 4;
+  const float* part0 = a.part + ((((size_t)(b * a.n_kv + h) * a.n_rb + rb) * a.n_groups_max) * 32 + qv) * PS;
+  const int maxpos = a.row_pos[mrow0 + nr - 1];
+  float m_r = NEG_INF, l_r = 0.f, o_r[4] = {0.f, 0.f, 0.f, 0.f};
+  int n_groups = -1;
+  for (int g0 = 0; g0 < a.n_groups_max; g0 += 8) {
+    float mg[8], lg[8], og[8][4];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const float* pp = part0 + ((size_t)min(g0 + u, n_groups - 1) * 32 + qv) * PS;
-        const float4 v = *reinterpret_cast<const float4*>(pp + d);
-        const float2 ml = *reinterpret_cast<const float2*>(pp + HD);
-        og[u][0] = v.x; og[u][1] = v.y; og[u][2] = v.z; og[u][3] = v.w;
-        mg[u] = ml.x;
-        lg[u] = ml.y;
-      }
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-        if (g0 + u < n_groups) softmax_merge(m_r, l_r, o_r, mg[u], lg[u], og[u], 4);
+    for (int u = 0; u < 8; ++u) {
+      const float* pp = part0 + (size_t)min(g0 + u, a.n_groups_max - 1) * 32 * PS;
+      const float4 v = *reinterpret_cast<const float4*>(pp + d);
+      const float2 ml = *reinterpret_cast<const float2*>(pp + HD);
+      og[u][0] = v.x; og[u][1] = v.y; og[u][2] = v.z; og[u][3] = v.w;
+      mg[u] = ml.x;
+      lg[u] = ml.y;
     }
-    const int rl = qv / a.G, gq = qv - rl * a.G;
-    *reinterpret_cast<float4*>(a.out + (size_t)(mrow0 + rl) * qstride + (h * a.G + gq) * HD + d) =
-        make_float4(o_r[0] / l_r, o_r[1] / l_r, o_r[2] / l_r, o_r[3] / l_r);
+    if (n_groups < 0) {
+      n_groups = maxpos / ATT_GROUP + 1;
+      if (n_groups == 1) return;   // k_attention wrote the final output
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (g0 + u < n_groups) softmax_merge(m_r, l_r, o_r, mg[u], lg[u], og[u], 4);
+    if (g0 + 8 >= n_groups) break;
   }
-  if (threadIdx.x == 0) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const int rl = qv / a.G, gq = qv - rl * a.G;
+  *reinterpret_cast<float4*>(a.out + (size_t)(mrow0 + rl) * a.n_heads * HD + (h * a.G + gq) * HD + d) =
+      make_float4(o_r[0] / l_r, o_r[1] / l_r, o_r[2] / l_r, o_r[3] / l_r);
+}
+
+template <typename T, int HD>
+static void launch_attention_hd(const AttnArgs& a, hipStream_t s) {
+  const dim3 grid(a.n_groups_max, a.n_kv * a.n_rb, a.B);
+  if (std::min(a.RB, a.R) * a.G > 16) hipLaunchKernelGGL((k_attention<T, HD, 2>), grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL((k_attention<T, HD, 1>), grid, dim3(256), 0, s, a);
+  if (a.n_groups_max > 1) {
+    const dim3 cgrid((32 * HD / 4 + 255) / 256, a.n_kv * a.n_rb, a.B);
+    hipLaunchKernelGGL((k_attn_combine<HD>), cgrid, dim3(256), 0, s, a);
+  }
 }
 
 template <typename T>
 void launch_attention(const AttnArgs& a, hipStream_t s) {
-  const dim3 grid(a.n_groups_max, a.n_kv * a.n_rb, a.B);
-  if (a.head_dim == 128) hipLaunchKernelGGL((k_attention<T, 128>), grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL((k_attention<T, 64>), grid, dim3(256), 0, s, a);
+  if (a.head_dim == 128) launch_attention_hd<T, 128>(a, s);
+  else launch_attention_hd<T, 64>(a, s);
 }
 
 template void launch_attention<uint16_t>(const AttnArgs&, hipStream_t);

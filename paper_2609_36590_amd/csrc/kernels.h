@@ -29,12 +29,9 @@ struct LinArgs {
   int N, K;               // output features, input features
   int M;                  // activation rows in this pass
   int NT, KS;             // n-tiles per workgroup pass, K-splits per n-tile
-  int S;                  // K-slices: the KS splits form S consecutive groups of KS/S; partial sums
-                          // are added group by group, in order (the LDS kernel gives each slice
-                          // its own workgroup and the last one to finish adds them up)
-  int NJ;                 // LDS kernel, S == 1: passes per workgroup (n-group blockIdx.x + j*gridDim.x)
-  float* lpart;           // S > 1: slice partials [n_groups][S][NT][M][16]
-  int* lcnt;              // S > 1: finished-slice counters [n_groups] (zero between launches)
+  int S;                  // the KS partial sums are added in S consecutive groups of KS/S, group
+                          // by group in order (k_linear_lds: S == 1)
+  int NJ;                 // LDS kernel: passes per workgroup (n-group blockIdx.x + j*gridDim.x)
   // input
   const float* X;         // [M][ldx] fp32 activations; PRO_NORM: x*g formed by the producer
   int ldx;
@@ -64,7 +61,7 @@ struct LinArgs {
   int amax_stride;
 };
 
-// Arguments of the split-KV paged attention kernel and its combine step.
+// Arguments of the split-KV paged attention kernel and its combine kernel.
 struct AttnArgs {
   const float* q;         // [M][n_heads*head_dim]
   const void* kv;
@@ -78,7 +75,6 @@ struct AttnArgs {
   int n_groups_max;       // grid extent over groups of 256 positions
   float scale_log2;       // log2(e) / sqrt(head_dim)
   float* part;            // group partials [B][n_kv][n_rb][n_groups_max][32][head_dim + 4]
-  int* cnt;               // [B][n_kv][n_rb] finished-group counters (zero between launches)
   float* out;             // [M][n_heads*head_dim]
 };
 

@@ -11,7 +11,7 @@
 // (y = sum_s (sum_{k in group s} p_k), each sum left to right, starting from 0). The split (KS, S)
 // depends only on the weight shape (N, K), so a row's output is bit-identical whatever kernel
 // runs it and however many rows share the pass: verifying d drafts gives the same logits, row by
-// row, as plain greedy decoding (d = 0).
+// row, as plain greedy decoding (d = 0). (k_linear_lds supports S == 1 only.)
 #include "device_common.h"
 
 namespace seedk {
@@ -205,11 +205,6 @@ __device__ __forceinline__ float sum_partials(const float* p, int n, int per) {
   return t;
 }
 
-// k-tiles of slice s: from slice_kt_begin(s) to slice_kt_begin(s + 1), the k-ranges of the
-// K-splits s*KS/S .. (s+1)*KS/S - 1
-__host__ __device__ inline int slice_kt_begin(int KT, int KS, int S, int s) { return (s * (KS / S) * KT) / KS; }
-// an upper bound of the k-tiles of any slice
-__host__ __device__ inline int slice_kt_max(int KT, int S) { return S == 1 ? KT : (KT + S - 1) / S + 1; }
 __host__ __device__ inline size_t lds_x_bytes(int M, int nkt) { return (size_t)nkt * 4 * M * 32 + 32; }
 
 // ---------------------------------------------------------------------------------------------
@@ -221,29 +216,22 @@ __host__ __device__ inline size_t lds_x_bytes(int M, int nkt) { return (size_t)n
 // for the token columns r >= M. Waves then stream weight tiles with P in flight, reading their B
 // operands from LDS.
 //
-// Work: with S == 1 the workgroup makes NJ passes over n-groups blockIdx.x + j*gridDim.x (NT
-// n-tiles each) and wave (nl, ks) covers k-range ks of n-tile nl of every pass, as one continuous
-// stream. With S > 1 (few n-tiles, long K) workgroup b takes slice b mod S of n-group b / S; its
-// slice sum goes to global memory and the last of the S workgroups to finish adds the S slice
-// sums in slice order and runs the epilogue.
+// Work: the workgroup makes NJ passes over n-groups blockIdx.x + j*gridDim.x (NT n-tiles each);
+// wave (nl, ks) covers k-range ks of n-tile nl of every pass, as one continuous stream. All KS
+// K-splits of an n-tile run in one workgroup (the runtime uses this kernel only with S == 1).
 // ---------------------------------------------------------------------------------------------
 template <typename T, int PRO, int EPI>
 __global__ void __launch_bounds__(1024) k_linear_lds(LinArgs a) {
   extern __shared__ __attribute__((aligned(16))) char lds[];
   __shared__ float s_rs[16];
-  __shared__ int s_last;
   constexpr int P = 8;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int S = a.S, KSs = a.KS / S;
-  const int NW = a.NT * KSs;
+  const int NW = a.NT * a.KS;
   const int KT = a.K >> 5, n_tiles = a.N >> 4, M = a.M;
-  const int nl = wave / KSs, kss = wave - nl * KSs;
+  const int nl = wave / a.KS, ks = wave - nl * a.KS;
   const int tl = lane & 15, kg = lane >> 4;
-  const int sl = (S > 1) ? (int)(blockIdx.x % S) : 0;
-  const Grp gr = (S > 1) ? Grp{(int)(blockIdx.x / S), 0} : Grp{(int)blockIdx.x, (int)gridDim.x};
-  const int ks = sl * KSs + kss;
+  const Grp gr{(int)blockIdx.x, (int)gridDim.x};
   const int kt0 = (ks * KT) / a.KS, nk = ((ks + 1) * KT) / a.KS - kt0;
-  const int ktA = slice_kt_begin(KT, a.KS, S, sl), nkt_s = slice_kt_begin(KT, a.KS, S, sl + 1) - ktA;
   int nj = 0;
   while (nj < a.NJ && (gr.g0 + nj * gr.gs) * a.NT + nl < n_tiles) ++nj;
   const int Sw = nj * nk;  // weight tiles this wave streams
@@ -267,11 +255,11 @@ __global__ void __launch_bounds__(1024) k_linear_lds(LinArgs a) {
   bool pre = false;
   if constexpr (PRO == PRO_NORM) pre = preload_row_ssq(a, wave, ssv);
 
-  // ---- stage the slice's X columns into LDS (loads first, then the LDS writes) ----
-  const size_t zero_off = (size_t)nkt_s * 4 * M * 32;
-  float* part = reinterpret_cast<float*>(lds + lds_x_bytes(M, slice_kt_max(KT, S)));  // [NJ][NW][M][16]
+  // ---- stage X into LDS (loads first, then the LDS writes) ----
+  const size_t zero_off = (size_t)KT * 4 * M * 32;
+  float* part = reinterpret_cast<float*>(lds + lds_x_bytes(M, KT));  // [NJ][NW][M][16]
   {
-    const int row_items = nkt_s * 4, items = M * row_items;
+    const int row_items = KT * 4, items = M * row_items;
     for (int q0 = 0; q0 < items; q0 += 2 * (int)blockDim.x) {
       float xv[2][8];
 #pragma unroll
@@ -279,7 +267,7 @@ __global__ void __launch_bounds__(1024) k_linear_lds(LinArgs a) {
         const int q = q0 + u * blockDim.x + tid;
         if (q < items) {
           const int r = q / row_items, rem = q - r * row_items;
-          load8(a.X + (size_t)r * a.ldx + (size_t)(ktA * 4 + rem) * 8, xv[u]);
+          load8(a.X + (size_t)r * a.ldx + (size_t)rem * 8, xv[u]);
         }
       }
 #pragma unroll
@@ -297,7 +285,7 @@ __global__ void __launch_bounds__(1024) k_linear_lds(LinArgs a) {
 
   // ---- stream ----
   const bool live_col = tl < M;
-  const char* xa = lds + (live_col ? ((size_t)(kt0 - ktA) * 4 * M + (size_t)kg * M + tl) * 32 : zero_off);
+  const char* xa = lds + (live_col ? ((size_t)kt0 * 4 * M + (size_t)kg * M + tl) * 32 : zero_off);
   const size_t xs = live_col ? (size_t)4 * M * 32 : 0;  // bytes per k-tile
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
   int jC = 0, iC = 0;  // pass / k-tile of the next tile to consume
@@ -335,7 +323,7 @@ __global__ void __launch_bounds__(1024) k_linear_lds(LinArgs a) {
   for (int p = 0; p < P; ++p)
     if (s0 + P + p < Sw) consume(p);
 
-  // ---- sums over the workgroup's K-splits, slice combine, RMSNorm row scale, epilogue ----
+  // ---- sums over the K-splits (in ks order), RMSNorm row scale, epilogue ----
   if constexpr (PRO == PRO_NORM) {
     for (int m = wave; m < M; m += NW) {
       const float r = wave_row_scale(a, m, ssv, pre && m == wave);
@@ -344,38 +332,16 @@ __global__ void __launch_bounds__(1024) k_linear_lds(LinArgs a) {
   }
   __syncthreads();
   const int per = M * 16;
-  const int n_out = a.NJ * a.NT * per;
-  for (int e = tid; e < n_out; e += blockDim.x) {
+  for (int e = tid; e < a.NJ * a.NT * per; e += blockDim.x) {
     const int lt = e / per, r = e - lt * per;
     const int j = lt / a.NT, nl2 = lt - j * a.NT;
-    float* src = part + (size_t)(j * NW + nl2 * KSs) * per + r;
-    float y = sum_partials(src, KSs, per);
-    if (S > 1) {
-      a.lpart[((size_t)gr.g0 * S + sl) * a.NT * per + e] = y;  // NJ == 1 here, so e < NT * per
-    } else {
-      if constexpr (PRO == PRO_NORM) y *= s_rs[r >> 4];
-      *src = y;
-    }
-  }
-  if (S > 1) {
-    // one agent-scope acquire-release count per workgroup, after the barrier has completed every
-    // wave's stores: it publishes this slice and, for the last slice, makes the others visible
-    __syncthreads();
-    if (tid == 0)
-      s_last = __hip_atomic_fetch_add(a.lcnt + gr.g0, 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) == S - 1;
-    __syncthreads();
-    if (!s_last) return;
-    for (int e = tid; e < a.NT * per; e += blockDim.x) {
-      const int nl2 = e / per, r = e - nl2 * per;
-      float y = 0.f;
-      for (int s2 = 0; s2 < S; ++s2) y += a.lpart[((size_t)gr.g0 * S + s2) * a.NT * per + e];
-      if constexpr (PRO == PRO_NORM) y *= s_rs[r >> 4];
-      part[(size_t)(nl2 * KSs) * per + r] = y;
-    }
-    if (tid == 0) __hip_atomic_store(a.lcnt + gr.g0, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    float* src = part + (size_t)(j * NW + nl2 * a.KS) * per + r;
+    float y = sum_partials(src, a.KS, per);
+    if constexpr (PRO == PRO_NORM) y *= s_rs[r >> 4];
+    *src = y;
   }
   __syncthreads();
-  linear_epilogue<T, EPI>(a, gr, part, KSs * per, epre);
+  linear_epilogue<T, EPI>(a, gr, part, a.KS * per, epre);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -519,10 +485,8 @@ __global__ void __launch_bounds__(256) k_argmax_finalize(const float* val, const
 // Launchers.
 // ---------------------------------------------------------------------------------------------
 size_t linear_lds_bytes(int M, int K, int NT, int KS, int S, int NJ, int kind) {
-  if (kind == LIN_LDS) {
-    const int NW = NT * (KS / S);
-    return lds_x_bytes(M, slice_kt_max(K >> 5, S)) + (size_t)NJ * NW * M * 16 * sizeof(float);
-  }
+  (void)S;
+  if (kind == LIN_LDS) return lds_x_bytes(M, K >> 5) + (size_t)NJ * NT * KS * M * 16 * sizeof(float);
   return (size_t)(NT * KS * M * 16) * sizeof(float);
 }
 
@@ -532,9 +496,8 @@ static void launch_linear_pe(const LinArgs& a0, int kind, hipStream_t s) {
   const int n_tiles = a.N >> 4;
   const int n_groups = (n_tiles + a.NT - 1) / a.NT;
   if (kind == LIN_LDS) {
-    if (a.S > 1) a.NJ = 1;
-    const dim3 grid(a.S > 1 ? n_groups * a.S : (n_groups + a.NJ - 1) / a.NJ);
-    const dim3 block(64 * a.NT * (a.KS / a.S));
+    const dim3 grid((n_groups + a.NJ - 1) / a.NJ);
+    const dim3 block(64 * a.NT * a.KS);
     const size_t lds = linear_lds_bytes(a.M, a.K, a.NT, a.KS, a.S, a.NJ, kind);
     hipLaunchKernelGGL((k_linear_lds<T, PRO, EPI>), grid, block, lds, s, a);
     return;
