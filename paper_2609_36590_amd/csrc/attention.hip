@@ -300,23 +300,38 @@ __global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
 }
 
 template <typename T, int HD>
-static void launch_attention_hd(const AttnArgs& a, hipStream_t s) {
+static void launch_attention_hd(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev) {
   const dim3 grid(a.n_groups_max, a.n_kv * a.n_rb, a.B);
-  if (std::min(a.RB, a.R) * a.G > 16) hipLaunchKernelGGL((k_attention<T, HD, 2>), grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL((k_attention<T, HD, 1>), grid, dim3(256), 0, s, a);
-  if (a.n_groups_max > 1) {
-    const dim3 cgrid((32 * HD / 4 + 255) / 256, a.n_kv * a.n_rb, a.B);
-    hipLaunchKernelGGL((k_attn_combine<HD>), cgrid, dim3(256), 0, s, a);
+  if (std::min(a.RB, a.R) * a.G > 16) {
+    if (ev) hipExtLaunchKernelGGL((k_attention<T, HD, 2>), grid, dim3(256), 0, s, ev->start, ev->stop, 0, a);
+    else hipLaunchKernelGGL((k_attention<T, HD, 2>), grid, dim3(256), 0, s, a);
+  } else {
+    if (ev) hipExtLaunchKernelGGL((k_attention<T, HD, 1>), grid, dim3(256), 0, s, ev->start, ev->stop, 0, a);
+    else hipLaunchKernelGGL((k_attention<T, HD, 1>), grid, dim3(256), 0, s, a);
   }
 }
 
-template <typename T>
-void launch_attention(const AttnArgs& a, hipStream_t s) {
-  if (a.head_dim == 128) launch_attention_hd<T, 128>(a, s);
-  else launch_attention_hd<T, 64>(a, s);
+template <int HD>
+static void launch_attn_combine_hd(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev) {
+  const dim3 cgrid((32 * HD / 4 + 255) / 256, a.n_kv * a.n_rb, a.B);
+  if (ev) hipExtLaunchKernelGGL((k_attn_combine<HD>), cgrid, dim3(256), 0, s, ev->start, ev->stop, 0, a);
+  else hipLaunchKernelGGL((k_attn_combine<HD>), cgrid, dim3(256), 0, s, a);
 }
 
-template void launch_attention<uint16_t>(const AttnArgs&, hipStream_t);
-template void launch_attention<float>(const AttnArgs&, hipStream_t);
+template <typename T>
+void launch_attention(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev) {
+  if (a.head_dim == 128) launch_attention_hd<T, 128>(a, s, ev);
+  else launch_attention_hd<T, 64>(a, s, ev);
+}
+
+bool attention_needs_combine(const AttnArgs& a) { return a.n_groups_max > 1; }
+
+void launch_attn_combine(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev) {
+  if (a.head_dim == 128) launch_attn_combine_hd<128>(a, s, ev);
+  else launch_attn_combine_hd<64>(a, s, ev);
+}
+
+template void launch_attention<uint16_t>(const AttnArgs&, hipStream_t, const LaunchEvents*);
+template void launch_attention<float>(const AttnArgs&, hipStream_t, const LaunchEvents*);
 
 }  // namespace seedk

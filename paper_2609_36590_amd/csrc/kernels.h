@@ -1,6 +1,7 @@
 // Internal interface between the host runtime and the gfx950 kernels of the SEED decode path.
 // Nothing here is part of the public C ABI (include/seed.h).
 #pragma once
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -136,10 +137,21 @@ struct DevState {
 // MFMA fragments (M <= 16 and the rows fit), else the activation fragments come from global memory.
 enum LinearKind { LIN_LDS = 0, LIN_GLOBAL = 1, LIN_VALU = 2 };
 
+// Optional timing events stamped by the launches themselves (hipExtLaunchKernel): `start` at the
+// start of the first kernel of the operation, `stop` at the end of its last kernel.
+struct LaunchEvents {
+  hipEvent_t start, stop;
+};
+
 template <typename T>
-void launch_linear(const LinArgs& a, int prologue, int epilogue, int kind, hipStream_t s);
+void launch_linear(const LinArgs& a, int prologue, int epilogue, int kind, hipStream_t s,
+                   const LaunchEvents* ev = nullptr);
+// Attention partials per group of 256 positions (the final output when the rows see one group).
 template <typename T>
-void launch_attention(const AttnArgs& a, hipStream_t s);
+void launch_attention(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev = nullptr);
+// Merge of the group partials; needed when the context can span more than one group.
+bool attention_needs_combine(const AttnArgs& a);
+void launch_attn_combine(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev = nullptr);
 template <typename T>
 void launch_setup(const SetupArgs& a, hipStream_t s);
 void launch_accept(const DevState& st, int B, int k, hipStream_t s);

@@ -490,8 +490,15 @@ size_t linear_lds_bytes(int M, int K, int NT, int KS, int S, int NJ, int kind) {
   return (size_t)(NT * KS * M * 16) * sizeof(float);
 }
 
+// a launch, optionally stamping timing events at the kernel's start and end
+template <typename K, typename... Args>
+static void launch(K kernel, dim3 grid, dim3 block, size_t lds, hipStream_t s, const LaunchEvents* ev, Args... args) {
+  if (ev) hipExtLaunchKernelGGL(kernel, grid, block, (uint32_t)lds, s, ev->start, ev->stop, 0, args...);
+  else hipLaunchKernelGGL(kernel, grid, block, lds, s, args...);
+}
+
 template <typename T, int PRO, int EPI>
-static void launch_linear_pe(const LinArgs& a0, int kind, hipStream_t s) {
+static void launch_linear_pe(const LinArgs& a0, int kind, hipStream_t s, const LaunchEvents* ev) {
   LinArgs a = a0;
   const int n_tiles = a.N >> 4;
   const int n_groups = (n_tiles + a.NT - 1) / a.NT;
@@ -499,7 +506,7 @@ static void launch_linear_pe(const LinArgs& a0, int kind, hipStream_t s) {
     const dim3 grid((n_groups + a.NJ - 1) / a.NJ);
     const dim3 block(64 * a.NT * a.KS);
     const size_t lds = linear_lds_bytes(a.M, a.K, a.NT, a.KS, a.S, a.NJ, kind);
-    hipLaunchKernelGGL((k_linear_lds<T, PRO, EPI>), grid, block, lds, s, a);
+    launch(k_linear_lds<T, PRO, EPI>, grid, block, lds, s, ev, a);
     return;
   }
   a.NJ = 1;
@@ -507,23 +514,23 @@ static void launch_linear_pe(const LinArgs& a0, int kind, hipStream_t s) {
   const size_t lds = linear_lds_bytes(a.M, a.K, a.NT, a.KS, a.S, 1, kind);
   const int TT = (a.M + 15) / 16;
   switch (TT) {
-    case 1: hipLaunchKernelGGL((k_linear_mfma<T, PRO, EPI, 1>), grid, block, lds, s, a); break;
-    case 2: hipLaunchKernelGGL((k_linear_mfma<T, PRO, EPI, 2>), grid, block, lds, s, a); break;
-    case 3: hipLaunchKernelGGL((k_linear_mfma<T, PRO, EPI, 3>), grid, block, lds, s, a); break;
-    default: hipLaunchKernelGGL((k_linear_mfma<T, PRO, EPI, 4>), grid, block, lds, s, a); break;
+    case 1: launch(k_linear_mfma<T, PRO, EPI, 1>, grid, block, lds, s, ev, a); break;
+    case 2: launch(k_linear_mfma<T, PRO, EPI, 2>, grid, block, lds, s, ev, a); break;
+    case 3: launch(k_linear_mfma<T, PRO, EPI, 3>, grid, block, lds, s, ev, a); break;
+    default: launch(k_linear_mfma<T, PRO, EPI, 4>, grid, block, lds, s, ev, a); break;
   }
 }
 
 template <typename T>
-void launch_linear(const LinArgs& a, int prologue, int epilogue, int kind, hipStream_t s) {
+void launch_linear(const LinArgs& a, int prologue, int epilogue, int kind, hipStream_t s, const LaunchEvents* ev) {
   if (prologue == PRO_NORM) {
     switch (epilogue) {
-      case EPI_QKV: launch_linear_pe<T, PRO_NORM, EPI_QKV>(a, kind, s); break;
-      case EPI_SWIGLU: launch_linear_pe<T, PRO_NORM, EPI_SWIGLU>(a, kind, s); break;
-      default: launch_linear_pe<T, PRO_NORM, EPI_HEAD>(a, kind, s); break;
+      case EPI_QKV: launch_linear_pe<T, PRO_NORM, EPI_QKV>(a, kind, s, ev); break;
+      case EPI_SWIGLU: launch_linear_pe<T, PRO_NORM, EPI_SWIGLU>(a, kind, s, ev); break;
+      default: launch_linear_pe<T, PRO_NORM, EPI_HEAD>(a, kind, s, ev); break;
     }
   } else {
-    launch_linear_pe<T, PRO_PLAIN, EPI_RESID>(a, kind, s);
+    launch_linear_pe<T, PRO_PLAIN, EPI_RESID>(a, kind, s, ev);
   }
 }
 
@@ -571,7 +578,7 @@ hipError_t configure_kernels(int bf16) {
 
 size_t linear_lds_limit() { return g_lds_limit; }
 
-template void launch_linear<uint16_t>(const LinArgs&, int, int, int, hipStream_t);
-template void launch_linear<float>(const LinArgs&, int, int, int, hipStream_t);
+template void launch_linear<uint16_t>(const LinArgs&, int, int, int, hipStream_t, const LaunchEvents*);
+template void launch_linear<float>(const LinArgs&, int, int, int, hipStream_t, const LaunchEvents*);
 
 }  // namespace seedk

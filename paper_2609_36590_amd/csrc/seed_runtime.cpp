@@ -217,6 +217,15 @@ hipError_t drain_timing(seed_ctx* c) {
   return hipSuccess;
 }
 
+// Linear and attention launches stamp timing events from the kernels themselves
+// (hipExtLaunchKernel); the small kernels are bracketed by event records on the stream.
+bool stamps_events(int op) {
+  return op == SEED_OP_QKV || op == SEED_OP_ATTN || op == SEED_OP_COMBINE || op == SEED_OP_O ||
+         op == SEED_OP_GATEUP || op == SEED_OP_DOWN || op == SEED_OP_HEAD;
+}
+
+// Runs fn(events): events is non-null only when this (phase, op) is being timed, the stream is
+// not being captured and the op's launches stamp the events themselves.
 template <typename F>
 void timed(seed_ctx* c, int phase, int op, bool capturing, F&& fn) {
   if (!capturing && c->timed_id == phase * 16 + op) {
@@ -224,12 +233,13 @@ void timed(seed_ctx* c, int phase, int op, bool capturing, F&& fn) {
     TimedLaunch t;
     if (!c->pool.empty()) { t = c->pool.back(); c->pool.pop_back(); }
     else { hipEventCreate(&t.a); hipEventCreate(&t.b); }
-    hipEventRecord(t.a, c->s);
-    fn();
-    hipEventRecord(t.b, c->s);
+    LaunchEvents ev{t.a, t.b};
+    if (!stamps_events(op)) hipEventRecord(t.a, c->s);
+    fn(stamps_events(op) ? &ev : nullptr);
+    if (!stamps_events(op)) hipEventRecord(t.b, c->s);
     c->pending.push_back(t);
   } else {
-    fn();
+    fn(nullptr);
   }
 }
 
@@ -322,7 +332,7 @@ template <typename T>
 void linear(seed_ctx* c, LinArgs a, int pro, int epi, int phase, int op, bool cap) {
   tile_policy(a.N, a.K, epi == EPI_HEAD, a.NT, a.KS, a.S, a.NJ);
   const int kind = linear_kind(a);
-  timed(c, phase, op, cap, [&] { launch_linear<T>(a, pro, epi, kind, c->s); });
+  timed(c, phase, op, cap, [&](const LaunchEvents* ev) { launch_linear<T>(a, pro, epi, kind, c->s, ev); });
 }
 
 // Layers [l0, l1) over M rows (B sequences x R rows each, consecutive positions per sequence).
@@ -355,7 +365,9 @@ void run_layers(seed_ctx* c, int M, int B, int R, int l0, int l1, int phase,
     at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)p.HD));
     at.part = c->ws<float>(p.o_part);
     at.out = c->ws<float>(p.o_attn);
-    timed(c, phase, SEED_OP_ATTN, cap, [&] { launch_attention<T>(at, c->s); });
+    timed(c, phase, SEED_OP_ATTN, cap, [&](const LaunchEvents* ev) { launch_attention<T>(at, c->s, ev); });
+    if (attention_needs_combine(at))
+      timed(c, phase, SEED_OP_COMBINE, cap, [&](const LaunchEvents* ev) { launch_attn_combine(at, c->s, ev); });
     // O + residual
     a = lin_base(c, M);
     a.W = c->W + p.w_o[li]; a.N = p.H; a.K = p.QD;
@@ -387,7 +399,7 @@ void run_head(seed_ctx* c, int M, int* tok_out, int tok_stride, float* logits, l
   int NT, KS, S, NJ;
   tile_policy(a.N, a.K, true, NT, KS, S, NJ);
   const int parts = cdiv(p.V / 16, NT);   // one argmax partial per n-group
-  timed(c, phase, SEED_OP_HEAD_ARGMAX, cap, [&] {
+  timed(c, phase, SEED_OP_HEAD_ARGMAX, cap, [&](const LaunchEvents*) {
     launch_argmax_finalize(a.amax_val, a.amax_idx, a.amax_stride, parts, M, tok_out, tok_stride, c->s);
   });
 }
@@ -432,7 +444,7 @@ void enqueue_draft(seed_ctx* c, int k, float* logits, bool cap) {
   for (int i = 1; i <= k; ++i) {
     SetupArgs s = setup_base(c, p.LD);
     s.mode = SETUP_DRAFT; s.M = B; s.R = 1; s.step = i;
-    timed(c, SEED_PHASE_DRAFT, SEED_OP_SETUP, cap, [&] { launch_setup<T>(s, c->s); });
+    timed(c, SEED_PHASE_DRAFT, SEED_OP_SETUP, cap, [&](const LaunchEvents*) { launch_setup<T>(s, c->s); });
     run_layers<T>(c, B, B, 1, p.LD, p.L, SEED_PHASE_DRAFT, nullptr, cap);
     run_head<T>(c, B, c->ws<int>(p.o_drafts) + i, p.dstride,
                 logits ? logits + (size_t)(i - 1) * p.V : nullptr, (long long)k * p.V, SEED_PHASE_DRAFT, cap);
@@ -446,11 +458,11 @@ void enqueue_verify(seed_ctx* c, int k, int sim_accept, float* logits, bool cap)
   const int B = c->B, R = k + 1, M = B * R;
   SetupArgs s = setup_base(c, 0);
   s.mode = SETUP_VERIFY; s.M = M; s.R = R; s.sim_accept = sim_accept;
-  timed(c, SEED_PHASE_VERIFY, SEED_OP_SETUP, cap, [&] { launch_setup<T>(s, c->s); });
+  timed(c, SEED_PHASE_VERIFY, SEED_OP_SETUP, cap, [&](const LaunchEvents*) { launch_setup<T>(s, c->s); });
   run_layers<T>(c, M, B, R, 0, p.L, SEED_PHASE_VERIFY, nullptr, cap);
   run_head<T>(c, M, c->ws<int>(p.o_vtok), 1, logits, (long long)p.V, SEED_PHASE_VERIFY, cap);
   DevState st = dev_state(c);
-  timed(c, SEED_PHASE_VERIFY, SEED_OP_ACCEPT, cap, [&] { launch_accept(st, B, k, c->s); });
+  timed(c, SEED_PHASE_VERIFY, SEED_OP_ACCEPT, cap, [&](const LaunchEvents*) { launch_accept(st, B, k, c->s); });
 }
 
 template <typename T>
@@ -661,7 +673,7 @@ seed_status do_prefill(seed_ctx* c, const std::vector<int>& tokens_packed) {
       const int M = std::min(PREFILL_ROWS, n - s0);
       SetupArgs s = setup_base(c, 0);
       s.mode = SETUP_PREFILL; s.M = M; s.R = M; s.pf_seq = b; s.pf_pos0 = s0;
-      timed(c, SEED_PHASE_PREFILL, SEED_OP_SETUP, false, [&] { launch_setup<T>(s, c->s); });
+      timed(c, SEED_PHASE_PREFILL, SEED_OP_SETUP, false, [&](const LaunchEvents*) { launch_setup<T>(s, c->s); });
       run_layers<T>(c, M, 1, M, 0, p.L, SEED_PHASE_PREFILL,
                     c->ws<int>(p.o_bt) + (size_t)b * p.bt_stride, false);
     }

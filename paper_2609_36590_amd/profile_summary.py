@@ -5,13 +5,115 @@ Dispatches are grouped by kernel and launch shape (grid, workgroup, dynamic LDS)
 same kernel template launched for different passes (prefill, verify, draft) is listed apart.
 
 usage: python3 paper_2609_36590_amd/profile_summary.py <run_results.db> [--min-calls N] [name-substring ...]
+       python3 paper_2609_36590_amd/profile_summary.py --pmc <run_results.db> [--min-calls N] [name-substring ...]
+
+With --pmc the database comes from a `rocprofv3 --pmc <counter>` run and the table lists, per
+kernel and launch shape, the mean value of each collected counter per dispatch.
+
+       python3 paper_2609_36590_amd/profile_summary.py --traffic <dir> <kernel> <name-substring> <grid> <lds> <out.md>
+
+writes the HBM-traffic summary that bench.py reads for `roofline.traffic`, from the four runs
+<dir>/pmc_copy_{FETCH,WRITE}_SIZE and <dir>/pmc_bench_{FETCH,WRITE}_SIZE (see the commands in the
+written file): the dominant kernel's per-dispatch FETCH_SIZE and WRITE_SIZE, each scaled by what
+the counter reads for the plain 1 GiB copy, stamped with the hash of the kernel sources.
 """
+import json
+import os
 import sqlite3
 import sys
 
 
+def pmc_summary(db, filt, min_calls):
+    rows = db.execute(
+        "select kernel_name, grid_size, workgroup_size, lds_block_size, counter_name, count(*), avg(value), "
+        "min(value), max(value) from counters_collection "
+        "group by kernel_name, grid_size, workgroup_size, lds_block_size, counter_name "
+        "order by avg(value) * count(*) desc").fetchall()
+    print(f"{'kernel':52s} {'grid':>9s} {'wg':>5s} {'lds':>6s} {'counter':>11s} {'dispatches':>10s} "
+          f"{'mean':>14s} {'min':>14s} {'max':>14s}")
+    for (name, grid, wg, lds, ctr, n, avg, mn, mx) in rows:
+        if n < min_calls or (filt and not any(f in name for f in filt)):
+            continue
+        short = name.replace("seedk::", "").replace("unsigned short", "bf16").replace("(seedk::LinArgs)", "")
+        short = short.replace("(seedk::AttnArgs)", "").replace("void ", "").split("(")[0]
+        print(f"{short[:52]:52s} {grid:9d} {wg:5d} {lds:6d} {ctr:>11s} {n:10d} {avg:14.2f} {mn:14.2f} {mx:14.2f}")
+
+
+def counter_mean(path, name_sub, grid=None, lds=None):
+    db = sqlite3.connect(path)
+    q = "select avg(value), count(*) from counters_collection where kernel_name like ?"
+    par = [f"%{name_sub}%"]
+    if grid is not None:
+        q += " and grid_size = ?"
+        par.append(grid)
+    if lds is not None:
+        q += " and lds_block_size = ?"
+        par.append(lds)
+    v, n = db.execute(q, par).fetchone()
+    if not n:
+        raise SystemExit(f"no dispatch of '{name_sub}' (grid {grid}) in {path}")
+    return v, n
+
+
+COPY_BYTES = 1 << 30
+COMMANDS = """```
+cd /tmp && export TMPDIR=/tmp && cd <repository root>
+for c in FETCH_SIZE WRITE_SIZE; do
+  timeout -s KILL 120 rocprofv3 --pmc $c -d gpurun_out/pmc_copy_$c -o run -- python3 bench.py --copy-calib
+done
+for c in FETCH_SIZE WRITE_SIZE; do
+  timeout -s KILL 300 rocprofv3 --pmc $c -d gpurun_out/pmc_bench_$c -o run -- python3 bench.py --profile-run --steps 20 --warmup 5
+done
+python3 paper_2609_36590_amd/profile_summary.py --traffic gpurun_out {args}
+```"""
+
+
+def traffic(argv):
+    d, kernel, name_sub, grid, lds, out = argv[0], argv[1], argv[2], int(argv[3]), int(argv[4]), argv[5]
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    sys.path.insert(0, root)
+    import bench
+
+    run = lambda c: os.path.join(d, f"pmc_{c}", "run_results.db")
+    cf, _ = counter_mean(run("copy_FETCH_SIZE"), "copyBuffer")
+    cw, _ = counter_mean(run("copy_WRITE_SIZE"), "copyBuffer")
+    kf, nf = counter_mean(run("bench_FETCH_SIZE"), name_sub, grid, lds)
+    kw, nw = counter_mean(run("bench_WRITE_SIZE"), name_sub, grid, lds)
+    rec = {"kernel": kernel, "kernel_name": name_sub, "grid_threads": grid, "lds_bytes": lds, "fetch_kib": round(kf, 3),
+           "write_kib": round(kw, 3), "fetch_scale": round(COPY_BYTES / 1024 / cf, 5),
+           "write_scale": round(COPY_BYTES / 1024 / cw, 5), "kernel_source_sha256": bench.kernel_source_hash()}
+    tb = rec["fetch_kib"] * 1024 * rec["fetch_scale"] + rec["write_kib"] * 1024 * rec["write_scale"]
+    lines = [f"# HBM traffic counters: {kernel} ({name_sub}, grid {grid} threads, {lds} B dynamic LDS)", "",
+             "FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each from a rocprofv3 pass of its own, scaled",
+             f"by what the same counter reads for a plain {COPY_BYTES >> 30} GiB device-to-device copy",
+             f"(`__amd_rocclr_copyBuffer`): the copy reads {cf:.2f} KiB of FETCH_SIZE (scale "
+             f"{rec['fetch_scale']}) and {cw:.2f} KiB of WRITE_SIZE (scale {rec['write_scale']}).", "",
+             f"{kernel}: {kf:.1f} KiB fetched x {rec['fetch_scale']} + {kw:.1f} KiB written x {rec['write_scale']}"
+             f" = {tb / 1e6:.2f} MB per launch (mean over {nf} / {nw} dispatches).", "",
+             "Commands (one MI355X, library built by `__graft_entry__.build()`):", "",
+             COMMANDS.format(args=f"{kernel} '{name_sub}' {grid} {lds} {out}"), ""]
+    for c in ("copy_FETCH_SIZE", "copy_WRITE_SIZE", "bench_FETCH_SIZE", "bench_WRITE_SIZE"):
+        import io
+        import contextlib
+        buf = io.StringIO()
+        with contextlib.redirect_stdout(buf):
+            pmc_summary(sqlite3.connect(run(c)), [], 1 if c.startswith("copy") else 100)
+        lines += ["```", buf.getvalue().rstrip(), "```", ""]
+    lines += ["Machine-readable record read by bench.py (`roofline.traffic` is reported only while the",
+              "kernel sources hash to the value below):", "", "traffic-json: " + json.dumps(rec)]
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print(json.dumps(rec))
+
+
 def main():
     args = sys.argv[1:]
+    if args and args[0] == "--traffic":
+        traffic(args[1:])
+        return
+    pmc = "--pmc" in args
+    if pmc:
+        args.remove("--pmc")
     min_calls = 1
     if "--min-calls" in args:
         i = args.index("--min-calls")
@@ -19,6 +121,9 @@ def main():
         del args[i:i + 2]
     db = sqlite3.connect(args[0])
     filt = args[1:]
+    if pmc:
+        pmc_summary(db, filt, min_calls)
+        return
     rows = db.execute(
         "select name, grid_x, grid_y, grid_z, workgroup_x, lds_size, vgpr_count, accum_vgpr_count, sgpr_count, "
         "count(*), sum(duration), avg(duration), min(duration), max(duration) from kernels "
