@@ -29,13 +29,26 @@ static constexpr int ATT_CHUNK = 64;
 static constexpr int ATT_WAVES = 4;
 static constexpr int ATT_GROUP = ATT_CHUNK * ATT_WAVES;
 
+__device__ __forceinline__ void store_coherent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float load_coherent(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <int HD, bool COHERENT>
+__device__ void merge_groups(const AttnArgs& a, const float* part0, int e, int n_groups, int mrow0, int h);
+
 template <typename T, int HD, int QT>
 __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
   constexpr int DS = HD / 32;    // 32-dim steps of S^T
   constexpr int DT = HD / 16;    // 16-dim tiles of O^T
   constexpr int PS = HD + 4;     // floats per query vector in a group partial
-  __shared__ float s_o[ATT_WAVES - 1][32][HD];
-  __shared__ float s_ml[ATT_WAVES - 1][32][2];
+  // chunk partials for the in-group merge; rows padded by 4 floats so that the 16 query lanes
+  // reading one column fall in different banks
+  __shared__ float s_o[ATT_WAVES][32][HD + 4];
+  __shared__ float s_ml[ATT_WAVES][32][2];
+  __shared__ int s_last;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, tl = lane & 15, kg = lane >> 4;
   const int g = blockIdx.x;
   const int h = blockIdx.y % a.n_kv, rb = blockIdx.y / a.n_kv;
@@ -197,66 +210,114 @@ __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
       }
   }
 
-  // ---- merge the group's 4 chunks left to right (wave 0 holds chunk 0) ----
-  if (wave > 0) {
+  // ---- merge the group's 4 chunks left to right: every wave parks its chunk partial in LDS,
+  // then thread e merges query vector e / (HD/4), columns 4*(e mod HD/4).., chunk 0 first ----
 #pragma unroll
-    for (int qt = 0; qt < QT; ++qt) {
-      const int qv = qt * 16 + tl;
-      if (qv >= nqv) continue;
+  for (int qt = 0; qt < QT; ++qt) {
+    const int qv = qt * 16 + tl;
+    if (qv >= nqv) continue;
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-        *reinterpret_cast<float4*>(&s_o[wave - 1][qv][dt * 16 + 4 * kg]) =
-            make_float4(o_c[qt][dt][0], o_c[qt][dt][1], o_c[qt][dt][2], o_c[qt][dt][3]);
-      if (kg == 0) {
-        s_ml[wave - 1][qv][0] = m_c[qt];
-        s_ml[wave - 1][qv][1] = l_c[qt];
-      }
+    for (int dt = 0; dt < DT; ++dt)
+      *reinterpret_cast<float4*>(&s_o[wave][qv][dt * 16 + 4 * kg]) =
+          make_float4(o_c[qt][dt][0], o_c[qt][dt][1], o_c[qt][dt][2], o_c[qt][dt][3]);
+    if (kg == 0) {
+      s_ml[wave][qv][0] = m_c[qt];
+      s_ml[wave][qv][1] = l_c[qt];
     }
   }
   __syncthreads();
   float* part = a.part + ((((size_t)(b * a.n_kv + h) * a.n_rb + rb) * a.n_groups_max + g) * 32) * PS;
-  if (wave == 0) {
+  constexpr int HD4 = HD / 4;
+  for (int e = threadIdx.x; e < nqv * HD4; e += blockDim.x) {
+    const int qv = e / HD4, d = (e - qv * HD4) * 4;
+    const float4 v0 = *reinterpret_cast<const float4*>(&s_o[0][qv][d]);
+    float m_r = s_ml[0][qv][0], l_r = s_ml[0][qv][1], o_r[4] = {v0.x, v0.y, v0.z, v0.w};
 #pragma unroll
-    for (int qt = 0; qt < QT; ++qt) {
-      const int qv = qt * 16 + tl;
-      if (qv >= nqv) continue;
-      for (int w = 0; w < ATT_WAVES - 1; ++w) {
-        float oc[DT * 4];
+    for (int w = 1; w < ATT_WAVES; ++w) {
+      const float4 v = *reinterpret_cast<const float4*>(&s_o[w][qv][d]);
+      const float oc[4] = {v.x, v.y, v.z, v.w};
+      softmax_merge(m_r, l_r, o_r, s_ml[w][qv][0], s_ml[w][qv][1], oc, 4);
+    }
+    if (n_groups == 1) {
+      // the only group: the merge of groups reduces to o / l for it (weight 1), so finish here
+      const int rl = qv / a.G, gq = qv - rl * a.G;
+      *reinterpret_cast<float4*>(a.out + (size_t)(mrow0 + rl) * qstride + (h * a.G + gq) * HD + d) =
+          make_float4(o_r[0] / l_r, o_r[1] / l_r, o_r[2] / l_r, o_r[3] / l_r);
+    } else if (a.fused_combine) {
+      // agent-coherent stores (written through to the level every XCD reads from): the merge of
+      // groups runs in this launch
+      float* pp = part + (size_t)qv * PS;
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-          const float4 v = *reinterpret_cast<const float4*>(&s_o[w][qv][dt * 16 + 4 * kg]);
-          oc[dt * 4 + 0] = v.x; oc[dt * 4 + 1] = v.y; oc[dt * 4 + 2] = v.z; oc[dt * 4 + 3] = v.w;
-        }
-        softmax_merge(m_c[qt], l_c[qt], &o_c[qt][0][0], s_ml[w][qv][0], s_ml[w][qv][1], oc, DT * 4);
+      for (int i = 0; i < 4; ++i) store_coherent(pp + d + i, o_r[i]);
+      if (d == 0) {
+        store_coherent(pp + HD, m_r);
+        store_coherent(pp + HD + 1, l_r);
       }
-      if (n_groups == 1) {
-        // the only group: the combine below reduces to o / l for it (weight 1), so finish here
-        const int rl = qv / a.G, gq = qv - rl * a.G;
-        float* op = a.out + (size_t)(mrow0 + rl) * qstride + (h * a.G + gq) * HD;
-        const float l = l_c[qt];
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-          *reinterpret_cast<float4*>(op + dt * 16 + 4 * kg) =
-              make_float4(o_c[qt][dt][0] / l, o_c[qt][dt][1] / l, o_c[qt][dt][2] / l, o_c[qt][dt][3] / l);
-      } else {
-        float* pp = part + (size_t)qv * PS;
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-          *reinterpret_cast<float4*>(pp + dt * 16 + 4 * kg) =
-              make_float4(o_c[qt][dt][0], o_c[qt][dt][1], o_c[qt][dt][2], o_c[qt][dt][3]);
-        if (kg == 0) {
-          pp[HD] = m_c[qt];
-          pp[HD + 1] = l_c[qt];
-        }
-      }
+    } else {
+      // plain stores: k_attn_combine reads them after this launch has ended
+      float* pp = part + (size_t)qv * PS;
+      *reinterpret_cast<float4*>(pp + d) = make_float4(o_r[0], o_r[1], o_r[2], o_r[3]);
+      if (d == 0) *reinterpret_cast<float2*>(pp + HD) = make_float2(m_r, l_r);
     }
   }
+  if (n_groups == 1 || !a.fused_combine) return;
+
+  // ---- fused combine: the last group of (b, h, rb) to finish merges all group partials ----
+  // Every wave waits for its coherent stores to complete before the barrier; then one relaxed
+  // agent-scope count per workgroup (no L2 write-back or invalidate is needed: the partials
+  // travel through coherent stores and loads).
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  int* cnt = a.cnt + (b * a.n_kv + h) * a.n_rb + rb;
+  if (threadIdx.x == 0)
+    s_last = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == n_groups - 1;
+  __syncthreads();
+  if (!s_last) return;
+  const float* part0 = a.part + ((((size_t)(b * a.n_kv + h) * a.n_rb + rb) * a.n_groups_max) * 32) * PS;
+  for (int e = threadIdx.x; e < nqv * (HD / 4); e += blockDim.x)
+    merge_groups<HD, true>(a, part0, e, n_groups, mrow0, h);
+  if (threadIdx.x == 0) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Merge the group partials of each query left to right (online softmax merge, fixed order).
-// Thread e owns columns 4*(e mod HD/4).. of query vector e / (HD/4). The first 8 groups are
-// loaded before the group count is known (the partial buffer holds n_groups_max groups), so a
-// short context costs one round trip after the position read.
+// Merge the group partials of query vector e / (HD/4), columns 4*(e mod HD/4).., left to right
+// (online softmax merge from the identity, fixed order) and write the normalised output. Each
+// batch of 8 groups is loaded at once; COHERENT reads them with agent-coherent loads (the fused
+// combine inside k_attention reads partials other workgroups wrote during the same launch).
+template <int HD, bool COHERENT>
+__device__ void merge_groups(const AttnArgs& a, const float* part0, int e, int n_groups, int mrow0, int h) {
+  constexpr int PS = HD + 4, HD4 = HD / 4;
+  const int qv = e / HD4, d = (e - qv * HD4) * 4;
+  const float* pq = part0 + (size_t)qv * PS;
+  float m_r = NEG_INF, l_r = 0.f, o_r[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int g0 = 0; g0 < n_groups; g0 += 8) {
+    float mg[8], lg[8], og[8][4];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const float* pp = pq + (size_t)min(g0 + u, n_groups - 1) * 32 * PS;
+      if (COHERENT) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) og[u][i] = load_coherent(pp + d + i);
+        mg[u] = load_coherent(pp + HD);
+        lg[u] = load_coherent(pp + HD + 1);
+      } else {
+        const float4 v = *reinterpret_cast<const float4*>(pp + d);
+        const float2 ml = *reinterpret_cast<const float2*>(pp + HD);
+        og[u][0] = v.x; og[u][1] = v.y; og[u][2] = v.z; og[u][3] = v.w;
+        mg[u] = ml.x;
+        lg[u] = ml.y;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (g0 + u < n_groups) softmax_merge(m_r, l_r, o_r, mg[u], lg[u], og[u], 4);
+  }
+  const int rl = qv / a.G, gq = qv - rl * a.G;
+  *reinterpret_cast<float4*>(a.out + (size_t)(mrow0 + rl) * a.n_heads * HD + (h * a.G + gq) * HD + d) =
+      make_float4(o_r[0] / l_r, o_r[1] / l_r, o_r[2] / l_r, o_r[3] / l_r);
+}
+
+// Separate merge of the group partials (contexts that can span many groups): thread e of the
+// grid's x extent owns one (query vector, 4 columns).
 template <int HD>
 __global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
   constexpr int PS = HD + 4, HD4 = HD / 4;
@@ -269,34 +330,10 @@ __global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
   const int mrow0 = b * a.R + r0;
   const int e = blockIdx.x * blockDim.x + threadIdx.x;
   if (e >= nqv * HD4) return;
-  const int qv = e / HD4, d = (e - qv * HD4) * 4;
-  const float* part0 = a.part + ((((size_t)(b * a.n_kv + h) * a.n_rb + rb) * a.n_groups_max) * 32 + qv) * PS;
-  const int maxpos = a.row_pos[mrow0 + nr - 1];
-  float m_r = NEG_INF, l_r = 0.f, o_r[4] = {0.f, 0.f, 0.f, 0.f};
-  int n_groups = -1;
-  for (int g0 = 0; g0 < a.n_groups_max; g0 += 8) {
-    float mg[8], lg[8], og[8][4];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const float* pp = part0 + (size_t)min(g0 + u, a.n_groups_max - 1) * 32 * PS;
-      const float4 v = *reinterpret_cast<const float4*>(pp + d);
-      const float2 ml = *reinterpret_cast<const float2*>(pp + HD);
-      og[u][0] = v.x; og[u][1] = v.y; og[u][2] = v.z; og[u][3] = v.w;
-      mg[u] = ml.x;
-      lg[u] = ml.y;
-    }
-    if (n_groups < 0) {
-      n_groups = maxpos / ATT_GROUP + 1;
-      if (n_groups == 1) return;   // k_attention wrote the final output
-    }
-#pragma unroll
-    for (int u = 0; u < 8; ++u)
-      if (g0 + u < n_groups) softmax_merge(m_r, l_r, o_r, mg[u], lg[u], og[u], 4);
-    if (g0 + 8 >= n_groups) break;
-  }
-  const int rl = qv / a.G, gq = qv - rl * a.G;
-  *reinterpret_cast<float4*>(a.out + (size_t)(mrow0 + rl) * a.n_heads * HD + (h * a.G + gq) * HD + d) =
-      make_float4(o_r[0] / l_r, o_r[1] / l_r, o_r[2] / l_r, o_r[3] / l_r);
+  const int n_groups = a.row_pos[mrow0 + nr - 1] / ATT_GROUP + 1;
+  if (n_groups == 1) return;   // k_attention wrote the final output
+  const float* part0 = a.part + ((((size_t)(b * a.n_kv + h) * a.n_rb + rb) * a.n_groups_max) * 32) * PS;
+  merge_groups<HD, false>(a, part0, e, n_groups, mrow0, h);
 }
 
 template <typename T, int HD>
@@ -324,7 +361,7 @@ void launch_attention(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev) 
   else launch_attention_hd<T, 64>(a, s, ev);
 }
 
-bool attention_needs_combine(const AttnArgs& a) { return a.n_groups_max > 1; }
+bool attention_needs_combine(const AttnArgs& a) { return a.n_groups_max > 1 && !a.fused_combine; }
 
 void launch_attn_combine(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev) {
   if (a.head_dim == 128) launch_attn_combine_hd<128>(a, s, ev);

@@ -76,6 +76,9 @@ struct AttnArgs {
   int n_groups_max;       // grid extent over groups of 256 positions
   float scale_log2;       // log2(e) / sqrt(head_dim)
   float* part;            // group partials [B][n_kv][n_rb][n_groups_max][32][head_dim + 4]
+  int fused_combine;      // 1: the last group's workgroup merges the partials (k_attention);
+                          // 0: k_attn_combine merges them
+  int* cnt;               // fused combine: finished-group counters [B][n_kv][n_rb] (zero between launches)
   float* out;             // [M][n_heads*head_dim]
 };
 
@@ -149,7 +152,8 @@ void launch_linear(const LinArgs& a, int prologue, int epilogue, int kind, hipSt
 // Attention partials per group of 256 positions (the final output when the rows see one group).
 template <typename T>
 void launch_attention(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev = nullptr);
-// Merge of the group partials; needed when the context can span more than one group.
+// Merge of the group partials as a kernel of its own; needed when the context can span more
+// than one group and the merge is not fused into k_attention.
 bool attention_needs_combine(const AttnArgs& a);
 void launch_attn_combine(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev = nullptr);
 template <typename T>

@@ -55,7 +55,7 @@ struct Plan {
   std::vector<size_t> w_attn_norm, w_mlp_norm, w_qkv, w_o, w_gu, w_down;
   size_t kv_total;
   // workspace
-  size_t o_h, o_xg, o_ssq, o_q, o_attn, o_act, o_part, o_row_seq, o_row_pos, o_row_blk, o_row_rope, o_amax_val,
+  size_t o_h, o_xg, o_ssq, o_q, o_attn, o_act, o_part, o_cnt, o_row_seq, o_row_pos, o_row_blk, o_row_rope, o_amax_val,
       o_amax_idx, o_vtok;
   size_t o_t, o_len, o_limit, o_active, o_nacc, o_bonus, o_rounds, o_counters, o_drafts, o_tokens,
       o_trace, o_log, o_bt, o_scratch, ws_total;
@@ -132,6 +132,7 @@ Plan make_plan(const seed_config& c) {
   p.o_attn = take(R * p.QD * 4);
   p.o_act = take(R * p.F * 4);
   p.o_part = take(B * p.NKV * p.n_rb_max * (size_t)p.n_groups_max * 32 * (p.HD + 4) * 4);
+  p.o_cnt = take(B * p.NKV * p.n_rb_max * 4);
   p.o_row_seq = take(R * 4);
   p.o_row_pos = take(R * 4);
   p.o_row_blk = take(R * 4);
@@ -362,6 +363,12 @@ void run_layers(seed_ctx* c, int M, int B, int R, int l0, int l1, int phase,
     at.n_heads = p.NQ; at.n_kv = p.NKV; at.head_dim = p.HD; at.G = p.G;
     at.RB = p.RB; at.n_rb = cdiv(R, p.RB);
     at.n_groups_max = p.n_groups_max;
+    // When the merge is one pass of the workgroup (a row-block of at most 256/(head_dim/4)
+    // query vectors, e.g. draft rows) and the context spans at most 8 groups, the last group's
+    // workgroup merges the partials; otherwise the separate combine kernel does (same merge
+    // order, so both give identical results).
+    at.fused_combine = p.n_groups_max <= 8 && std::min(p.RB, R) * p.G * (p.HD / 4) <= 256;
+    at.cnt = c->ws<int>(p.o_cnt);
     at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)p.HD));
     at.part = c->ws<float>(p.o_part);
     at.out = c->ws<float>(p.o_attn);
