@@ -119,6 +119,116 @@ def copy_calibration(torch):
 
 
 # ------------------------------------------------------------------------------------------
+# every workload at measured and forced acceptance
+# ------------------------------------------------------------------------------------------
+SWEEP = (("tiny-4L-h256", (4,)), ("28L-h2048", (4,)), ("4B-36L-h2560", (2, 4, 6)),
+         ("4B-36L-h2560-b8", (4,)), ("4B-36L-h2560-16k", (4,)))
+
+
+def step_latency(dec, k, torch, n=8):
+    """Median verify latency and per-draft-step latency (HIP events) at the current state."""
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    ver, dr = [], []
+    for _ in range(n):
+        ev[0].record(dec.stream)
+        if k:
+            dec.draft(k)
+        ev[1].record(dec.stream)
+        dec.verify(k)
+        ev[2].record(dec.stream)
+        dec.stream.synchronize()
+        if k:
+            dr.append(ev[0].elapsed_time(ev[1]) / k)
+        ver.append(ev[1].elapsed_time(ev[2]))
+    return statistics.median(ver), (statistics.median(dr) if dr else 0.0)
+
+
+def measure_config(cfg, k, weights, torch):
+    lens = synth.make_prompt_lengths(cfg)
+    prompts = synth.make_prompts(cfg, lengths=lens)
+    B, gen = len(prompts), cfg.gen_len
+    dec = binding.Decoder(cfg, max_batch=B, max_ctx=max(lens) + gen + 2 * 7 + 2, max_draft=max(k, 1))
+    dec.load_weights(weights)
+    res = {"workload": cfg.name, "batch": B, "k": k, "prompt_lens": lens if B > 1 else lens[0], "gen": gen}
+    out0, _, st0 = dec.generate(prompts, 0, gen, use_graph=True)
+    res["greedy_tokens_per_s"] = round(B * gen / (st0["decode_ms"] * 1e-3), 2)
+    out, cnt, st = dec.generate(prompts, k, gen, use_graph=True)
+    res["measured"] = {"tokens_per_s": round(int(cnt.sum()) / (st["decode_ms"] * 1e-3), 2),
+                       "mean_accept": round(st["accepted"] / max(1, st["rounds"] * B), 4),
+                       "output_equals_greedy": bool(np.array_equal(out, out0))}
+    dec.prefill(prompts)
+    t_ver, t_dr = step_latency(dec, k, torch)
+    Lm = int(np.mean(lens)) + 3
+    vb = step_bytes(cfg, B * (k + 1), Lm, cfg.n_layers) + (B - 1) * cfg.n_layers * kernel_bytes(
+        cfg, binding.OP_ATTN, 0, Lm)
+    db = step_bytes(cfg, B, Lm, cfg.n_dec_layers) + (B - 1) * cfg.n_dec_layers * kernel_bytes(
+        cfg, binding.OP_ATTN, 0, Lm)
+    res["verify_ms"], res["draft_step_ms"] = round(t_ver, 4), round(t_dr, 4)
+    res["verify_gbps"] = round(vb / (t_ver * 1e-3) / 1e9, 1)
+    res["verify_frac"] = round(vb / (t_ver * 1e-3) / PEAK_HBM, 4)
+    if k:
+        res["draft_gbps"] = round(db / (t_dr * 1e-3) / 1e9, 1)
+        res["draft_frac"] = round(db / (t_dr * 1e-3) / PEAK_HBM, 4)
+    forced = {}
+    for a in range(k + 1):
+        o, c, sa = dec.generate(prompts, k, gen, sim_accept=a, forced_trace=out0, use_graph=True)
+        meas = int(c.sum()) / (sa["decode_ms"] * 1e-3)
+        # cost model of the Computational Cost Analysis appendix with the measured step latencies:
+        # B (a+1) tokens per round of k draft steps and one verification
+        pred = B * (a + 1) / ((k * t_dr + t_ver) * 1e-3)
+        forced[str(a)] = {"tokens_per_s": round(meas, 2), "model_tokens_per_s": round(pred, 2),
+                          "output_equals_greedy": bool(np.array_equal(o, out0))}
+    res["forced_acceptance"] = forced
+    dec.close()
+    return res
+
+
+def config_sweep(torch, out_md):
+    results, cache = [], {}
+    t0 = time.perf_counter()
+    for name, ks in SWEEP:
+        cfg = synth.CONFIGS[name]
+        key = (cfg.n_layers, cfg.hidden, cfg.ffn, cfg.vocab, cfg.dtype)
+        if key not in cache:
+            cache.clear()
+            log(f"[sweep] weights for {name}")
+            cache[key] = synth.make_weights(cfg)
+        for k in ks:
+            log(f"[sweep] {name} k={k}")
+            r = measure_config(cfg, k, cache[key], torch)
+            log(f"[sweep] {json.dumps(r)}")
+            results.append(r)
+            torch.cuda.empty_cache()
+    lines = ["# Decode throughput on every workload (one MI355X)", "",
+             "Command: `python3 bench.py --config-sweep " + out_md + "` (repository root, library built by",
+             "`__graft_entry__.build()`). Random-init weights (seed 0), uniform-random prompts (seed 1),",
+             "ragged batch lengths (seed 2); rounds replayed from HIP graphs. `measured` = real drafts",
+             "(acceptance ~0 with random weights); `forced a` = drafts overridden after the draft kernels",
+             "ran so that exactly a are accepted each round; `model` = the cost model B(a+1)/(k t_draft +",
+             "t_verify) with the step latencies measured in the same run; greedy = plain greedy decoding",
+             "(k = 0). Bytes are algorithmic (weights + KV read at the mean context).", "",
+             "| workload | B | k | greedy tok/s | measured tok/s (accept) | verify ms (TB/s, frac) | draft step ms "
+             "(TB/s, frac) | forced a: tok/s (model) | spec == greedy |",
+             "|---|---|---|---|---|---|---|---|---|"]
+    for r in results:
+        fa = "; ".join(f"{a}: {v['tokens_per_s']:.0f} ({v['model_tokens_per_s']:.0f})"
+                       for a, v in r["forced_acceptance"].items())
+        ok = r["measured"]["output_equals_greedy"] and all(v["output_equals_greedy"]
+                                                            for v in r["forced_acceptance"].values())
+        dr = (f"{r['draft_step_ms']:.3f} ({r['draft_gbps'] / 1e3:.2f}, {r['draft_frac']:.2f})"
+              if r["k"] else "-")
+        lines.append(f"| {r['workload']} | {r['batch']} | {r['k']} | {r['greedy_tokens_per_s']:.0f} | "
+                     f"{r['measured']['tokens_per_s']:.0f} ({r['measured']['mean_accept']:.2f}) | "
+                     f"{r['verify_ms']:.3f} ({r['verify_gbps'] / 1e3:.2f}, {r['verify_frac']:.2f}) | {dr} | "
+                     f"{fa} | {ok} |")
+    lines += ["", "Raw results:", "", "```json"] + [json.dumps(r) for r in results] + ["```"]
+    with open(out_md, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    log(f"[sweep] done in {time.perf_counter() - t0:.1f}s")
+    print(json.dumps({"config_sweep": out_md, "workloads": len(results)}), flush=True)
+
+
+# ------------------------------------------------------------------------------------------
 # CPU oracle baseline
 # ------------------------------------------------------------------------------------------
 def cpu_baseline(cfg, weights, prompt, k, rounds):
@@ -159,6 +269,9 @@ def main():
                     help="only prefill + eager rounds (for rocprofv3 counter passes)")
     ap.add_argument("--copy-calib", action="store_true",
                     help="only a plain 1 GiB device-to-device copy (counter calibration)")
+    ap.add_argument("--config-sweep", metavar="OUT_MD",
+                    help="measure every workload (tiny, 28L, 4B k=2/4/6, 4B batch 8, 4B 16k) at the "
+                         "measured and forced acceptance lengths and write a summary to OUT_MD")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
@@ -168,6 +281,9 @@ def main():
 
     if args.copy_calib:
         copy_calibration(torch)
+        return
+    if args.config_sweep:
+        config_sweep(torch, args.config_sweep)
         return
 
     cfg = synth.CONFIGS[args.config]
