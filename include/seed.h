@@ -127,7 +127,7 @@ typedef struct seed_stats {
 
 /* Kernel ids for seed_kernel_timing: phase * 16 + op. SEED_OP_ATTN times the attention partial
  * kernel, SEED_OP_COMBINE the merge of its group partials (launched when the context capacity
- * spans more than one 256-position group). */
+ * spans more than one attention group of 64, 128 or 256 positions). */
 enum {
   SEED_PHASE_VERIFY = 0, SEED_PHASE_DRAFT = 1, SEED_PHASE_PREFILL = 2,
   SEED_OP_SETUP = 0, SEED_OP_QKV = 1, SEED_OP_ATTN = 2, SEED_OP_COMBINE = 3, SEED_OP_O = 4,

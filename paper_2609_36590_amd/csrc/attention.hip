@@ -1,54 +1,85 @@
 // Paged split-KV attention on MFMA for the verify, draft and prefill passes.
 //
-// k_attention: one workgroup = 4 waves = one group of 256 absolute positions (4 chunks of 64) for
-// one (sequence b, KV head h, row-block rb). The queries of a row-block (G query heads x RB rows,
-// <= 32) are the MFMA B operand. Per chunk, a wave computes S^T = K Q^T with the paged K block
-// rows as the A operand, masks positions later than each query's own, takes the chunk softmax in
-// base 2, and forms O^T = V^T P^T with the transposed V block as the A operand. The wave issues
-// its block-table reads together with the row positions, then all K/V loads of its chunk and the
-// query loads, so it waits for two memory round trips. The group's 4 chunks are merged left to
-// right in LDS and written as one partial (o, m, l), or as the final output when the rows see a
-// single group.
+// The unit of work is one 16-position paged KV block (a "tile"). A wave takes a run of `tpw`
+// consecutive tiles of one (sequence b, KV head h, row-block rb); a workgroup of 4 waves takes 4
+// consecutive runs, one "group" of span = 64 * tpw absolute positions. The queries of a
+// row-block (G query heads x RB rows, <= 32 query vectors) are the MFMA B operand:
+//   S^T = K Q^T     16x16x32 MFMAs, the block's K rows as the A operand (k = head dim);
+//   O^T += V^T P^T  16x16x16 MFMAs, the block's transposed V as the A operand (k = positions).
+// After S^T, lane (qv, kg) holds the scores of positions 4kg..4kg+3 of the tile for query vector
+// qv, which is exactly the k-slot layout O^T needs for P^T: no cross-lane shuffle of P.
+// Positions later than a query's own are masked; a wave keeps an online softmax (base 2) over its
+// tiles. The 4 waves' partials are merged left to right in LDS and written as the group partial
+// (o, m, l), or as the final output when the pass sees a single group.
 //
-// k_attn_combine merges the group partials of each query left to right. A chunk or group with no
-// visible position is an exact identity of the merge, so a query's result depends only on the
-// positions it attends to, not on how many rows share the pass (verify rows vs plain greedy
-// decoding give bit-identical outputs).
-//
-// Position tile pt (16 positions) of chunk base P0, MFMA row r <-> position
-//   P0 + 32*(pt>>1) + 8*(r>>2) + (r&3) + 4*(pt&1),
-// so after S^T the lane group kg holds positions 8kg..8kg+7 of each 32-position step, which is
-// exactly the k-slot layout O^T needs for P^T: no cross-lane shuffle of P.
+// k_attn_combine merges the group partials of each query vector with a fixed tree: lane j of an
+// 8-lane team merges groups j, j+8, j+16, ... left to right, then the 8 results are merged
+// pairwise (0+1, 2+3, ..; then 01+23, ..). A tile, run or group with no visible position is an
+// exact identity of every merge, and the tree's shape depends only on absolute group indices, so
+// a query's result depends only on the positions it attends to, not on how many rows share the
+// pass: verify rows and plain greedy decoding give bit-identical outputs, and so do a sequence
+// decoded alone and inside a batch.
 #include "device_common.h"
 
 #include <algorithm>
 
 namespace seedk {
 
-static constexpr int ATT_CHUNK = 64;
 static constexpr int ATT_WAVES = 4;
-static constexpr int ATT_GROUP = ATT_CHUNK * ATT_WAVES;
+static constexpr int CMB_LANES = 8;
 
-__device__ __forceinline__ void store_coherent(float* p, float v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float load_coherent(const float* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
+// 16-position contraction (k = 16) for O^T: 4 stored elements per lane as the A operand, 4 fp32
+// probabilities per lane as the B operand (bf16 hi/lo pair, or fp32 for fp32 caches).
+template <typename T>
+struct PV;
 
-template <int HD, bool COHERENT>
-__device__ void merge_groups(const AttnArgs& a, const float* part0, int e, int n_groups, int mrow0, int h);
+template <>
+struct PV<uint16_t> {
+  typedef __attribute__((ext_vector_type(4))) short s16x4;
+  struct A { uint2 v; };
+  struct B { s16x4 hi, lo; };
+  __device__ static A load(const uint16_t* p) { return A{*reinterpret_cast<const uint2*>(p)}; }
+  __device__ static B split(const float x[4]) {
+    B r;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint16_t h = f2bf(x[j]);
+      r.hi[j] = (short)h;
+      r.lo[j] = (short)f2bf(x[j] - bf2f(h));
+    }
+    return r;
+  }
+  __device__ static void mma(f32x4& acc, const A& a, const B& b) {
+    const s16x4 av = __builtin_bit_cast(s16x4, a.v);
+    acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(av, b.hi, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(av, b.lo, acc, 0, 0, 0);
+  }
+};
 
-template <typename T, int HD, int QT>
+template <>
+struct PV<float> {
+  struct A { float4 v; };
+  struct B { float x[4]; };
+  __device__ static A load(const float* p) { return A{*reinterpret_cast<const float4*>(p)}; }
+  __device__ static B split(const float x[4]) { return B{{x[0], x[1], x[2], x[3]}}; }
+  __device__ static void mma(f32x4& acc, const A& a, const B& b) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.v.x, b.x[0], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.v.y, b.x[1], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.v.z, b.x[2], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a.v.w, b.x[3], acc, 0, 0, 0);
+  }
+};
+
+template <typename T, int HD, int QT, int TPW>
 __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
   constexpr int DS = HD / 32;    // 32-dim steps of S^T
   constexpr int DT = HD / 16;    // 16-dim tiles of O^T
   constexpr int PS = HD + 4;     // floats per query vector in a group partial
-  // chunk partials for the in-group merge; rows padded by 4 floats so that the 16 query lanes
+  constexpr int SPAN = ATT_WAVES * TPW * 16;
+  // run partials for the in-group merge; rows padded by 4 floats so that the 16 query lanes
   // reading one column fall in different banks
   __shared__ float s_o[ATT_WAVES][32][HD + 4];
   __shared__ float s_ml[ATT_WAVES][32][2];
-  __shared__ int s_last;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, tl = lane & 15, kg = lane >> 4;
   const int g = blockIdx.x;
   const int h = blockIdx.y % a.n_kv, rb = blockIdx.y / a.n_kv;
@@ -59,18 +90,16 @@ __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
   const int nqv = nr * a.G;
   const int mrow0 = b * a.R + r0;
   const int qstride = a.n_heads * HD;
-  const int P0 = (g * ATT_WAVES + wave) * ATT_CHUNK;
+  const int P0 = (g * ATT_WAVES + wave) * TPW * 16;   // first position of this wave's run
   const T* kvp = reinterpret_cast<const T*>(a.kv);
   const int* btp = a.bt + b * a.bt_stride;   // the grid covers exactly bt_stride * 16 positions
   const size_t layer_base = (size_t)a.layer * a.n_blocks;
 
-  // ---- round trip 1: the last row's position and this wave's block-table entries ----
+  // ---- round trip 1: the last row's position, the run's block-table entries, the queries ----
   const int maxpos = a.row_pos[mrow0 + nr - 1];
-  int kblk[4], vblk[2];
+  int blk[TPW];
 #pragma unroll
-  for (int pt = 0; pt < 4; ++pt) kblk[pt] = btp[(P0 + 32 * (pt >> 1) + 8 * (tl >> 2) + (tl & 3) + 4 * (pt & 1)) >> 4];
-#pragma unroll
-  for (int s = 0; s < 2; ++s) vblk[s] = btp[(P0 + 32 * s + 8 * kg) >> 4];
+  for (int t = 0; t < TPW; ++t) blk[t] = btp[(P0 >> 4) + t];
   // queries (lane column qv = qt*16 + tl, k-slots d = ds*32 + kg*8 + j) and their positions:
   // loaded branch-free from a valid row, masked when converted
   float qraw[QT][DS][8];
@@ -87,27 +116,24 @@ __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
     for (int ds = 0; ds < DS; ++ds) load8(qp + ds * 32, qraw[qt][ds]);
   }
   __builtin_amdgcn_sched_barrier(0);
-  const int n_groups = maxpos / ATT_GROUP + 1;
+  const int n_groups = maxpos / SPAN + 1;
   if (g >= n_groups) return;
-  const bool live = P0 <= maxpos;
+  const int n_live = P0 > maxpos ? 0 : min(TPW, ((maxpos - P0) >> 4) + 1);   // tiles with a visible position
 
-  // ---- round trip 2: the chunk's K and V, then the queries ----
-  typename ET<T>::A kf[4][DS];
-  typename ET<T>::A vf[2][DT];
-  if (live) {
+  // ---- round trip 2: the run's K and V tiles ----
+  // K: lane (tl, kg) holds K[position tl][d = ds*32 + kg*8 + j]; V^T: lane holds V[positions
+  // 4kg..4kg+3][d = dt*16 + tl] (the cache keeps V transposed per block)
+  typename ET<T>::A kf[TPW][DS];
+  typename PV<T>::A vf[TPW][DT];
 #pragma unroll
-    for (int pt = 0; pt < 4; ++pt) {
-      const int pos = P0 + 32 * (pt >> 1) + 8 * (tl >> 2) + (tl & 3) + 4 * (pt & 1);
-      const T* kp = kvp + (((layer_base + kblk[pt]) * 2 + 0) * a.n_kv + h) * 16 * HD + (pos & 15) * HD + kg * 8;
+  for (int t = 0; t < TPW; ++t) {
+    if (t < n_live) {
+      const T* kp = kvp + (((layer_base + blk[t]) * 2 + 0) * a.n_kv + h) * 16 * HD + tl * HD + kg * 8;
 #pragma unroll
-      for (int ds = 0; ds < DS; ++ds) kf[pt][ds] = ET<T>::load(kp + ds * 32);
-    }
+      for (int ds = 0; ds < DS; ++ds) kf[t][ds] = ET<T>::load(kp + ds * 32);
+      const T* vp = kvp + (((layer_base + blk[t]) * 2 + 1) * a.n_kv + h) * HD * 16 + tl * 16 + 4 * kg;
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      const int pos = P0 + 32 * s + 8 * kg;
-      const T* vp = kvp + (((layer_base + vblk[s]) * 2 + 1) * a.n_kv + h) * HD * 16 + tl * 16 + (pos & 15);
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) vf[s][dt] = ET<T>::load(vp + dt * 16 * 16);
+      for (int dt = 0; dt < DT; ++dt) vf[t][dt] = PV<T>::load(vp + dt * 16 * 16);
     }
   }
   // keep every K/V load here, ahead of all arithmetic: left to itself the scheduler trades them
@@ -118,100 +144,76 @@ __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
   typename ET<T>::B qf[QT][DS];
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
-    if (!(live && qok[qt])) qpos[qt] = -1;
+    if (!qok[qt]) qpos[qt] = -1;
 #pragma unroll
     for (int ds = 0; ds < DS; ++ds) {
       float x[8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) x[j] = (live && qok[qt]) ? qraw[qt][ds][j] * a.scale_log2 : 0.f;
+      for (int j = 0; j < 8; ++j) x[j] = qok[qt] ? qraw[qt][ds][j] * a.scale_log2 : 0.f;
       qf[qt][ds] = ET<T>::split(x);
     }
   }
 
+  // ---- online softmax over the run's tiles, left to right ----
   float m_c[QT], l_c[QT];
-  float o_c[QT][DT][4];
+  f32x4 o_c[QT][DT];
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
     m_c[qt] = NEG_INF;
     l_c[qt] = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) o_c[qt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 #pragma unroll
-  for (int qt = 0; qt < QT; ++qt)
+  for (int t = 0; t < TPW; ++t) {
+    if (t >= n_live) break;
+    f32x4 sacc[QT];
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
+    for (int qt = 0; qt < QT; ++qt) sacc[qt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int i = 0; i < 4; ++i) o_c[qt][dt][i] = 0.f;
-
-  if (live) {
-    // ---- S^T = K Q^T ----
-    f32x4 sacc[4][QT];
+    for (int ds = 0; ds < DS; ++ds)
 #pragma unroll
-    for (int pt = 0; pt < 4; ++pt) {
-#pragma unroll
-      for (int qt = 0; qt < QT; ++qt) sacc[pt][qt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ds = 0; ds < DS; ++ds)
-#pragma unroll
-        for (int qt = 0; qt < QT; ++qt) ET<T>::mma(sacc[pt][qt], kf[pt][ds], qf[qt][ds]);
-    }
-    // ---- mask + chunk softmax (base 2) ----
-    float p[QT][4][4];
+      for (int qt = 0; qt < QT; ++qt) ET<T>::mma(sacc[qt], kf[t][ds], qf[qt][ds]);
+    typename PV<T>::B pf[QT];
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
-      float mx = NEG_INF;
+      float s[4], mx = NEG_INF;
 #pragma unroll
-      for (int pt = 0; pt < 4; ++pt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int pos = P0 + 32 * (pt >> 1) + 8 * kg + i + 4 * (pt & 1);
-          const float s = (pos <= qpos[qt]) ? sacc[pt][qt][i] : NEG_INF;
-          p[qt][pt][i] = s;
-          mx = fmaxf(mx, s);
-        }
+      for (int i = 0; i < 4; ++i) {
+        const int pos = P0 + 16 * t + 4 * kg + i;
+        s[i] = (pos <= qpos[qt]) ? sacc[qt][i] : NEG_INF;
+        mx = fmaxf(mx, s[i]);
+      }
       mx = fmaxf(mx, __shfl_xor(mx, 16));
       mx = fmaxf(mx, __shfl_xor(mx, 32));
-      float sum = 0.f;
+      const float m_n = fmaxf(m_c[qt], mx);
+      // m_n = -inf: nothing visible so far; the running state stays the identity
+      const float alpha = (m_c[qt] == NEG_INF) ? 0.f : exp2f(m_c[qt] - m_n);
+      float p[4], sum = 0.f;
 #pragma unroll
-      for (int pt = 0; pt < 4; ++pt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float e = (mx == NEG_INF) ? 0.f : exp2f(p[qt][pt][i] - mx);
-          p[qt][pt][i] = e;
-          sum += e;
-        }
+      for (int i = 0; i < 4; ++i) {
+        p[i] = (m_n == NEG_INF) ? 0.f : exp2f(s[i] - m_n);
+        sum += p[i];
+      }
       sum += __shfl_xor(sum, 16);
       sum += __shfl_xor(sum, 32);
-      m_c[qt] = mx;
-      l_c[qt] = sum;
+      l_c[qt] = l_c[qt] * alpha + sum;
+      m_c[qt] = m_n;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o_c[qt][dt][i] *= alpha;
+      pf[qt] = PV<T>::split(p);
     }
-    // ---- O^T = V^T P^T ----
-    typename ET<T>::B pf[QT][2];
-#pragma unroll
-    for (int qt = 0; qt < QT; ++qt)
-#pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        float x[8];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          x[j] = p[qt][2 * s][j];
-          x[j + 4] = p[qt][2 * s + 1][j];
-        }
-        pf[qt][s] = ET<T>::split(x);
-      }
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-      for (int qt = 0; qt < QT; ++qt) {
-        f32x4 oacc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int s = 0; s < 2; ++s) ET<T>::mma(oacc, vf[s][dt], pf[qt][s]);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) o_c[qt][dt][i] = oacc[i];
-      }
+      for (int qt = 0; qt < QT; ++qt) PV<T>::mma(o_c[qt][dt], vf[t][dt], pf[qt]);
   }
 
-  // ---- merge the group's 4 chunks left to right: every wave parks its chunk partial in LDS,
-  // then thread e merges query vector e / (HD/4), columns 4*(e mod HD/4).., chunk 0 first ----
+  // ---- merge the group's 4 runs left to right: every wave parks its run partial in LDS (lane
+  // (qv, kg) holds dims dt*16 + 4kg..+3), then thread e merges query vector e / (HD/4),
+  // columns 4*(e mod HD/4).., run 0 first ----
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
     const int qv = qt * 16 + tl;
@@ -243,81 +245,17 @@ __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
       const int rl = qv / a.G, gq = qv - rl * a.G;
       *reinterpret_cast<float4*>(a.out + (size_t)(mrow0 + rl) * qstride + (h * a.G + gq) * HD + d) =
           make_float4(o_r[0] / l_r, o_r[1] / l_r, o_r[2] / l_r, o_r[3] / l_r);
-    } else if (a.fused_combine) {
-      // agent-coherent stores (written through to the level every XCD reads from): the merge of
-      // groups runs in this launch
-      float* pp = part + (size_t)qv * PS;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) store_coherent(pp + d + i, o_r[i]);
-      if (d == 0) {
-        store_coherent(pp + HD, m_r);
-        store_coherent(pp + HD + 1, l_r);
-      }
     } else {
-      // plain stores: k_attn_combine reads them after this launch has ended
       float* pp = part + (size_t)qv * PS;
       *reinterpret_cast<float4*>(pp + d) = make_float4(o_r[0], o_r[1], o_r[2], o_r[3]);
       if (d == 0) *reinterpret_cast<float2*>(pp + HD) = make_float2(m_r, l_r);
     }
   }
-  if (n_groups == 1 || !a.fused_combine) return;
-
-  // ---- fused combine: the last group of (b, h, rb) to finish merges all group partials ----
-  // Every wave waits for its coherent stores to complete before the barrier; then one relaxed
-  // agent-scope count per workgroup (no L2 write-back or invalidate is needed: the partials
-  // travel through coherent stores and loads).
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  int* cnt = a.cnt + (b * a.n_kv + h) * a.n_rb + rb;
-  if (threadIdx.x == 0)
-    s_last = __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == n_groups - 1;
-  __syncthreads();
-  if (!s_last) return;
-  const float* part0 = a.part + ((((size_t)(b * a.n_kv + h) * a.n_rb + rb) * a.n_groups_max) * 32) * PS;
-  for (int e = threadIdx.x; e < nqv * (HD / 4); e += blockDim.x)
-    merge_groups<HD, true>(a, part0, e, n_groups, mrow0, h);
-  if (threadIdx.x == 0) __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Merge the group partials of query vector e / (HD/4), columns 4*(e mod HD/4).., left to right
-// (online softmax merge from the identity, fixed order) and write the normalised output. Each
-// batch of 8 groups is loaded at once; COHERENT reads them with agent-coherent loads (the fused
-// combine inside k_attention reads partials other workgroups wrote during the same launch).
-template <int HD, bool COHERENT>
-__device__ void merge_groups(const AttnArgs& a, const float* part0, int e, int n_groups, int mrow0, int h) {
-  constexpr int PS = HD + 4, HD4 = HD / 4;
-  const int qv = e / HD4, d = (e - qv * HD4) * 4;
-  const float* pq = part0 + (size_t)qv * PS;
-  float m_r = NEG_INF, l_r = 0.f, o_r[4] = {0.f, 0.f, 0.f, 0.f};
-  for (int g0 = 0; g0 < n_groups; g0 += 8) {
-    float mg[8], lg[8], og[8][4];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const float* pp = pq + (size_t)min(g0 + u, n_groups - 1) * 32 * PS;
-      if (COHERENT) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) og[u][i] = load_coherent(pp + d + i);
-        mg[u] = load_coherent(pp + HD);
-        lg[u] = load_coherent(pp + HD + 1);
-      } else {
-        const float4 v = *reinterpret_cast<const float4*>(pp + d);
-        const float2 ml = *reinterpret_cast<const float2*>(pp + HD);
-        og[u][0] = v.x; og[u][1] = v.y; og[u][2] = v.z; og[u][3] = v.w;
-        mg[u] = ml.x;
-        lg[u] = ml.y;
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < 8; ++u)
-      if (g0 + u < n_groups) softmax_merge(m_r, l_r, o_r, mg[u], lg[u], og[u], 4);
-  }
-  const int rl = qv / a.G, gq = qv - rl * a.G;
-  *reinterpret_cast<float4*>(a.out + (size_t)(mrow0 + rl) * a.n_heads * HD + (h * a.G + gq) * HD + d) =
-      make_float4(o_r[0] / l_r, o_r[1] / l_r, o_r[2] / l_r, o_r[3] / l_r);
-}
-
-// Separate merge of the group partials (contexts that can span many groups): thread e of the
-// grid's x extent owns one (query vector, 4 columns).
+// Merge of the group partials: an 8-lane team per (query vector, 4 columns). Lane j merges groups
+// j, j+8, .. left to right from the identity (4 groups' loads in flight at a time), then the team
+// merges pairwise with a fixed butterfly; both lanes of a pair compute merge(lower, upper).
 template <int HD>
 __global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
   constexpr int PS = HD + 4, HD4 = HD / 4;
@@ -328,32 +266,80 @@ __global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
   const int nr = min(a.RB, a.R - r0);
   const int nqv = nr * a.G;
   const int mrow0 = b * a.R + r0;
-  const int e = blockIdx.x * blockDim.x + threadIdx.x;
-  if (e >= nqv * HD4) return;
-  const int n_groups = a.row_pos[mrow0 + nr - 1] / ATT_GROUP + 1;
+  const int gid = blockIdx.x * blockDim.x + threadIdx.x;
+  const int item = gid / CMB_LANES, j = gid % CMB_LANES;
+  const int qv = item / HD4, d = (item - qv * HD4) * 4;
+  if (qv >= nqv) return;   // the 8 lanes of an item leave together
+  const int n_groups = a.row_pos[mrow0 + nr - 1] / a.span + 1;
   if (n_groups == 1) return;   // k_attention wrote the final output
-  const float* part0 = a.part + ((((size_t)(b * a.n_kv + h) * a.n_rb + rb) * a.n_groups_max) * 32) * PS;
-  merge_groups<HD, false>(a, part0, e, n_groups, mrow0, h);
+  const float* pq = a.part + ((((size_t)(b * a.n_kv + h) * a.n_rb + rb) * a.n_groups_max) * 32 + qv) * PS;
+  float m_r = NEG_INF, l_r = 0.f, o_r[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int g0 = j; g0 < n_groups; g0 += 4 * CMB_LANES) {
+    float4 ov[4];
+    float2 ml[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float* pp = pq + (size_t)min(g0 + u * CMB_LANES, n_groups - 1) * 32 * PS;
+      ov[u] = *reinterpret_cast<const float4*>(pp + d);
+      ml[u] = *reinterpret_cast<const float2*>(pp + HD);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (g0 + u * CMB_LANES < n_groups) {
+        const float oc[4] = {ov[u].x, ov[u].y, ov[u].z, ov[u].w};
+        softmax_merge(m_r, l_r, o_r, ml[u].x, ml[u].y, oc, 4);
+      }
+    }
+  }
+#pragma unroll
+  for (int s = 1; s < CMB_LANES; s <<= 1) {
+    const float pm = __shfl_xor(m_r, s), pl = __shfl_xor(l_r, s);
+    float po[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) po[i] = __shfl_xor(o_r[i], s);
+    const bool upper = j & s;
+    float am = upper ? pm : m_r, al = upper ? pl : l_r, ao[4], bo[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      ao[i] = upper ? po[i] : o_r[i];
+      bo[i] = upper ? o_r[i] : po[i];
+    }
+    softmax_merge(am, al, ao, upper ? m_r : pm, upper ? l_r : pl, bo, 4);
+    m_r = am;
+    l_r = al;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) o_r[i] = ao[i];
+  }
+  if (j == 0) {
+    const int rl = qv / a.G, gq = qv - rl * a.G;
+    *reinterpret_cast<float4*>(a.out + (size_t)(mrow0 + rl) * a.n_heads * HD + (h * a.G + gq) * HD + d) =
+        make_float4(o_r[0] / l_r, o_r[1] / l_r, o_r[2] / l_r, o_r[3] / l_r);
+  }
+}
+
+template <typename Kern>
+static void launch_kernel(Kern k, dim3 grid, hipStream_t s, const LaunchEvents* ev, const AttnArgs& a) {
+  if (ev) hipExtLaunchKernelGGL(k, grid, dim3(256), 0, s, ev->start, ev->stop, 0, a);
+  else hipLaunchKernelGGL(k, grid, dim3(256), 0, s, a);
+}
+
+template <typename T, int HD, int QT>
+static void launch_attention_qt(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev) {
+  const dim3 grid(a.n_groups_max, a.n_kv * a.n_rb, a.B);
+  switch (a.span) {
+    case 64: launch_kernel(k_attention<T, HD, QT, 1>, grid, s, ev, a); break;
+    case 128: launch_kernel(k_attention<T, HD, QT, 2>, grid, s, ev, a); break;
+    default: launch_kernel(k_attention<T, HD, QT, 4>, grid, s, ev, a); break;
+  }
 }
 
 template <typename T, int HD>
 static void launch_attention_hd(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev) {
-  const dim3 grid(a.n_groups_max, a.n_kv * a.n_rb, a.B);
-  if (std::min(a.RB, a.R) * a.G > 16) {
-    if (ev) hipExtLaunchKernelGGL((k_attention<T, HD, 2>), grid, dim3(256), 0, s, ev->start, ev->stop, 0, a);
-    else hipLaunchKernelGGL((k_attention<T, HD, 2>), grid, dim3(256), 0, s, a);
-  } else {
-    if (ev) hipExtLaunchKernelGGL((k_attention<T, HD, 1>), grid, dim3(256), 0, s, ev->start, ev->stop, 0, a);
-    else hipLaunchKernelGGL((k_attention<T, HD, 1>), grid, dim3(256), 0, s, a);
-  }
+  if (std::min(a.RB, a.R) * a.G > 16) launch_attention_qt<T, HD, 2>(a, s, ev);
+  else launch_attention_qt<T, HD, 1>(a, s, ev);
 }
 
-template <int HD>
-static void launch_attn_combine_hd(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev) {
-  const dim3 cgrid((32 * HD / 4 + 255) / 256, a.n_kv * a.n_rb, a.B);
-  if (ev) hipExtLaunchKernelGGL((k_attn_combine<HD>), cgrid, dim3(256), 0, s, ev->start, ev->stop, 0, a);
-  else hipLaunchKernelGGL((k_attn_combine<HD>), cgrid, dim3(256), 0, s, a);
-}
+int attention_span(int max_ctx) { return max_ctx <= 4096 ? 64 : (max_ctx <= 8192 ? 128 : 256); }
 
 template <typename T>
 void launch_attention(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev) {
@@ -361,11 +347,13 @@ void launch_attention(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev) 
   else launch_attention_hd<T, 64>(a, s, ev);
 }
 
-bool attention_needs_combine(const AttnArgs& a) { return a.n_groups_max > 1 && !a.fused_combine; }
+bool attention_needs_combine(const AttnArgs& a) { return a.n_groups_max > 1; }
 
 void launch_attn_combine(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev) {
-  if (a.head_dim == 128) launch_attn_combine_hd<128>(a, s, ev);
-  else launch_attn_combine_hd<64>(a, s, ev);
+  const int items = 32 * (a.head_dim / 4) * CMB_LANES;
+  const dim3 grid((items + 255) / 256, a.n_kv * a.n_rb, a.B);
+  if (a.head_dim == 128) launch_kernel(k_attn_combine<128>, grid, s, ev, a);
+  else launch_kernel(k_attn_combine<64>, grid, s, ev, a);
 }
 
 template void launch_attention<uint16_t>(const AttnArgs&, hipStream_t, const LaunchEvents*);

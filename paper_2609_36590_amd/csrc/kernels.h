@@ -73,12 +73,10 @@ struct AttnArgs {
   int B, R;               // sequences, rows per sequence
   int n_heads, n_kv, head_dim, G;  // G = n_heads / n_kv
   int RB, n_rb;           // rows per row-block (G*RB <= 32), row-blocks per sequence
-  int n_groups_max;       // grid extent over groups of 256 positions
+  int span;               // positions per workgroup group: 64, 128 or 256 (attention_span)
+  int n_groups_max;       // grid extent over groups; n_groups_max * span == bt_stride * 16
   float scale_log2;       // log2(e) / sqrt(head_dim)
   float* part;            // group partials [B][n_kv][n_rb][n_groups_max][32][head_dim + 4]
-  int fused_combine;      // 1: the last group's workgroup merges the partials (k_attention);
-                          // 0: k_attn_combine merges them
-  int* cnt;               // fused combine: finished-group counters [B][n_kv][n_rb] (zero between launches)
   float* out;             // [M][n_heads*head_dim]
 };
 
@@ -138,7 +136,7 @@ struct DevState {
 
 // Kernel choice for a linear launch: weights streamed with the activation rows staged in LDS as
 // MFMA fragments (M <= 16 and the rows fit), else the activation fragments come from global memory.
-enum LinearKind { LIN_LDS = 0, LIN_GLOBAL = 1, LIN_VALU = 2 };
+enum LinearKind { LIN_LDS = 0, LIN_GLOBAL = 1 };
 
 // Optional timing events stamped by the launches themselves (hipExtLaunchKernel): `start` at the
 // start of the first kernel of the operation, `stop` at the end of its last kernel.
@@ -149,12 +147,14 @@ struct LaunchEvents {
 template <typename T>
 void launch_linear(const LinArgs& a, int prologue, int epilogue, int kind, hipStream_t s,
                    const LaunchEvents* ev = nullptr);
-// Attention partials per group of 256 positions (the final output when the rows see one group).
+// Attention partials per group of span positions (the final output when the rows see one group).
 template <typename T>
 void launch_attention(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev = nullptr);
-// Merge of the group partials as a kernel of its own; needed when the context can span more
-// than one group and the merge is not fused into k_attention.
+// Merge of the group partials; needed when the context capacity spans more than one group.
 bool attention_needs_combine(const AttnArgs& a);
+// Positions per attention group for a context capacity (fixed per decoder, so that a query's
+// merge tree depends only on absolute positions).
+int attention_span(int max_ctx);
 void launch_attn_combine(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev = nullptr);
 template <typename T>
 void launch_setup(const SetupArgs& a, hipStream_t s);

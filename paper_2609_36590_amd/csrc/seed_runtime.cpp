@@ -39,7 +39,6 @@ seed_status fail(seed_status s, const std::string& msg) {
 
 constexpr int PREFILL_ROWS = 48;   // rows per prefill pass (3 MFMA token tiles)
 constexpr int MAX_ROWS = 64;       // rows per decode pass: max_batch * (max_draft + 1)
-constexpr int GROUP = 256;         // attention workgroup span (positions): 4 chunks of 64
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 int cdiv(int a, int b) { return (a + b - 1) / b; }
@@ -48,14 +47,14 @@ struct Plan {
   seed_config cfg;
   int esize = 2;
   int H, NQ, NKV, HD, F, V, L, LD, QD, KVD, G;
-  int RB, n_rb_max, max_rows, bt_stride, blocks_per_seq, n_blocks, n_groups_max;
+  int RB, n_rb_max, max_rows, bt_stride, blocks_per_seq, n_blocks, span, n_groups_max;
   int dstride, tstride, log_cap;
   // weight arena
   size_t w_embed, w_final_norm, w_rope_cos, w_rope_sin, w_total;
   std::vector<size_t> w_attn_norm, w_mlp_norm, w_qkv, w_o, w_gu, w_down;
   size_t kv_total;
   // workspace
-  size_t o_h, o_xg, o_ssq, o_q, o_attn, o_act, o_part, o_cnt, o_row_seq, o_row_pos, o_row_blk, o_row_rope, o_amax_val,
+  size_t o_h, o_xg, o_ssq, o_q, o_attn, o_act, o_part, o_row_seq, o_row_pos, o_row_blk, o_row_rope, o_amax_val,
       o_amax_idx, o_vtok;
   size_t o_t, o_len, o_limit, o_active, o_nacc, o_bonus, o_rounds, o_counters, o_drafts, o_tokens,
       o_trace, o_log, o_bt, o_scratch, ws_total;
@@ -96,10 +95,11 @@ Plan make_plan(const seed_config& c) {
   p.n_rb_max = cdiv(std::max(c.max_draft + 1, PREFILL_ROWS), p.RB);
   p.max_rows = std::max(PREFILL_ROWS, c.max_batch * (c.max_draft + 1));
   p.blocks_per_seq = cdiv(c.max_ctx, 16);
-  p.bt_stride = cdiv(p.blocks_per_seq, GROUP / 16) * (GROUP / 16);   // whole groups, padded with block 0
+  p.span = seedk::attention_span(c.max_ctx);
+  p.bt_stride = cdiv(p.blocks_per_seq, p.span / 16) * (p.span / 16);   // whole groups, padded with block 0
   p.n_blocks = c.max_batch * p.blocks_per_seq + 1;                  // block 0 = permanent zero block
 
-  p.n_groups_max = p.bt_stride * 16 / GROUP;
+  p.n_groups_max = p.bt_stride * 16 / p.span;
   p.dstride = c.max_draft + 1;
   p.tstride = c.max_ctx;
   p.log_cap = c.max_ctx;
@@ -132,7 +132,6 @@ Plan make_plan(const seed_config& c) {
   p.o_attn = take(R * p.QD * 4);
   p.o_act = take(R * p.F * 4);
   p.o_part = take(B * p.NKV * p.n_rb_max * (size_t)p.n_groups_max * 32 * (p.HD + 4) * 4);
-  p.o_cnt = take(B * p.NKV * p.n_rb_max * 4);
   p.o_row_seq = take(R * 4);
   p.o_row_pos = take(R * 4);
   p.o_row_blk = take(R * 4);
@@ -362,13 +361,8 @@ void run_layers(seed_ctx* c, int M, int B, int R, int l0, int l1, int phase,
     at.B = B; at.R = R;
     at.n_heads = p.NQ; at.n_kv = p.NKV; at.head_dim = p.HD; at.G = p.G;
     at.RB = p.RB; at.n_rb = cdiv(R, p.RB);
+    at.span = p.span;
     at.n_groups_max = p.n_groups_max;
-    // When the merge is one pass of the workgroup (a row-block of at most 256/(head_dim/4)
-    // query vectors, e.g. draft rows) and the context spans at most 8 groups, the last group's
-    // workgroup merges the partials; otherwise the separate combine kernel does (same merge
-    // order, so both give identical results).
-    at.fused_combine = p.n_groups_max <= 8 && std::min(p.RB, R) * p.G * (p.HD / 4) <= 256;
-    at.cnt = c->ws<int>(p.o_cnt);
     at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)p.HD));
     at.part = c->ws<float>(p.o_part);
     at.out = c->ws<float>(p.o_attn);
