@@ -59,7 +59,12 @@ def kernel_bytes(cfg, op, M, L):
     return 0
 
 
-def combine_bytes(cfg, M, L, group=256):
+def attention_span(max_ctx):
+    """Positions per attention group for a context capacity (the runtime's rule)."""
+    return 64 if max_ctx <= 4096 else (128 if max_ctx <= 8192 else 256)
+
+
+def combine_bytes(cfg, M, L, group):
     """Group partials read (o, m, l per query vector and group) + output written."""
     groups = (L + group - 1) // group
     return groups * M * cfg.n_heads * (cfg.head_dim + 2) * 4 + M * cfg.q_dim * 4
@@ -229,6 +234,79 @@ def config_sweep(torch, out_md):
 
 
 # ------------------------------------------------------------------------------------------
+# decoder size sweep (Fig. 6 / Table 4): draft-step cost vs the number of decoder layers
+# ------------------------------------------------------------------------------------------
+SPLITS = (1, 2, 4, 6, 8, 10, 12, 14)
+
+
+def split_sweep(torch, out_md):
+    base = synth.CONFIGS["28L-h2048"]
+    k, gen = base.k, base.gen_len
+    log(f"[split] weights for {base.name} (the same tensors serve every split)")
+    weights = synth.make_weights(base)
+    prompt = synth.make_prompts(base)[0]
+    Lm = len(prompt) + gen // 2
+    rows = []
+    t0 = time.perf_counter()
+    for n in SPLITS:
+        cfg = base.replace(name=f"{base.name}-dec{n}", n_dec_layers=n)
+        log(f"[split] n_dec={n}")
+        dec = binding.Decoder(cfg, max_batch=1, max_ctx=len(prompt) + gen + 2 * 7 + 2, max_draft=k)
+        dec.load_weights(weights)
+        out0, _, st0 = dec.generate([prompt], 0, gen, use_graph=True)
+        out, cnt, st = dec.generate([prompt], k, gen, use_graph=True)
+        dec.prefill([prompt])
+        t_ver, t_dr = step_latency(dec, k, torch)
+        db = step_bytes(cfg, 1, Lm, n)
+        vb = step_bytes(cfg, k + 1, Lm, cfg.n_layers)
+        r = {"n_dec": n, "draft_step_ms": round(t_dr, 4), "verify_ms": round(t_ver, 4),
+             "draft_gbps": round(db / (t_dr * 1e-3) / 1e9, 1), "draft_frac": round(db / (t_dr * 1e-3) / PEAK_HBM, 4),
+             "draft_over_verify": round(t_dr / t_ver, 4),
+             # the byte model of the cost appendix: a draft step reads n decoder layers + the head,
+             # a verification the whole model
+             "byte_model_ratio": round(db / vb, 4),
+             "greedy_tokens_per_s": round(gen / (st0["decode_ms"] * 1e-3), 2),
+             "measured": {"tokens_per_s": round(int(cnt.sum()) / (st["decode_ms"] * 1e-3), 2),
+                          "mean_accept": round(st["accepted"] / max(1, st["rounds"]), 4),
+                          "output_equals_greedy": bool(np.array_equal(out, out0))}}
+        forced = {}
+        for a in (0, k):
+            o, c, sa = dec.generate([prompt], k, gen, sim_accept=a, forced_trace=out0, use_graph=True)
+            forced[str(a)] = {"tokens_per_s": round(int(c.sum()) / (sa["decode_ms"] * 1e-3), 2),
+                              "model_tokens_per_s": round((a + 1) / ((k * t_dr + t_ver) * 1e-3), 2),
+                              "output_equals_greedy": bool(np.array_equal(o, out0))}
+        r["forced_acceptance"] = forced
+        log(f"[split] {json.dumps(r)}")
+        rows.append(r)
+        dec.close()
+        torch.cuda.empty_cache()
+    lines = ["# Draft-step cost vs decoder size (one MI355X)", "",
+             f"Command: `python3 bench.py --split-sweep {out_md}` (repository root, library built by",
+             "`__graft_entry__.build()`). Model: " + base.name + f" (28 layers, hidden 2048), k={k}, "
+             f"{len(prompt)}-token prompt, {gen} generated tokens; the split n_dec = l - l' only changes",
+             "which layers the drafter runs (same random-init weights, seed 0). Step latencies are HIP-event",
+             "medians; bytes are algorithmic (weights + KV at the mean context). `byte model` = draft-step",
+             "bytes / verification bytes (the cost appendix's c_draft in bytes), against the measured",
+             "latency ratio. `forced a` = drafts overridden after the draft kernels ran so that exactly a",
+             "are accepted per round (model = (a+1)/(k t_draft + t_verify)).", "",
+             "| n_dec | draft step ms (TB/s, frac) | t_draft / t_verify | byte model | verify ms | "
+             "forced a=0 tok/s (model) | forced a=k tok/s (model) | spec == greedy |",
+             "|---|---|---|---|---|---|---|---|"]
+    for r in rows:
+        f0, fk = r["forced_acceptance"]["0"], r["forced_acceptance"][str(k)]
+        ok = r["measured"]["output_equals_greedy"] and f0["output_equals_greedy"] and fk["output_equals_greedy"]
+        lines.append(f"| {r['n_dec']} | {r['draft_step_ms']:.3f} ({r['draft_gbps'] / 1e3:.2f}, "
+                     f"{r['draft_frac']:.2f}) | {r['draft_over_verify']:.3f} | {r['byte_model_ratio']:.3f} | "
+                     f"{r['verify_ms']:.3f} | {f0['tokens_per_s']:.0f} ({f0['model_tokens_per_s']:.0f}) | "
+                     f"{fk['tokens_per_s']:.0f} ({fk['model_tokens_per_s']:.0f}) | {ok} |")
+    lines += ["", "Raw results:", "", "```json"] + [json.dumps(r) for r in rows] + ["```"]
+    with open(out_md, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    log(f"[split] done in {time.perf_counter() - t0:.1f}s")
+    print(json.dumps({"split_sweep": out_md, "splits": len(rows)}), flush=True)
+
+
+# ------------------------------------------------------------------------------------------
 # CPU oracle baseline
 # ------------------------------------------------------------------------------------------
 def cpu_baseline(cfg, weights, prompt, k, rounds):
@@ -272,6 +350,9 @@ def main():
     ap.add_argument("--config-sweep", metavar="OUT_MD",
                     help="measure every workload (tiny, 28L, 4B k=2/4/6, 4B batch 8, 4B 16k) at the "
                          "measured and forced acceptance lengths and write a summary to OUT_MD")
+    ap.add_argument("--split-sweep", metavar="OUT_MD",
+                    help="draft-step cost of the 28-layer model for n_dec in 1..14 decoder layers "
+                         "(measured and forced acceptance); write a summary to OUT_MD")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
@@ -284,6 +365,9 @@ def main():
         return
     if args.config_sweep:
         config_sweep(torch, args.config_sweep)
+        return
+    if args.split_sweep:
+        split_sweep(torch, args.split_sweep)
         return
 
     cfg = synth.CONFIGS[args.config]
@@ -360,7 +444,8 @@ def main():
         L_here = len(dec.tokens(0)) - probe_rounds // 2
         name = ("verify_" if phase == binding.PHASE_VERIFY else "draft_") + names[op]
         avg = ms / n
-        b = combine_bytes(cfg, M, L_here) if op == binding.OP_COMBINE else kernel_bytes(cfg, op, M, L_here)
+        b = (combine_bytes(cfg, M, L_here, attention_span(max_ctx)) if op == binding.OP_COMBINE
+             else kernel_bytes(cfg, op, M, L_here))
         per_kernel[name] = {"launches_per_round": n / probe_rounds, "avg_us": avg * 1e3,
                             "us_per_round": avg * 1e3 * n / probe_rounds,
                             "alg_bytes": b, "gbps": (b / (avg * 1e-3) / 1e9) if b else None}
