@@ -1,5 +1,6 @@
-"""Algorithm 2 (SEED inference with fixed draft length), brute-force greedy decoding, and the
-parallel block-mask drafter pass, in plain NumPy.
+"""Algorithm 2 (SEED inference with fixed draft length), brute-force greedy decoding, the
+parallel block-mask drafter pass, and the forward pass of the speculative drafting objective
+(Algorithm 1, L_spec), in plain NumPy.
 
 TEST INFRASTRUCTURE (see ``oracle/__init__.py``): never imported by the HIP path.
 
@@ -187,3 +188,35 @@ def block_draft_logits(model, context, draft_inputs):
     for i in range(model.first_decoder_layer, c.n_layers):
         h, _, _ = model.block(i, h, pos, Ks[i], Vs[i])
     return model.head(h)
+
+
+def spec_forward(model, tokens, b):
+    """Forward pass of the speculative drafting objective L_spec of Algorithm 1.
+
+    For every input position q = 0..n-2 (the drafter predicts X[q+1]) the block start is
+    s = floor(q / b) * b (0-based form of Algorithm 1's n'). The decoder layers run over the raw
+    embeddings H^0 of X[s..q] (causal inside the block) and attend to the deep decoder keys /
+    values KV^dec of positions < s, which come from one full pass of f over the whole sequence.
+    Written as Algorithm 1's loop over blocks, one block at a time; the GPU computes all blocks
+    in one pass with the block-causal mask of Fig. 2 (right).
+
+    Returns (logits [n-1, V], L_spec = sum over q of -log softmax(logits[q])[X[q+1]]).
+    """
+    c = model.cfg
+    tokens = [int(x) for x in tokens]
+    n = len(tokens)
+    assert n >= 2 and b >= 1
+    _, Ks, Vs = full_forward(model, tokens, return_kv=True)
+    logits = np.zeros((n - 1, c.vocab), dtype=model.dtype)
+    for s in range(0, n - 1, b):
+        e = min(s + b, n - 1)                      # inputs X[s..e-1] predict X[s+1..e]
+        h = model.embed(tokens[s:e])
+        pos = np.arange(s, e)
+        for i in range(model.first_decoder_layer, c.n_layers):
+            h, _, _ = model.block(i, h, pos, Ks[i][:s], Vs[i][:s])
+        logits[s:e] = model.head(h)
+    z = logits.astype(np.float64)
+    zmax = z.max(axis=1, keepdims=True)
+    lse = zmax[:, 0] + np.log(np.exp(z - zmax).sum(axis=1))
+    nll = lse - z[np.arange(n - 1), np.asarray(tokens[1:], dtype=np.int64)]
+    return logits, float(nll.sum())

@@ -160,3 +160,70 @@ def test_fp32_oracle_tracks_fp64_on_tiny_config():
     l32 = om.full_forward(om.Model(cfg, w, np.float32), prompt)
     l64 = om.full_forward(om.Model(cfg, w, np.float64), prompt)
     assert np.abs(l32 - l64).max() < 1e-5
+
+
+# ---- forward pass of the speculative drafting objective (Algorithm 1) ----
+
+def _spec_case(n_dec, n=13, seed=4):
+    m = _model(SMALL, n_dec=n_dec, seed=seed)
+    return m, _prompt(SMALL, n, seed=seed + 1)
+
+
+def test_spec_forward_block_one_is_first_draft_step_everywhere():
+    """b = 1: row q sees the deep cache of X[0..q-1] and only its own raw embedding, i.e. the
+    first drafting step after a prefill of X[0..q] (cached path of Algorithm 2)."""
+    m, x = _spec_case(2)
+    logits, _ = os_.spec_forward(m, x, 1)
+    for q in range(len(x) - 1):
+        st = os_.prefill(m, x[:q + 1], 32)
+        _, ql = os_.draft(st, 1)
+        np.testing.assert_allclose(logits[q], ql[0], rtol=1e-9, atol=1e-11)
+
+
+def test_spec_forward_single_block_is_the_decoder_alone():
+    """b >= n: no deep context at all; the decoder layers act as a causal LM over H^0."""
+    m, x = _spec_case(2)
+    logits, _ = os_.spec_forward(m, x, 64)
+    sub_cfg = SMALL.replace(n_layers=2, n_dec_layers=2)
+    L0 = SMALL.n_layers - 2
+    w = {}
+    for k, v in m.w.items():
+        if k.startswith("layers."):
+            i = int(k.split(".")[1])
+            if i >= L0:
+                w[f"layers.{i - L0}." + k.split(".", 2)[2]] = v
+        else:
+            w[k] = v
+    sub = om.Model(sub_cfg, w, np.float64)
+    ref = om.full_forward(sub, x[:-1])
+    np.testing.assert_allclose(logits, ref, rtol=1e-9, atol=1e-11)
+
+
+@pytest.mark.parametrize("b", [1, 3, 5])
+def test_spec_forward_without_encoder_is_the_full_model(b):
+    """n_dec = l: the drafter is the whole model, so every block reproduces causal f."""
+    m, x = _spec_case(SMALL.n_layers)
+    logits, _ = os_.spec_forward(m, x, b)
+    np.testing.assert_allclose(logits, om.full_forward(m, x)[:-1], rtol=1e-9, atol=1e-11)
+
+
+@pytest.mark.parametrize("b", [2, 4])
+def test_spec_forward_blocks_are_independent_drafts(b):
+    """Each block equals the block-mask drafter pass from the committed prefix X[0..s] with the
+    block's tokens as teacher-forced draft inputs."""
+    m, x = _spec_case(2, n=12)
+    logits, _ = os_.spec_forward(m, x, b)
+    for s in range(0, len(x) - 1, b):
+        e = min(s + b, len(x) - 1)
+        ref = os_.block_draft_logits(m, x[:s + 1], x[s + 1:e])
+        np.testing.assert_allclose(logits[s:e], ref, rtol=1e-9, atol=1e-11)
+
+
+def test_spec_loss_is_the_summed_negative_log_likelihood():
+    m, x = _spec_case(2)
+    logits, loss = os_.spec_forward(m, x, 3)
+    z = logits.astype(np.float64)
+    p = np.exp(z - z.max(axis=1, keepdims=True))
+    p /= p.sum(axis=1, keepdims=True)
+    ref = -sum(np.log(p[q, x[q + 1]]) for q in range(len(x) - 1))
+    assert abs(loss - ref) <= 1e-9 * abs(ref)
