@@ -307,6 +307,76 @@ def split_sweep(torch, out_md):
 
 
 # ------------------------------------------------------------------------------------------
+# forward pass of the speculative drafting objective (Algorithm 1) on the 4B model
+# ------------------------------------------------------------------------------------------
+SPEC_ROWS = 48   # rows per pass of the GPU path (its prefill chunk)
+
+
+def spec_sweep(torch, out_md, reps=5):
+    cfg = synth.C3_4B
+    n = cfg.prompt_len
+    log(f"[spec] weights for {cfg.name}")
+    weights = synth.make_weights(cfg)
+    x = synth.make_prompts(cfg)[0]
+    dec = binding.Decoder(cfg, max_batch=1, max_ctx=n + 8, max_draft=4)
+    dec.load_weights(weights)
+    es = 2
+    dec_layer = sum(kernel_bytes(cfg, op, 0, 0) for op in (binding.OP_QKV, binding.OP_O, binding.OP_GATEUP,
+                                                           binding.OP_DOWN))
+    head = cfg.vocab * cfg.hidden * es
+    passes = (n - 1 + SPEC_ROWS - 1) // SPEC_ROWS
+    # weights are streamed once per pass of 48 rows; keys/values: each row reads the deep cache
+    # below its block start and the pass's own cache of its block (decoder layers)
+    kv_row = 2 * cfg.kv_dim * es
+    rows = []
+    for b in (4, 16):
+        # prefill alone, then prefill + the drafter pass: the difference is the pass itself
+        tp, ts = [], []
+        for _ in range(reps):
+            t0 = time.perf_counter()
+            dec.prefill([x])
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            _, _, loss = dec.spec_forward(x, b, logits=False)
+            t2 = time.perf_counter()
+            tp.append(t1 - t0)
+            ts.append(t2 - t1)
+        t_pf, t_all = statistics.median(tp), statistics.median(ts)
+        t_spec = t_all - t_pf
+        kv_bytes = sum((q // b * b + (q - q // b * b + 1)) for q in range(n - 1)) * kv_row * cfg.n_dec_layers
+        wbytes = passes * (cfg.n_dec_layers * dec_layer + head)
+        flops = 2 * (n - 1) * (cfg.n_dec_layers * dec_layer / es + head / es)
+        r = {"block": b, "n": n, "rows": n - 1, "passes": passes, "prefill_ms": round(t_pf * 1e3, 3),
+             "spec_ms": round(t_spec * 1e3, 3), "rows_per_s": round((n - 1) / t_spec, 1),
+             "alg_bytes": int(wbytes + kv_bytes), "gbps": round((wbytes + kv_bytes) / t_spec / 1e9, 1),
+             "frac_hbm": round((wbytes + kv_bytes) / t_spec / PEAK_HBM, 4),
+             "tflops": round(flops / t_spec / 1e12, 2), "L_spec": round(loss, 4)}
+        log(f"[spec] {json.dumps(r)}")
+        rows.append(r)
+    dec.close()
+    lines = ["# Forward pass of the speculative drafting objective (one MI355X)", "",
+             f"Command: `python3 bench.py --spec-forward {out_md}` (repository root, library built by",
+             "`__graft_entry__.build()`). Model " + cfg.name + f", one {n}-token sequence of uniform-random",
+             "tokens (seed 1), random-init weights (seed 0). `seed_spec_forward` runs the full model over",
+             "the sequence (prefill) and then the decoder layers over the raw embeddings of every block",
+             "at once with the block-causal mask; the pass time is the median of prefill + pass minus the",
+             f"median of the prefill alone ({reps} repetitions, host clock around synchronous calls). The",
+             f"GPU path takes {SPEC_ROWS} rows per pass, so the two decoder layers and the LM head are",
+             "streamed once per pass: algorithmic bytes = passes x (decoder layers + head) + the keys and",
+             "values each row reads; FLOPs = 2 x rows x (decoder + head parameters).", "",
+             "| block | rows | passes | pass ms | rows/s | HBM GB/s (frac of 8 TB/s) | TFLOP/s | prefill ms | L_spec |",
+             "|---|---|---|---|---|---|---|---|---|"]
+    for r in rows:
+        lines.append(f"| {r['block']} | {r['rows']} | {r['passes']} | {r['spec_ms']:.3f} | {r['rows_per_s']:.0f} | "
+                     f"{r['gbps']:.0f} ({r['frac_hbm']:.2f}) | {r['tflops']:.1f} | {r['prefill_ms']:.2f} | "
+                     f"{r['L_spec']:.2f} |")
+    lines += ["", "Raw results:", "", "```json"] + [json.dumps(r) for r in rows] + ["```"]
+    with open(out_md, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print(json.dumps({"spec_forward": out_md, "blocks": [r["block"] for r in rows]}), flush=True)
+
+
+# ------------------------------------------------------------------------------------------
 # CPU oracle baseline
 # ------------------------------------------------------------------------------------------
 def cpu_baseline(cfg, weights, prompt, k, rounds):
@@ -353,6 +423,9 @@ def main():
     ap.add_argument("--split-sweep", metavar="OUT_MD",
                     help="draft-step cost of the 28-layer model for n_dec in 1..14 decoder layers "
                          "(measured and forced acceptance); write a summary to OUT_MD")
+    ap.add_argument("--spec-forward", metavar="OUT_MD",
+                    help="time the forward pass of the speculative drafting objective (4B model, "
+                         "1024 tokens, block sizes 4 and 16) and write a summary to OUT_MD")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
@@ -368,6 +441,9 @@ def main():
         return
     if args.split_sweep:
         split_sweep(torch, args.split_sweep)
+        return
+    if args.spec_forward:
+        spec_sweep(torch, args.spec_forward)
         return
 
     cfg = synth.CONFIGS[args.config]

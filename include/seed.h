@@ -129,7 +129,7 @@ typedef struct seed_stats {
  * kernel, SEED_OP_COMBINE the merge of its group partials (launched when the context capacity
  * spans more than one attention group of 64, 128 or 256 positions). */
 enum {
-  SEED_PHASE_VERIFY = 0, SEED_PHASE_DRAFT = 1, SEED_PHASE_PREFILL = 2,
+  SEED_PHASE_VERIFY = 0, SEED_PHASE_DRAFT = 1, SEED_PHASE_PREFILL = 2, SEED_PHASE_SPEC = 3,
   SEED_OP_SETUP = 0, SEED_OP_QKV = 1, SEED_OP_ATTN = 2, SEED_OP_COMBINE = 3, SEED_OP_O = 4,
   SEED_OP_GATEUP = 5, SEED_OP_DOWN = 6, SEED_OP_HEAD = 7, SEED_OP_ACCEPT = 8,
   SEED_OP_HEAD_ARGMAX = 9
@@ -208,6 +208,26 @@ seed_status seed_rounds(seed_ctx* ctx, int32_t k, int32_t n_rounds, int32_t use_
 seed_status seed_generate(seed_ctx* ctx, int32_t B, const int32_t* tokens, const int32_t* lens,
                           const seed_gen_opts* opts, int32_t* out, int32_t* counts,
                           seed_stats* stats);
+
+/*
+ * Forward pass of the speculative drafting objective L_spec (Algorithm 1, Sec. 3.2, Fig. 2 right)
+ * on one sequence X[0..n-1] with training block size `block`: the full model runs over the
+ * sequence (as seed_prefill, which this call replaces: afterwards the decode state is that of
+ * seed_prefill(ctx, 1, tokens, &n)), then the decoder layers run once, in parallel for every
+ * block, over the raw embeddings H^0 of X[0..n-2]: the row of position q (block start
+ * s = floor(q / block) * block) attends causally to the rows s..q of its own block and to the
+ * deep decoder keys/values of positions < s, and predicts X[q+1]. Forward only.
+ * shallow_kv: device, at least seed_spec_kv_bytes bytes, 256-byte aligned, caller-owned: the
+ *             decoder layers' keys/values of this pass (its contents are scratch).
+ * logits: device [(n-1) * vocab], the drafter's logits of every row (required).
+ * row_nll: nullable device [n-1]: -log softmax(logits[q])[X[q+1]].
+ * loss: nullable host: L_spec = the sum of row_nll (accumulated in double on the host).
+ * Errors: SEED_ERR_ARG if n < 2, block < 1, a token is out of range or a required pointer is
+ * NULL; SEED_ERR_CAPACITY if n + 1 > max_ctx.
+ */
+seed_status seed_spec_kv_bytes(const seed_config* cfg, size_t* bytes);
+seed_status seed_spec_forward(seed_ctx* ctx, int32_t n, const int32_t* tokens, int32_t block,
+                              void* shallow_kv, float* logits, float* row_nll, double* loss);
 
 /* Committed tokens of sequence b (prompt included): out host [cap]; *len receives t_b. */
 seed_status seed_get_tokens(seed_ctx* ctx, int32_t b, int32_t* out, int32_t cap, int32_t* len);

@@ -56,7 +56,8 @@ class SeedStats(ctypes.Structure):
 
 EXPORTS = ("seed_arena_bytes", "seed_create", "seed_load_weights", "seed_prefill", "seed_draft",
            "seed_verify", "seed_rounds", "seed_generate", "seed_get_tokens", "seed_kernel_timing",
-           "seed_kernel_timing_read", "seed_last_error", "seed_destroy")
+           "seed_kernel_timing_read", "seed_last_error", "seed_destroy", "seed_spec_kv_bytes",
+           "seed_spec_forward")
 
 _LIB = None
 _P = ctypes.c_void_p
@@ -94,6 +95,8 @@ def load_library(path: str | None = None):
         "seed_get_tokens": [_P, ctypes.c_int32, _I32P, ctypes.c_int32, _I32P],
         "seed_kernel_timing": [_P, ctypes.c_int32, ctypes.c_int32],
         "seed_kernel_timing_read": [_P, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_double)],
+        "seed_spec_kv_bytes": [ctypes.POINTER(SeedConfig), ctypes.POINTER(ctypes.c_size_t)],
+        "seed_spec_forward": [_P, ctypes.c_int32, _I32P, ctypes.c_int32, _P, _P, _P, ctypes.POINTER(ctypes.c_double)],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -228,6 +231,21 @@ def seed_kernel_timing_read(ctx: int):
     return n.value, ms.value
 
 
+def seed_spec_kv_bytes(cfg: SeedConfig) -> int:
+    n = ctypes.c_size_t()
+    _check(load_library().seed_spec_kv_bytes(ctypes.byref(cfg), ctypes.byref(n)), "seed_spec_kv_bytes")
+    return n.value
+
+
+def seed_spec_forward(ctx: int, tokens, block: int, shallow_kv: int, logits: int, row_nll: int | None = None,
+                      want_loss: bool = True):
+    t, tp = _i32(tokens)
+    loss = ctypes.c_double()
+    _check(load_library().seed_spec_forward(ctx, len(t), tp, block, shallow_kv, logits, row_nll,
+                                            ctypes.byref(loss) if want_loss else None), "seed_spec_forward")
+    return loss.value if want_loss else None
+
+
 def seed_destroy(ctx: int):
     load_library().seed_destroy(ctx)
 
@@ -293,6 +311,20 @@ class Decoder:
 
     def tokens(self, b: int):
         return seed_get_tokens(self.ctx, b, self.cfg.max_ctx)
+
+    def spec_forward(self, tokens, block: int, logits: bool = True):
+        """Forward pass of the speculative drafting objective on one sequence: (drafter logits
+        [n-1, vocab] or None, per-row negative log-likelihoods [n-1], L_spec)."""
+        torch = self.torch
+        n = len(tokens)
+        if getattr(self, "_skv", None) is None:
+            self._skv = torch.empty(seed_spec_kv_bytes(self.cfg), dtype=torch.uint8, device=self.weights.device)
+        lg = self._logits(max(n - 1, 1))
+        nll = torch.empty(max(n - 1, 1), dtype=torch.float32, device=self.weights.device)
+        loss = seed_spec_forward(self.ctx, tokens, block, self._skv.data_ptr(), lg.data_ptr(), nll.data_ptr())
+        self.B = 1
+        self.stream.synchronize()
+        return (self._host(lg, (n - 1,)) if logits else None), nll.cpu().numpy()[:n - 1], loss
 
     def _logits(self, rows):
         return self.torch.empty(rows * self.cfg.vocab, dtype=self.torch.float32, device=self.weights.device)

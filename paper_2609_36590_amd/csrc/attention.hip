@@ -12,6 +12,12 @@
 // tiles. The 4 waves' partials are merged left to right in LDS and written as the group partial
 // (o, m, l), or as the final output when the pass sees a single group.
 //
+// The block-causal variant (SPEC) computes the drafter pass of the speculative drafting objective
+// (Algorithm 1, Fig. 2 right): row q attends to the deep cache at positions below its block start
+// s and to the pass's own keys/values (a second, position-indexed cache) at s..q. Tiles that
+// hold positions of both kinds for some row are contracted with both caches and selected per
+// (query, position).
+//
 // k_attn_combine merges the group partials of each query vector with a fixed tree: lane j of an
 // 8-lane team merges groups j, j+8, j+16, ... left to right, then the 8 results are merged
 // pairwise (0+1, 2+3, ..; then 01+23, ..). A tile, run or group with no visible position is an
@@ -70,7 +76,7 @@ struct PV<float> {
   }
 };
 
-template <typename T, int HD, int QT, int TPW>
+template <typename T, int HD, int QT, int TPW, bool SPEC>
 __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
   constexpr int DS = HD / 32;    // 32-dim steps of S^T
   constexpr int DT = HD / 16;    // 16-dim tiles of O^T
@@ -97,13 +103,16 @@ __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
 
   // ---- round trip 1: the last row's position, the run's block-table entries, the queries ----
   const int maxpos = a.row_pos[mrow0 + nr - 1];
+  // block-causal pass: the first and last rows' block starts bound which tiles need which cache
+  const int s_first = SPEC ? (a.row_pos[mrow0] / a.s_block) * a.s_block : 0;
+  const int s_last = SPEC ? (maxpos / a.s_block) * a.s_block : 0;
   int blk[TPW];
 #pragma unroll
   for (int t = 0; t < TPW; ++t) blk[t] = btp[(P0 >> 4) + t];
   // queries (lane column qv = qt*16 + tl, k-slots d = ds*32 + kg*8 + j) and their positions:
   // loaded branch-free from a valid row, masked when converted
   float qraw[QT][DS][8];
-  int qpos[QT];
+  int qpos[QT], qstart[QT];
   bool qok[QT];
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
@@ -125,15 +134,36 @@ __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
   // 4kg..4kg+3][d = dt*16 + tl] (the cache keeps V transposed per block)
   typename ET<T>::A kf[TPW][DS];
   typename PV<T>::A vf[TPW][DT];
+  // block-causal pass: the pass's own keys/values of the same tiles, and which caches each tile
+  // needs (deep: some row's block starts after the tile's first position; shallow: some row's
+  // block starts at or before its last position)
+  typename ET<T>::A kfs[SPEC ? TPW : 1][DS];
+  typename PV<T>::A vfs[SPEC ? TPW : 1][DT];
+  bool need_deep[TPW], need_sh[TPW];
 #pragma unroll
   for (int t = 0; t < TPW; ++t) {
-    if (t < n_live) {
+    const int T0 = P0 + 16 * t;
+    need_deep[t] = !SPEC || T0 < s_last;
+    need_sh[t] = SPEC && T0 + 15 >= s_first;
+    if (t < n_live && need_deep[t]) {
       const T* kp = kvp + (((layer_base + blk[t]) * 2 + 0) * a.n_kv + h) * 16 * HD + tl * HD + kg * 8;
 #pragma unroll
       for (int ds = 0; ds < DS; ++ds) kf[t][ds] = ET<T>::load(kp + ds * 32);
       const T* vp = kvp + (((layer_base + blk[t]) * 2 + 1) * a.n_kv + h) * HD * 16 + tl * 16 + 4 * kg;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) vf[t][dt] = PV<T>::load(vp + dt * 16 * 16);
+    }
+    if constexpr (SPEC) {
+      if (t < n_live && need_sh[t]) {
+        const T* sp = reinterpret_cast<const T*>(a.skv);
+        const size_t sb = (size_t)a.s_layer * a.s_n_blocks + (T0 >> 4);
+        const T* kp = sp + ((sb * 2 + 0) * a.n_kv + h) * 16 * HD + tl * HD + kg * 8;
+#pragma unroll
+        for (int ds = 0; ds < DS; ++ds) kfs[t][ds] = ET<T>::load(kp + ds * 32);
+        const T* vp = sp + ((sb * 2 + 1) * a.n_kv + h) * HD * 16 + tl * 16 + 4 * kg;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) vfs[t][dt] = PV<T>::load(vp + dt * 16 * 16);
+      }
     }
   }
   // keep every K/V load here, ahead of all arithmetic: left to itself the scheduler trades them
@@ -145,6 +175,8 @@ __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
     if (!qok[qt]) qpos[qt] = -1;
+    // block-causal pass: positions below qstart come from the deep cache
+    qstart[qt] = SPEC ? (qpos[qt] / a.s_block) * a.s_block : 0;
 #pragma unroll
     for (int ds = 0; ds < DS; ++ds) {
       float x[8];
@@ -167,21 +199,35 @@ __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
 #pragma unroll
   for (int t = 0; t < TPW; ++t) {
     if (t >= n_live) break;
-    f32x4 sacc[QT];
+    f32x4 sacc[QT], ssh[QT];
 #pragma unroll
-    for (int qt = 0; qt < QT; ++qt) sacc[qt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int qt = 0; qt < QT; ++qt) {
+      sacc[qt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      ssh[qt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    if (need_deep[t]) {
 #pragma unroll
-    for (int ds = 0; ds < DS; ++ds)
+      for (int ds = 0; ds < DS; ++ds)
 #pragma unroll
-      for (int qt = 0; qt < QT; ++qt) ET<T>::mma(sacc[qt], kf[t][ds], qf[qt][ds]);
-    typename PV<T>::B pf[QT];
+        for (int qt = 0; qt < QT; ++qt) ET<T>::mma(sacc[qt], kf[t][ds], qf[qt][ds]);
+    }
+    if constexpr (SPEC) {
+      if (need_sh[t]) {
+#pragma unroll
+        for (int ds = 0; ds < DS; ++ds)
+#pragma unroll
+          for (int qt = 0; qt < QT; ++qt) ET<T>::mma(ssh[qt], kfs[t][ds], qf[qt][ds]);
+      }
+    }
+    typename PV<T>::B pf[QT], pfs[QT];
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
       float s[4], mx = NEG_INF;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int pos = P0 + 16 * t + 4 * kg + i;
-        s[i] = (pos <= qpos[qt]) ? sacc[qt][i] : NEG_INF;
+        if constexpr (SPEC) s[i] = (pos > qpos[qt]) ? NEG_INF : (pos < qstart[qt] ? sacc[qt][i] : ssh[qt][i]);
+        else s[i] = (pos <= qpos[qt]) ? sacc[qt][i] : NEG_INF;
         mx = fmaxf(mx, s[i]);
       }
       mx = fmaxf(mx, __shfl_xor(mx, 16));
@@ -203,12 +249,34 @@ __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
       for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) o_c[qt][dt][i] *= alpha;
-      pf[qt] = PV<T>::split(p);
+      if constexpr (SPEC) {
+        float pd[4], ps[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const bool deep = P0 + 16 * t + 4 * kg + i < qstart[qt];
+          pd[i] = deep ? p[i] : 0.f;
+          ps[i] = deep ? 0.f : p[i];
+        }
+        pf[qt] = PV<T>::split(pd);
+        pfs[qt] = PV<T>::split(ps);
+      } else {
+        pf[qt] = PV<T>::split(p);
+      }
     }
+    if (need_deep[t]) {
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
+      for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-      for (int qt = 0; qt < QT; ++qt) PV<T>::mma(o_c[qt][dt], vf[t][dt], pf[qt]);
+        for (int qt = 0; qt < QT; ++qt) PV<T>::mma(o_c[qt][dt], vf[t][dt], pf[qt]);
+    }
+    if constexpr (SPEC) {
+      if (need_sh[t]) {
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+          for (int qt = 0; qt < QT; ++qt) PV<T>::mma(o_c[qt][dt], vfs[t][dt], pfs[qt]);
+      }
+    }
   }
 
   // ---- merge the group's 4 runs left to right: every wave parks its run partial in LDS (lane
@@ -323,20 +391,26 @@ static void launch_kernel(Kern k, dim3 grid, hipStream_t s, const LaunchEvents* 
   else hipLaunchKernelGGL(k, grid, dim3(256), 0, s, a);
 }
 
-template <typename T, int HD, int QT>
+template <typename T, int HD, int QT, bool SPEC>
 static void launch_attention_qt(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev) {
   const dim3 grid(a.n_groups_max, a.n_kv * a.n_rb, a.B);
   switch (a.span) {
-    case 64: launch_kernel(k_attention<T, HD, QT, 1>, grid, s, ev, a); break;
-    case 128: launch_kernel(k_attention<T, HD, QT, 2>, grid, s, ev, a); break;
-    default: launch_kernel(k_attention<T, HD, QT, 4>, grid, s, ev, a); break;
+    case 64: launch_kernel(k_attention<T, HD, QT, 1, SPEC>, grid, s, ev, a); break;
+    case 128: launch_kernel(k_attention<T, HD, QT, 2, SPEC>, grid, s, ev, a); break;
+    default: launch_kernel(k_attention<T, HD, QT, 4, SPEC>, grid, s, ev, a); break;
   }
 }
 
 template <typename T, int HD>
 static void launch_attention_hd(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev) {
-  if (std::min(a.RB, a.R) * a.G > 16) launch_attention_qt<T, HD, 2>(a, s, ev);
-  else launch_attention_qt<T, HD, 1>(a, s, ev);
+  const bool q2 = std::min(a.RB, a.R) * a.G > 16;
+  if (a.s_block > 0) {
+    if (q2) launch_attention_qt<T, HD, 2, true>(a, s, ev);
+    else launch_attention_qt<T, HD, 1, true>(a, s, ev);
+  } else {
+    if (q2) launch_attention_qt<T, HD, 2, false>(a, s, ev);
+    else launch_attention_qt<T, HD, 1, false>(a, s, ev);
+  }
 }
 
 int attention_span(int max_ctx) { return max_ctx <= 4096 ? 64 : (max_ctx <= 8192 ? 128 : 256); }

@@ -73,6 +73,11 @@ struct AttnArgs {
   int B, R;               // sequences, rows per sequence
   int n_heads, n_kv, head_dim, G;  // G = n_heads / n_kv
   int RB, n_rb;           // rows per row-block (G*RB <= 32), row-blocks per sequence
+  // block-causal pass of the speculative drafting objective (s_block > 0): row q (position q)
+  // attends to the deep cache (kv, bt) at positions < s = floor(q / s_block) * s_block and to
+  // the shallow cache skv (this pass's keys/values, block id = position / 16) at s..q
+  const void* skv;
+  int s_layer, s_n_blocks, s_block;
   int span;               // positions per workgroup group: 64, 128 or 256 (attention_span)
   int n_groups_max;       // grid extent over groups; n_groups_max * span == bt_stride * 16
   float scale_log2;       // log2(e) / sqrt(head_dim)
@@ -81,7 +86,7 @@ struct AttnArgs {
 };
 
 // Per-pass row setup + embedding gather.
-enum SetupMode { SETUP_PREFILL = 0, SETUP_DRAFT = 1, SETUP_VERIFY = 2 };
+enum SetupMode { SETUP_PREFILL = 0, SETUP_DRAFT = 1, SETUP_VERIFY = 2, SETUP_SPEC = 3 };
 
 struct SetupArgs {
   int mode;
@@ -92,7 +97,7 @@ struct SetupArgs {
   int step;               // SETUP_DRAFT: draft step i (>= 1)
   const int* tokens;      // committed tokens [B][tstride]
   int tstride;
-  int pf_seq, pf_pos0;    // SETUP_PREFILL
+  int pf_seq, pf_pos0;    // SETUP_PREFILL, SETUP_SPEC (rows at positions pf_pos0..)
   int sim_accept;         // SETUP_VERIFY: -1 or forced acceptance length
   const int* trace;       // [B][tstride] greedy trace by absolute position
   int vocab;
@@ -159,6 +164,8 @@ void launch_attn_combine(const AttnArgs& a, hipStream_t s, const LaunchEvents* e
 template <typename T>
 void launch_setup(const SetupArgs& a, hipStream_t s);
 void launch_accept(const DevState& st, int B, int k, hipStream_t s);
+// nll[r] = logsumexp(logits[r]) - logits[r][target[r]] for r < rows (row stride V)
+void launch_row_nll(const float* logits, int rows, int V, const int* target, float* nll, hipStream_t s);
 // Reduce the head's per-workgroup argmax partials of M rows; row m's token goes to
 // tok_out[m * tok_stride] (lowest token id among equal maxima).
 void launch_argmax_finalize(const float* val, const int* idx, int stride, int n_parts, int M, int* tok_out,

@@ -5,7 +5,8 @@ namespace seedk {
 
 // ---------------------------------------------------------------------------------------------
 // Row setup for a pass: pick each row's sequence, position and token (Algorithm 2: drafts feed
-// X_draft[i-1], verification feeds X_draft[0..d]), gather the raw embedding H^0 = W_in x from
+// X_draft[i-1], verification feeds X_draft[0..d]; prefill and the drafting objective's pass of
+// Algorithm 1 feed the sequence itself), gather the raw embedding H^0 = W_in x from
 // the packed table into the fp32 residual stream, and write its per-16-feature sums of squares.
 // ---------------------------------------------------------------------------------------------
 template <typename T>
@@ -14,7 +15,7 @@ __global__ void __launch_bounds__(256) k_setup(SetupArgs a) {
   __shared__ int s_tok, s_pos, s_seq;
   if (threadIdx.x == 0) {
     int b, pos, tok;
-    if (a.mode == SETUP_PREFILL) {
+    if (a.mode == SETUP_PREFILL || a.mode == SETUP_SPEC) {
       b = a.pf_seq;
       pos = a.pf_pos0 + m;
       tok = a.tokens[b * a.tstride + pos];
@@ -44,7 +45,9 @@ __global__ void __launch_bounds__(256) k_setup(SetupArgs a) {
   {
     // the row's KV block and RoPE angles, read once per pass by every layer's QKV epilogue
     const int pos = s_pos, half = a.head_dim >> 1;
-    if (threadIdx.x == 0) a.row_blk[m] = a.bt[s_seq * a.bt_stride + (pos >> 4)];
+    // the block-causal drafter pass writes its keys/values to a cache of its own, indexed by
+    // position (block id = position / 16)
+    if (threadIdx.x == 0) a.row_blk[m] = a.mode == SETUP_SPEC ? (pos >> 4) : a.bt[s_seq * a.bt_stride + (pos >> 4)];
     for (int i = threadIdx.x; i < half; i += blockDim.x) {
       a.row_rope[(size_t)m * a.head_dim + i] = a.rope_cos[(size_t)pos * half + i];
       a.row_rope[(size_t)m * a.head_dim + half + i] = a.rope_sin[(size_t)pos * half + i];
@@ -115,6 +118,32 @@ __global__ void __launch_bounds__(64) k_accept(DevState st, int B, int k) {
 }
 
 // ---------------------------------------------------------------------------------------------
+// Negative log-likelihood of each row's target under the softmax of its logits (the per-position
+// term of L_spec, Algorithm 1): one workgroup per row; max, then the sum of exponentials, both
+// reduced with a fixed tree.
+// ---------------------------------------------------------------------------------------------
+__global__ void __launch_bounds__(256) k_row_nll(const float* logits, int V, const int* target, float* nll) {
+  const int r = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const float* z = logits + (size_t)r * V;
+  __shared__ float s_red[4];
+  float mx = NEG_INF;
+  for (int j = tid; j < V; j += blockDim.x) mx = fmaxf(mx, z[j]);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
+  if (lane == 0) s_red[wave] = mx;
+  __syncthreads();
+  mx = fmaxf(fmaxf(s_red[0], s_red[1]), fmaxf(s_red[2], s_red[3]));
+  __syncthreads();
+  float sum = 0.f;
+  for (int j = tid; j < V; j += blockDim.x) sum += __expf(z[j] - mx);
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o);
+  if (lane == 0) s_red[wave] = sum;
+  __syncthreads();
+  if (tid == 0) nll[r] = mx + logf((s_red[0] + s_red[1]) + (s_red[2] + s_red[3])) - z[target[r]];
+}
+
+// ---------------------------------------------------------------------------------------------
 // Load-time helpers.
 // ---------------------------------------------------------------------------------------------
 template <typename T>
@@ -152,6 +181,10 @@ void launch_setup(const SetupArgs& a, hipStream_t s) {
 
 void launch_accept(const DevState& st, int B, int k, hipStream_t s) {
   hipLaunchKernelGGL(k_accept, dim3(1), dim3(64), 0, s, st, B, k);
+}
+
+void launch_row_nll(const float* logits, int rows, int V, const int* target, float* nll, hipStream_t s) {
+  if (rows > 0) hipLaunchKernelGGL(k_row_nll, dim3(rows), dim3(256), 0, s, logits, V, target, nll);
 }
 
 template <typename T>

@@ -57,7 +57,7 @@ struct Plan {
   size_t o_h, o_xg, o_ssq, o_q, o_attn, o_act, o_part, o_row_seq, o_row_pos, o_row_blk, o_row_rope, o_amax_val,
       o_amax_idx, o_vtok;
   size_t o_t, o_len, o_limit, o_active, o_nacc, o_bonus, o_rounds, o_counters, o_drafts, o_tokens,
-      o_trace, o_log, o_bt, o_scratch, ws_total;
+      o_trace, o_log, o_bt, o_nll, o_scratch, ws_total;
 };
 
 seed_status validate(const seed_config* c) {
@@ -152,6 +152,7 @@ Plan make_plan(const seed_config& c) {
   p.o_trace = take(B * (size_t)p.tstride * 4);
   p.o_log = take((size_t)p.log_cap * B * 4);
   p.o_bt = take(B * (size_t)p.bt_stride * 4);
+  p.o_nll = take((size_t)c.max_ctx * 4);
   p.o_scratch = take((size_t)std::max({p.V, p.QD + 2 * p.KVD, 2 * p.F, p.H}) * 4);
   p.ws_total = o;
   return p;
@@ -335,15 +336,28 @@ void linear(seed_ctx* c, LinArgs a, int pro, int epi, int phase, int op, bool ca
   timed(c, phase, op, cap, [&](const LaunchEvents* ev) { launch_linear<T>(a, pro, epi, kind, c->s, ev); });
 }
 
+// The block-causal decoder pass of the speculative drafting objective: its keys/values go to a
+// cache of their own (decoder layers only, indexed by position), the deep cache is only read.
+struct SpecPass {
+  void* kv;
+  int n_blocks;   // blocks per layer of kv
+  int block;      // block size b of the objective
+};
+
 // Layers [l0, l1) over M rows (B sequences x R rows each, consecutive positions per sequence).
 template <typename T>
 void run_layers(seed_ctx* c, int M, int B, int R, int l0, int l1, int phase,
-                const int* bt_override, bool cap) {
+                const int* bt_override, bool cap, const SpecPass* spec = nullptr) {
   const Plan& p = c->p;
   float* h = c->ws<float>(p.o_h);
   for (int li = l0; li < l1; ++li) {
     LinArgs a = lin_base(c, M);
     a.layer = li;
+    if (spec) {
+      a.kv = spec->kv;
+      a.layer = li - p.LD;
+      a.n_blocks = spec->n_blocks;
+    }
     // QKV + RoPE + KV write
     a.W = c->W + p.w_qkv[li]; a.N = p.QD + 2 * p.KVD; a.K = p.H;
     a.X = c->ws<float>(p.o_xg); a.ldx = p.H;
@@ -363,6 +377,12 @@ void run_layers(seed_ctx* c, int M, int B, int R, int l0, int l1, int phase,
     at.RB = p.RB; at.n_rb = cdiv(R, p.RB);
     at.span = p.span;
     at.n_groups_max = p.n_groups_max;
+    if (spec) {
+      at.skv = spec->kv;
+      at.s_layer = li - p.LD;
+      at.s_n_blocks = spec->n_blocks;
+      at.s_block = spec->block;
+    }
     at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)p.HD));
     at.part = c->ws<float>(p.o_part);
     at.out = c->ws<float>(p.o_attn);
@@ -678,6 +698,30 @@ seed_status do_prefill(seed_ctx* c, const std::vector<int>& tokens_packed) {
       run_layers<T>(c, M, 1, M, 0, p.L, SEED_PHASE_PREFILL,
                     c->ws<int>(p.o_bt) + (size_t)b * p.bt_stride, false);
     }
+  }
+  HIPCHK(hipGetLastError());
+  return SEED_OK;
+}
+
+// Bytes of the block-causal pass's own cache: the decoder layers' keys/values by position.
+size_t spec_kv_bytes(const Plan& p) {
+  return align256((size_t)std::max(1, p.L - p.LD) * p.blocks_per_seq * 2 * p.NKV * 16 * p.HD * p.esize);
+}
+
+// Decoder rows of the speculative drafting objective (Algorithm 1) over positions 0..n-2, in
+// passes of PREFILL_ROWS rows; the deep cache holds the prefill of the same sequence.
+template <typename T>
+seed_status do_spec(seed_ctx* c, int n, int block, void* skv, float* logits) {
+  const Plan& p = c->p;
+  const SpecPass sp{skv, p.blocks_per_seq, block};
+  const int rows = n - 1;
+  for (int s0 = 0; s0 < rows; s0 += PREFILL_ROWS) {
+    const int M = std::min(PREFILL_ROWS, rows - s0);
+    SetupArgs s = setup_base(c, p.LD);
+    s.mode = SETUP_SPEC; s.M = M; s.R = M; s.pf_seq = 0; s.pf_pos0 = s0;
+    timed(c, SEED_PHASE_SPEC, SEED_OP_SETUP, false, [&](const LaunchEvents*) { launch_setup<T>(s, c->s); });
+    run_layers<T>(c, M, 1, M, p.LD, p.L, SEED_PHASE_SPEC, c->ws<int>(p.o_bt), false, &sp);
+    run_head<T>(c, M, c->ws<int>(p.o_vtok), 1, logits + (size_t)s0 * p.V, (long long)p.V, SEED_PHASE_SPEC, false);
   }
   HIPCHK(hipGetLastError());
   return SEED_OK;
@@ -1047,6 +1091,52 @@ seed_status seed_generate(seed_ctx* c, int32_t B, const int32_t* tokens, const i
   hipEventDestroy(e2);
   c->sim_accept = -1;
   c->drafts_k = -1;
+  return SEED_OK;
+}
+
+seed_status seed_spec_kv_bytes(const seed_config* cfg, size_t* bytes) {
+  seed_status st = validate(cfg);
+  if (st != SEED_OK) return st;
+  if (!bytes) return fail(SEED_ERR_ARG, "bytes must not be NULL");
+  *bytes = spec_kv_bytes(make_plan(*cfg));
+  return SEED_OK;
+}
+
+seed_status seed_spec_forward(seed_ctx* c, int32_t n, const int32_t* tokens, int32_t block, void* shallow_kv,
+                              float* logits, float* row_nll, double* loss) {
+  seed_status st = check_ready(c);
+  if (st != SEED_OK) return st;
+  if (n < 2) return fail(SEED_ERR_ARG, "the sequence needs at least two tokens");
+  if (block < 1) return fail(SEED_ERR_ARG, "block must be >= 1");
+  if (!shallow_kv || !logits) return fail(SEED_ERR_ARG, "shallow_kv and logits must not be NULL");
+  if ((uintptr_t)shallow_kv & 255) return fail(SEED_ERR_ARG, "shallow_kv must be 256-byte aligned");
+  std::vector<int> packed;
+  st = check_prompts(c, 1, tokens, &n, 1, packed);
+  if (st != SEED_OK) return st;
+  st = start_sequences(c, 1, &n, 1);
+  if (st != SEED_OK) return st;
+  c->sim_accept = -1;
+  c->eos = -1;
+  const bool bf = c->p.cfg.dtype == SEED_BF16;
+  st = bf ? do_prefill<uint16_t>(c, packed) : do_prefill<float>(c, packed);
+  if (st != SEED_OK) return st;
+  c->prefilled = true;
+  st = bf ? do_spec<uint16_t>(c, n, block, shallow_kv, logits) : do_spec<float>(c, n, block, shallow_kv, logits);
+  if (st != SEED_OK) return st;
+  if (row_nll || loss) {
+    float* nll = row_nll ? row_nll : c->ws<float>(c->p.o_nll);
+    launch_row_nll(logits, n - 1, c->p.V, c->ws<int>(c->p.o_tokens) + 1, nll, c->s);
+    HIPCHK(hipGetLastError());
+    if (loss) {
+      std::vector<float> h(n - 1);
+      HIPCHK(hipMemcpyAsync(h.data(), nll, (size_t)(n - 1) * 4, hipMemcpyDeviceToHost, c->s));
+      HIPCHK(hipStreamSynchronize(c->s));
+      double sum = 0.0;
+      for (float v : h) sum += v;
+      *loss = sum;
+    }
+  }
+  HIPCHK(hipStreamSynchronize(c->s));
   return SEED_OK;
 }
 

@@ -84,3 +84,11 @@ def test_null_arguments(lib):
     assert lib.seed_verify(None, 1, None, None, None, None) == -1
     assert lib.seed_generate(None, 1, None, None, None, None, None, None) == -1
     lib.seed_destroy(None)
+
+
+def test_spec_cache_bytes_cover_the_decoder_layers(lib):
+    c = binding.make_config(synth.C3_4B, 1, 1545, 4)
+    n = binding.seed_spec_kv_bytes(c)
+    # 2 decoder layers x 2 (K, V) x 8 heads x 128 dims x 2 bytes per position
+    assert n >= 2 * 2 * 8 * 128 * 2 * 1545
+    assert n < 1.1 * 2 * 2 * 8 * 128 * 2 * (1545 + 16)

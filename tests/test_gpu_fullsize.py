@@ -145,3 +145,23 @@ def test_long_context_16k_spec_equals_greedy(weights_4b):
         spec_equals_greedy(dec, [prompt])
     finally:
         dec.close()
+
+
+@pytest.mark.timeout(900)
+def test_spec_forward_28l_matches_oracle():
+    """Forward pass of the speculative drafting objective (Algorithm 1) on the 28-layer model, a
+    512-token sequence, block size 4: every row's drafter logits within 2e-2 of the oracle."""
+    cfg = synth.C2_28L
+    w = synth.make_weights(cfg, seed=0)
+    x = synth.make_prompts(cfg)[0]
+    dec = decoder(cfg, w, max_batch=1, max_ctx=len(x) + 8, max_draft=K)
+    try:
+        lg, nll, loss = dec.spec_forward(x, 4)
+    finally:
+        dec.close()
+    say(f"[gpu] oracle spec forward {cfg.name} over {len(x)} tokens")
+    ref, ref_loss = os_.spec_forward(oracle_model(cfg, w), x, 4)
+    err = float(np.abs(lg - ref).max())
+    say(f"[gpu] max |logits - oracle| = {err:.3g}; L_spec {loss:.6g} vs {ref_loss:.6g}")
+    assert err <= TOL
+    assert abs(loss - ref_loss) <= 2 * TOL * (len(x) - 1)
