@@ -60,6 +60,8 @@ struct LinArgs {
   float* amax_val;        // per-workgroup argmax partials [M][amax_stride]
   int* amax_idx;
   int amax_stride;
+  float* part;            // LIN_SPLITK: k-range partials [KS][M][N]
+  float* part_rs;         // LIN_SPLITK with the RMSNorm prologue: row scales [M]
 };
 
 // Arguments of the split-KV paged attention kernel and its combine kernel.
@@ -141,7 +143,7 @@ struct DevState {
 
 // Kernel choice for a linear launch: weights streamed with the activation rows staged in LDS as
 // MFMA fragments (M <= 16 and the rows fit), else the activation fragments come from global memory.
-enum LinearKind { LIN_LDS = 0, LIN_GLOBAL = 1 };
+enum LinearKind { LIN_LDS = 0, LIN_GLOBAL = 1, LIN_SPLITK = 2 };
 
 // Optional timing events stamped by the launches themselves (hipExtLaunchKernel): `start` at the
 // start of the first kernel of the operation, `stop` at the end of its last kernel.

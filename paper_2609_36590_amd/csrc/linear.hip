@@ -14,6 +14,8 @@
 // row, as plain greedy decoding (d = 0). (k_linear_lds supports S == 1 only.)
 #include "device_common.h"
 
+#include <algorithm>
+
 namespace seedk {
 
 // n-group of pass j of this workgroup: g0 + j * gs
@@ -454,6 +456,156 @@ __global__ void __launch_bounds__(1024) k_linear_mfma(LinArgs a) {
   linear_epilogue<T, EPI>(a, gr, s_red, a.KS * per, epre);
 }
 
+// ---------------------------------------------------------------------------------------------
+// Wide passes (16 < M <= 64 rows: batched verification, prefill, the drafting objective's pass):
+// the K split runs across workgroups. Workgroup (n-group g, k-range ks) stages the activation
+// columns of its k-range only (they fit LDS where the whole K of M rows does not) and its NT
+// waves stream one n-tile each over that range, exactly as wave (nl, ks) of the narrow kernels
+// does (same tiles, same order, same B slots), for TT token tiles of 16 rows. The range partials
+// go to global memory; k_splitk_reduce adds them in k-range order from 0 and runs the epilogue,
+// so every row gets the bit-identical output of the narrow kernels.
+// ---------------------------------------------------------------------------------------------
+template <typename T, int TT, int XI, int PRO>
+__global__ void __launch_bounds__(512) k_linear_splitk(LinArgs a, float* part) {
+  extern __shared__ __attribute__((aligned(16))) char lds[];
+  constexpr int P = 8;
+  const int tid = threadIdx.x, lane = tid & 63, nl = tid >> 6;
+  const int KT = a.K >> 5, n_tiles = a.N >> 4, M = a.M;
+  const int tl = lane & 15, kg = lane >> 4;
+  const int ks = blockIdx.y;
+  const int kt0 = (ks * KT) / a.KS, nk = ((ks + 1) * KT) / a.KS - kt0;
+  const int nt = blockIdx.x * a.NT + nl;
+  const bool live = nt < n_tiles;
+  const T* w0 = reinterpret_cast<const T*>(a.W) + ((size_t)(live ? nt : 0) * KT + kt0) * 512 + lane * 8;
+
+  // ---- the k-range's activations first (cache hits: issued ahead of the weight tiles they do
+  // not queue behind the weights' HBM round trip), XI items per thread, branch-free: item
+  // q = (i*4 + kg)*M + r is slot q = x[r][32(kt0+i) + 8kg .. +7]; items past the end load item 0
+  // and go to a dummy slot ----
+  const int items = nk * 4 * M;
+  float xv[XI][8];
+#pragma unroll
+  for (int u = 0; u < XI; ++u) {
+    const int q = u * (int)blockDim.x + tid, qc = q < items ? q : 0;
+    const int r = qc % M, rest = qc / M;
+    load8(a.X + (size_t)r * a.ldx + (size_t)kt0 * 32 + rest * 8, xv[u]);
+  }
+
+  // ---- weight prefetch (slots past the range re-read its last tile, never consumed) ----
+  typename ET<T>::A wb[P];
+#pragma unroll
+  for (int p = 0; p < P; ++p) wb[p] = ET<T>::load_nt(w0 + (size_t)min(p, nk - 1) * 512);
+
+  const size_t zero_off = (size_t)items * 32;
+#pragma unroll
+  for (int u = 0; u < XI; ++u) {
+    const int q = u * (int)blockDim.x + tid;
+    ET<T>::to_lds(lds + (q < items ? (size_t)q * 32 : zero_off + 32), xv[u]);
+  }
+  // items beyond XI per thread (shapes the launcher could not cover up front)
+  for (int q = XI * (int)blockDim.x + tid; q < items; q += blockDim.x) {
+    const int r = q % M, rest = q / M;
+    float x[8];
+    load8(a.X + (size_t)r * a.ldx + (size_t)kt0 * 32 + rest * 8, x);
+    ET<T>::to_lds(lds + (size_t)q * 32, x);
+  }
+  if (tid < 2) *reinterpret_cast<float4*>(lds + zero_off + tid * 16) = make_float4(0.f, 0.f, 0.f, 0.f);
+  __syncthreads();
+
+  // ---- stream the range: TT token tiles per weight tile ----
+  const char* xa[TT];
+#pragma unroll
+  for (int tt = 0; tt < TT; ++tt) {
+    const int m = tt * 16 + tl;
+    xa[tt] = lds + (m < M ? ((size_t)kg * M + m) * 32 : zero_off);
+  }
+  const size_t xs = (size_t)4 * M * 32;   // bytes per k-tile
+  f32x4 acc[TT];
+#pragma unroll
+  for (int tt = 0; tt < TT; ++tt) acc[tt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto consume = [&](int slot, int i) {
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt) {
+      const int m = tt * 16 + tl;
+      ET<T>::mma(acc[tt], wb[slot], ET<T>::from_lds(xa[tt] + (m < M ? i * xs : 0)));
+    }
+  };
+  int s0 = 0;
+  for (; s0 + 2 * P <= nk; s0 += P) {
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+      consume(p, s0 + p);
+      wb[p] = ET<T>::load_nt(w0 + (size_t)(s0 + p + P) * 512);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+#pragma unroll
+  for (int p = 0; p < P; ++p) {
+    if (s0 + p < nk) {
+      consume(p, s0 + p);
+      if (s0 + p + P < nk) wb[p] = ET<T>::load_nt(w0 + (size_t)(s0 + p + P) * 512);
+    }
+  }
+#pragma unroll
+  for (int p = 0; p < P; ++p)
+    if (s0 + P + p < nk) consume(p, s0 + P + p);
+
+  // ---- the RMSNorm row scales, once per launch (workgroup (0, 0)), for the reduction ----
+  if constexpr (PRO == PRO_NORM) {
+    if (blockIdx.x == 0 && blockIdx.y == 0) {
+      const float ssv[4] = {0.f, 0.f, 0.f, 0.f};
+      for (int m = nl; m < M; m += a.NT) {
+        const float r = wave_row_scale(a, m, ssv, false);
+        if (lane == 0) a.part_rs[m] = r;
+      }
+    }
+  }
+  // ---- range partial: part[ks][m][n], lane (tl, kg) holds features 4kg..4kg+3 of token tt*16+tl ----
+  if (live) {
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt) {
+      const int m = tt * 16 + tl;
+      if (m < M)
+        *reinterpret_cast<float4*>(part + ((size_t)ks * M + m) * a.N + nt * 16 + 4 * kg) =
+            make_float4(acc[tt][0], acc[tt][1], acc[tt][2], acc[tt][3]);
+    }
+  }
+}
+
+// Sum of the k-range partials (k-range order, from 0), RMSNorm row scale, epilogue. Workgroup g
+// handles n-tiles g*NT .. g*NT+NT-1 of all M rows (a.NT, a.NJ = 1 describe that layout to the
+// shared epilogue); the launcher gives it one thread per output element.
+template <typename T, int PRO, int EPI>
+__global__ void __launch_bounds__(1024) k_splitk_reduce(LinArgs a, const float* part) {
+  extern __shared__ float Y[];   // [NT][M][16]
+  const int tid = threadIdx.x;
+  const int M = a.M, n_tiles = a.N >> 4;
+  const Grp gr{(int)blockIdx.x, (int)gridDim.x};
+  EpiPre epre{};
+  epi_load<EPI>(a, gr, tid, epre);
+  const int per = M * 16;
+  for (int e = tid; e < a.NT * per; e += blockDim.x) {
+    const int lt = e / per, r = e - lt * per, m = r >> 4, c = r & 15;
+    const int nt = blockIdx.x * a.NT + lt;
+    // all k-range partials in flight at once, then added in k-range order from 0 (the order of
+    // sum_partials)
+    const float* pp = part + (size_t)m * a.N + min(nt, n_tiles - 1) * 16 + c;
+    const size_t stride = (size_t)M * a.N;
+    float v[16];
+#pragma unroll
+    for (int k = 0; k < 16; ++k) v[k] = k < a.KS ? pp[k * stride] : 0.f;
+    float y = 0.f;
+#pragma unroll
+    for (int k = 0; k < 16; ++k)
+      if (k < a.KS) y += v[k];
+    for (int k = 16; k < a.KS; ++k) y += pp[k * stride];
+    if constexpr (PRO == PRO_NORM) y *= a.part_rs[m];   // row scale from the split-K launch
+    Y[e] = nt < n_tiles ? y : 0.f;
+  }
+  __syncthreads();
+  linear_epilogue<T, EPI>(a, gr, Y, per, epre);
+}
+
 // Reduce per-n-group argmax partials of one row; lowest token id wins among equal maxima.
 __global__ void __launch_bounds__(256) k_argmax_finalize(const float* val, const int* idx, int stride, int n_parts,
                                                          int* tok_out, int tok_stride) {
@@ -484,9 +636,16 @@ __global__ void __launch_bounds__(256) k_argmax_finalize(const float* val, const
 // ---------------------------------------------------------------------------------------------
 // Launchers.
 // ---------------------------------------------------------------------------------------------
+// waves (n-tiles) per workgroup of the split-K kernel
+static constexpr int SPLITK_NT = 8;
+
 size_t linear_lds_bytes(int M, int K, int NT, int KS, int S, int NJ, int kind) {
   (void)S;
   if (kind == LIN_LDS) return lds_x_bytes(M, K >> 5) + (size_t)NJ * NT * KS * M * 16 * sizeof(float);
+  if (kind == LIN_SPLITK) {
+    const int nk_max = ((K >> 5) + KS - 1) / KS;
+    return (size_t)nk_max * 4 * M * 32 + 64;
+  }
   return (size_t)(NT * KS * M * 16) * sizeof(float);
 }
 
@@ -507,6 +666,35 @@ static void launch_linear_pe(const LinArgs& a0, int kind, hipStream_t s, const L
     const dim3 block(64 * a.NT * a.KS);
     const size_t lds = linear_lds_bytes(a.M, a.K, a.NT, a.KS, a.S, a.NJ, kind);
     launch(k_linear_lds<T, PRO, EPI>, grid, block, lds, s, ev, a);
+    return;
+  }
+  if (kind == LIN_SPLITK) {
+    const int nk_max = ((a.K >> 5) + a.KS - 1) / a.KS;
+    LinArgs b = a;
+    b.NT = SPLITK_NT;
+    b.NJ = 1;
+    const dim3 grid((n_tiles + SPLITK_NT - 1) / SPLITK_NT, a.KS), block(64 * SPLITK_NT);
+    const size_t lds = (size_t)nk_max * 4 * a.M * 32 + 64;   // + zero slot + dummy slot
+    const LaunchEvents e0{ev ? ev->start : nullptr, nullptr}, e1{nullptr, ev ? ev->stop : nullptr};
+    const int xi = (nk_max * 4 * a.M + (int)block.x - 1) / (int)block.x <= 4 ? 4 : 8;
+    const LaunchEvents* e = ev ? &e0 : nullptr;
+    switch ((a.M + 15) / 16 * 16 + xi) {
+      case 20: launch(k_linear_splitk<T, 1, 4, PRO>, grid, block, lds, s, e, b, a.part); break;
+      case 24: launch(k_linear_splitk<T, 1, 8, PRO>, grid, block, lds, s, e, b, a.part); break;
+      case 36: launch(k_linear_splitk<T, 2, 4, PRO>, grid, block, lds, s, e, b, a.part); break;
+      case 40: launch(k_linear_splitk<T, 2, 8, PRO>, grid, block, lds, s, e, b, a.part); break;
+      case 52: launch(k_linear_splitk<T, 3, 4, PRO>, grid, block, lds, s, e, b, a.part); break;
+      case 56: launch(k_linear_splitk<T, 3, 8, PRO>, grid, block, lds, s, e, b, a.part); break;
+      case 68: launch(k_linear_splitk<T, 4, 4, PRO>, grid, block, lds, s, e, b, a.part); break;
+      default: launch(k_linear_splitk<T, 4, 8, PRO>, grid, block, lds, s, e, b, a.part); break;
+    }
+    // one output element per thread (the epilogue loads each thread's row data up front)
+    LinArgs r = a;
+    r.NT = 1;
+    r.NJ = 1;
+    const int rthreads = (a.M * 16 + 63) / 64 * 64;
+    launch(k_splitk_reduce<T, PRO, EPI>, dim3(n_tiles), dim3(rthreads), (size_t)a.M * 16 * sizeof(float), s,
+           ev ? &e1 : nullptr, r, (const float*)a.part);
     return;
   }
   a.NJ = 1;
@@ -542,6 +730,14 @@ void launch_argmax_finalize(const float* val, const int* idx, int stride, int n_
 template <typename T, int PRO, int EPI>
 static bool allow_big_lds(int bytes) {
   const void* fns[] = {reinterpret_cast<const void*>(&k_linear_lds<T, PRO, EPI>),
+                       reinterpret_cast<const void*>(&k_linear_splitk<T, 1, 4, PRO>),
+                       reinterpret_cast<const void*>(&k_linear_splitk<T, 1, 8, PRO>),
+                       reinterpret_cast<const void*>(&k_linear_splitk<T, 2, 4, PRO>),
+                       reinterpret_cast<const void*>(&k_linear_splitk<T, 2, 8, PRO>),
+                       reinterpret_cast<const void*>(&k_linear_splitk<T, 3, 4, PRO>),
+                       reinterpret_cast<const void*>(&k_linear_splitk<T, 3, 8, PRO>),
+                       reinterpret_cast<const void*>(&k_linear_splitk<T, 4, 4, PRO>),
+                       reinterpret_cast<const void*>(&k_linear_splitk<T, 4, 8, PRO>),
                        reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 1>),
                        reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 2>),
                        reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 3>),

@@ -57,7 +57,7 @@ struct Plan {
   size_t o_h, o_xg, o_ssq, o_q, o_attn, o_act, o_part, o_row_seq, o_row_pos, o_row_blk, o_row_rope, o_amax_val,
       o_amax_idx, o_vtok;
   size_t o_t, o_len, o_limit, o_active, o_nacc, o_bonus, o_rounds, o_counters, o_drafts, o_tokens,
-      o_trace, o_log, o_bt, o_nll, o_scratch, ws_total;
+      o_trace, o_log, o_bt, o_nll, o_splitk, o_splitk_rs, o_scratch, ws_total;
 };
 
 seed_status validate(const seed_config* c) {
@@ -83,6 +83,8 @@ seed_status validate(const seed_config* c) {
   if (!(c->rope_base > 0.f) || !(c->rms_eps >= 0.f)) return fail(SEED_ERR_ARG, "rope_base must be > 0 and rms_eps >= 0");
   return SEED_OK;
 }
+
+void tile_policy(int N, int K, bool head, int& NT, int& KS, int& S, int& NJ);
 
 Plan make_plan(const seed_config& c) {
   Plan p;
@@ -153,6 +155,18 @@ Plan make_plan(const seed_config& c) {
   p.o_log = take((size_t)p.log_cap * B * 4);
   p.o_bt = take(B * (size_t)p.bt_stride * 4);
   p.o_nll = take((size_t)c.max_ctx * 4);
+  {
+    // k-range partials of the split-K path (passes of more than 16 rows): KS x rows x N floats
+    size_t ksn = 0;
+    const int shapes[4][2] = {{p.QD + 2 * p.KVD, p.H}, {p.H, p.QD}, {2 * p.F, p.H}, {p.H, p.F}};
+    for (const auto& sh : shapes) {
+      int NT, KS, S, NJ;
+      tile_policy(sh[0], sh[1], false, NT, KS, S, NJ);
+      ksn = std::max(ksn, (size_t)KS * sh[0]);
+    }
+    p.o_splitk = take(ksn * R * 4);
+    p.o_splitk_rs = take(R * 4);
+  }
   p.o_scratch = take((size_t)std::max({p.V, p.QD + 2 * p.KVD, 2 * p.F, p.H}) * 4);
   p.ws_total = o;
   return p;
@@ -319,20 +333,25 @@ LinArgs lin_base(seed_ctx* c, int M) {
   a.amax_val = c->ws<float>(p.o_amax_val);
   a.amax_idx = c->ws<int>(p.o_amax_idx);
   a.amax_stride = p.V / 16;
+  a.part = c->ws<float>(p.o_splitk);
+  a.part_rs = c->ws<float>(p.o_splitk_rs);
   return a;
 }
 
-// Kernel for one linear launch: activation rows staged in LDS when they fit (M <= 16), else
-// activation fragments read from global memory (prefill, large batches, very large K).
-int linear_kind(const LinArgs& a) {
+// Kernel for one linear launch: activation rows staged in LDS when they fit (M <= 16); passes of
+// more rows split K across workgroups (each stages its k-range only) and add the range partials
+// in a second kernel; otherwise activation fragments are read from global memory.
+int linear_kind(const LinArgs& a, bool head) {
   if (a.M <= 16 && linear_lds_bytes(a.M, a.K, a.NT, a.KS, a.S, a.NJ, LIN_LDS) <= linear_lds_limit()) return LIN_LDS;
+  if (a.M > 16 && !head && linear_lds_bytes(a.M, a.K, a.NT, a.KS, a.S, a.NJ, LIN_SPLITK) <= linear_lds_limit())
+    return LIN_SPLITK;
   return LIN_GLOBAL;
 }
 
 template <typename T>
 void linear(seed_ctx* c, LinArgs a, int pro, int epi, int phase, int op, bool cap) {
   tile_policy(a.N, a.K, epi == EPI_HEAD, a.NT, a.KS, a.S, a.NJ);
-  const int kind = linear_kind(a);
+  const int kind = linear_kind(a, epi == EPI_HEAD);
   timed(c, phase, op, cap, [&](const LaunchEvents* ev) { launch_linear<T>(a, pro, epi, kind, c->s, ev); });
 }
 
