@@ -10,6 +10,9 @@ Modules:
   model  -- the decoder-only transformer f (Preliminaries, Eq. 1) with an explicit KV cache.
   seed   -- Algorithm 2 (fixed-length drafting + verification), brute-force greedy decoding
             and the parallel block-mask drafter pass (Sec. 3.2).
+  tree   -- confidence-aware dynamic drafting with tree-based verification (the main-experiment
+            decoding mode; appendix "Confidence-Aware Dynamic Drafting", "Tree-Based
+            Verification", Fig. 3).
   cost   -- the parameter-count cost model of Appendix E (Tables 9 and 10).
 
 Every function cites the passage it follows. Readings taken where the paper is silent are listed
