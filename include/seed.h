@@ -210,6 +210,25 @@ seed_status seed_generate(seed_ctx* ctx, int32_t B, const int32_t* tokens, const
                           seed_stats* stats);
 
 /*
+ * Tree-based verification (Method, Adaptive Drafting with Tree-Based Verification; appendix
+ * "Tree-Based Verification", Fig. 3 right) of one packed draft tree of the context's single
+ * sequence (B = 1), with acceptance and commit. Node 0 is the pending token X[p] (p = t - 1, the
+ * root); nodes 1..D are the top-1 chain (parent of node i is i-1, depth i); every later node is a
+ * leaf whose parent is the root or a chain node of depth < D, at depth parent + 1. One full-model
+ * pass runs over the nodes: node i at rotary position p + depth(i) attends to the committed prefix
+ * and to its ancestors (and itself). From the root, the path follows the child whose token equals
+ * the verifier's argmax at the current node; the accepted tokens and the bonus token (the argmax
+ * at the last node reached) are appended; the cache keeps the root's and the accepted nodes'
+ * keys/values at positions p, p+1, ...
+ * tokens, parents: host [n], 1 <= n <= 64. path: nullable host [D], the accepted nodes;
+ * path_len, bonus: nullable host. logits: nullable device [n * vocab], one row per node.
+ * Errors: SEED_ERR_STATE before seed_prefill; SEED_ERR_UNSUPPORTED if B != 1; SEED_ERR_ARG for a
+ * malformed tree or token; SEED_ERR_CAPACITY if t + n + 1 > max_ctx.
+ */
+seed_status seed_verify_tree(seed_ctx* ctx, int32_t n, const int32_t* tokens, const int32_t* parents,
+                             int32_t* path, int32_t* path_len, int32_t* bonus, float* logits);
+
+/*
  * Forward pass of the speculative drafting objective L_spec (Algorithm 1, Sec. 3.2, Fig. 2 right)
  * on one sequence X[0..n-1] with training block size `block`: the full model runs over the
  * sequence (as seed_prefill, which this call replaces: afterwards the decode state is that of

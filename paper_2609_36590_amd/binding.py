@@ -57,7 +57,7 @@ class SeedStats(ctypes.Structure):
 EXPORTS = ("seed_arena_bytes", "seed_create", "seed_load_weights", "seed_prefill", "seed_draft",
            "seed_verify", "seed_rounds", "seed_generate", "seed_get_tokens", "seed_kernel_timing",
            "seed_kernel_timing_read", "seed_last_error", "seed_destroy", "seed_spec_kv_bytes",
-           "seed_spec_forward")
+           "seed_spec_forward", "seed_verify_tree")
 
 _LIB = None
 _P = ctypes.c_void_p
@@ -96,6 +96,7 @@ def load_library(path: str | None = None):
         "seed_kernel_timing": [_P, ctypes.c_int32, ctypes.c_int32],
         "seed_kernel_timing_read": [_P, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_double)],
         "seed_spec_kv_bytes": [ctypes.POINTER(SeedConfig), ctypes.POINTER(ctypes.c_size_t)],
+        "seed_verify_tree": [_P, ctypes.c_int32, _I32P, _I32P, _I32P, _I32P, _I32P, _P],
         "seed_spec_forward": [_P, ctypes.c_int32, _I32P, ctypes.c_int32, _P, _P, _P, ctypes.POINTER(ctypes.c_double)],
     }
     for name, args in sig.items():
@@ -246,6 +247,16 @@ def seed_spec_forward(ctx: int, tokens, block: int, shallow_kv: int, logits: int
     return loss.value if want_loss else None
 
 
+def seed_verify_tree(ctx: int, tokens, parents, logits_ptr: int | None = None):
+    t, tp = _i32(tokens)
+    pa, pp = _i32(parents)
+    path = np.zeros(len(t), dtype=np.int32)
+    n_path, bonus = ctypes.c_int32(), ctypes.c_int32()
+    _check(load_library().seed_verify_tree(ctx, len(t), tp, pp, path.ctypes.data_as(_I32P), ctypes.byref(n_path),
+                                           ctypes.byref(bonus), logits_ptr), "seed_verify_tree")
+    return [int(x) for x in path[:n_path.value]], bonus.value
+
+
 def seed_destroy(ctx: int):
     load_library().seed_destroy(ctx)
 
@@ -311,6 +322,13 @@ class Decoder:
 
     def tokens(self, b: int):
         return seed_get_tokens(self.ctx, b, self.cfg.max_ctx)
+
+    def verify_tree(self, tokens, parents, logits: bool = False):
+        """Tree-based verification of one packed draft tree: (accepted path nodes, bonus token,
+        logits [n, vocab] or None)."""
+        lg = self._logits(len(tokens)) if logits else None
+        path, bonus = seed_verify_tree(self.ctx, tokens, parents, lg.data_ptr() if lg is not None else None)
+        return path, bonus, (self._host(lg, (len(tokens),)) if logits else None)
 
     def spec_forward(self, tokens, block: int, logits: bool = True):
         """Forward pass of the speculative drafting objective on one sequence: (drafter logits

@@ -12,6 +12,11 @@
 // tiles. The 4 waves' partials are merged left to right in LDS and written as the group partial
 // (o, m, l), or as the final output when the pass sees a single group.
 //
+// The tree variant verifies a packed draft tree (Tree-Based Verification): node i of the tree sits
+// at rotary position p + depth(i) and cache slot p + i, the top-1 chain first, so a node's
+// ancestors are exactly the positions below its rotary position; it attends to those and to its
+// own slot.
+//
 // The block-causal variant (SPEC) computes the drafter pass of the speculative drafting objective
 // (Algorithm 1, Fig. 2 right): row q attends to the deep cache at positions below its block start
 // s and to the pass's own keys/values (a second, position-indexed cache) at s..q. Tiles that
@@ -76,8 +81,14 @@ struct PV<float> {
   }
 };
 
-template <typename T, int HD, int QT, int TPW, bool SPEC>
+enum AttnMode { ATT_CAUSAL = 0, ATT_SPEC = 1, ATT_TREE = 2 };
+
+template <typename T, int HD, int QT, int TPW, int MODE>
 __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
+  constexpr bool SPEC = MODE == ATT_SPEC;
+  // packed draft tree: a row sees positions below its rotary position (the committed prefix and
+  // its ancestors on the top-1 chain) and its own cache slot
+  constexpr bool TREE = MODE == ATT_TREE;
   constexpr int DS = HD / 32;    // 32-dim steps of S^T
   constexpr int DT = HD / 16;    // 16-dim tiles of O^T
   constexpr int PS = HD + 4;     // floats per query vector in a group partial
@@ -102,7 +113,7 @@ __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
   const size_t layer_base = (size_t)a.layer * a.n_blocks;
 
   // ---- round trip 1: the last row's position, the run's block-table entries, the queries ----
-  const int maxpos = a.row_pos[mrow0 + nr - 1];
+  const int maxpos = TREE ? a.row_slot[mrow0 + nr - 1] : a.row_pos[mrow0 + nr - 1];
   // block-causal pass: the first and last rows' block starts bound which tiles need which cache
   const int s_first = SPEC ? (a.row_pos[mrow0] / a.s_block) * a.s_block : 0;
   const int s_last = SPEC ? (maxpos / a.s_block) * a.s_block : 0;
@@ -112,7 +123,7 @@ __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
   // queries (lane column qv = qt*16 + tl, k-slots d = ds*32 + kg*8 + j) and their positions:
   // loaded branch-free from a valid row, masked when converted
   float qraw[QT][DS][8];
-  int qpos[QT], qstart[QT];
+  int qpos[QT], qstart[QT], qslot[QT];
   bool qok[QT];
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
@@ -120,6 +131,7 @@ __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
     qok[qt] = qv < nqv;
     const int rl = qok[qt] ? qv / a.G : 0, gq = qok[qt] ? qv - rl * a.G : 0;
     qpos[qt] = a.row_pos[mrow0 + rl];
+    qslot[qt] = TREE ? a.row_slot[mrow0 + rl] : 0;
     const float* qp = a.q + (size_t)(mrow0 + rl) * qstride + (h * a.G + gq) * HD + kg * 8;
 #pragma unroll
     for (int ds = 0; ds < DS; ++ds) load8(qp + ds * 32, qraw[qt][ds]);
@@ -174,7 +186,10 @@ __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
   typename ET<T>::B qf[QT][DS];
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
-    if (!qok[qt]) qpos[qt] = -1;
+    if (!qok[qt]) {
+      qpos[qt] = -1;
+      qslot[qt] = -1;
+    }
     // block-causal pass: positions below qstart come from the deep cache
     qstart[qt] = SPEC ? (qpos[qt] / a.s_block) * a.s_block : 0;
 #pragma unroll
@@ -227,6 +242,7 @@ __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
       for (int i = 0; i < 4; ++i) {
         const int pos = P0 + 16 * t + 4 * kg + i;
         if constexpr (SPEC) s[i] = (pos > qpos[qt]) ? NEG_INF : (pos < qstart[qt] ? sacc[qt][i] : ssh[qt][i]);
+        else if constexpr (TREE) s[i] = (pos < qpos[qt] || pos == qslot[qt]) ? sacc[qt][i] : NEG_INF;
         else s[i] = (pos <= qpos[qt]) ? sacc[qt][i] : NEG_INF;
         mx = fmaxf(mx, s[i]);
       }
@@ -338,7 +354,8 @@ __global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
   const int item = gid / CMB_LANES, j = gid % CMB_LANES;
   const int qv = item / HD4, d = (item - qv * HD4) * 4;
   if (qv >= nqv) return;   // the 8 lanes of an item leave together
-  const int n_groups = a.row_pos[mrow0 + nr - 1] / a.span + 1;
+  // the same group count as k_attention: a tree's rows reach their cache slots, not positions
+  const int n_groups = (a.tree ? a.row_slot[mrow0 + nr - 1] : a.row_pos[mrow0 + nr - 1]) / a.span + 1;
   if (n_groups == 1) return;   // k_attention wrote the final output
   const float* pq = a.part + ((((size_t)(b * a.n_kv + h) * a.n_rb + rb) * a.n_groups_max) * 32 + qv) * PS;
   float m_r = NEG_INF, l_r = 0.f, o_r[4] = {0.f, 0.f, 0.f, 0.f};
@@ -391,13 +408,13 @@ static void launch_kernel(Kern k, dim3 grid, hipStream_t s, const LaunchEvents* 
   else hipLaunchKernelGGL(k, grid, dim3(256), 0, s, a);
 }
 
-template <typename T, int HD, int QT, bool SPEC>
+template <typename T, int HD, int QT, int MODE>
 static void launch_attention_qt(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev) {
   const dim3 grid(a.n_groups_max, a.n_kv * a.n_rb, a.B);
   switch (a.span) {
-    case 64: launch_kernel(k_attention<T, HD, QT, 1, SPEC>, grid, s, ev, a); break;
-    case 128: launch_kernel(k_attention<T, HD, QT, 2, SPEC>, grid, s, ev, a); break;
-    default: launch_kernel(k_attention<T, HD, QT, 4, SPEC>, grid, s, ev, a); break;
+    case 64: launch_kernel(k_attention<T, HD, QT, 1, MODE>, grid, s, ev, a); break;
+    case 128: launch_kernel(k_attention<T, HD, QT, 2, MODE>, grid, s, ev, a); break;
+    default: launch_kernel(k_attention<T, HD, QT, 4, MODE>, grid, s, ev, a); break;
   }
 }
 
@@ -405,11 +422,14 @@ template <typename T, int HD>
 static void launch_attention_hd(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev) {
   const bool q2 = std::min(a.RB, a.R) * a.G > 16;
   if (a.s_block > 0) {
-    if (q2) launch_attention_qt<T, HD, 2, true>(a, s, ev);
-    else launch_attention_qt<T, HD, 1, true>(a, s, ev);
+    if (q2) launch_attention_qt<T, HD, 2, ATT_SPEC>(a, s, ev);
+    else launch_attention_qt<T, HD, 1, ATT_SPEC>(a, s, ev);
+  } else if (a.tree) {
+    if (q2) launch_attention_qt<T, HD, 2, ATT_TREE>(a, s, ev);
+    else launch_attention_qt<T, HD, 1, ATT_TREE>(a, s, ev);
   } else {
-    if (q2) launch_attention_qt<T, HD, 2, false>(a, s, ev);
-    else launch_attention_qt<T, HD, 1, false>(a, s, ev);
+    if (q2) launch_attention_qt<T, HD, 2, ATT_CAUSAL>(a, s, ev);
+    else launch_attention_qt<T, HD, 1, ATT_CAUSAL>(a, s, ev);
   }
 }
 

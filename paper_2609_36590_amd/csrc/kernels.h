@@ -51,6 +51,7 @@ struct LinArgs {
   float* q;               // [M][n_heads*head_dim] rotated queries (fp32)
   void* kv;               // KV pool
   const int* row_pos;     // [M] absolute position of each row
+  const int* row_slot;     // [M] cache position each row's keys/values are written to (= row_pos except for tree rows)
   const int* row_blk;     // [M] KV-pool block holding that position (same block in every layer)
   const float* row_rope;  // [M][head_dim]: cos(pos*theta_i) for i < head_dim/2, then sin(pos*theta_i)
   int layer, n_blocks, n_heads, n_kv, head_dim;
@@ -72,6 +73,8 @@ struct AttnArgs {
   const int* bt;
   int bt_stride;
   const int* row_pos;     // [M]; rows m = b*R + r, consecutive positions within a sequence
+  const int* row_slot;    // [M] cache slot of each row's keys/values (tree rows: p + node index;
+                          // elsewhere equal to row_pos); the tree variant masks with it
   int B, R;               // sequences, rows per sequence
   int n_heads, n_kv, head_dim, G;  // G = n_heads / n_kv
   int RB, n_rb;           // rows per row-block (G*RB <= 32), row-blocks per sequence
@@ -80,6 +83,7 @@ struct AttnArgs {
   // the shallow cache skv (this pass's keys/values, block id = position / 16) at s..q
   const void* skv;
   int s_layer, s_n_blocks, s_block;
+  int tree;               // 1: packed draft tree rows (mask by row_pos and row_slot)
   int span;               // positions per workgroup group: 64, 128 or 256 (attention_span)
   int n_groups_max;       // grid extent over groups; n_groups_max * span == bt_stride * 16
   float scale_log2;       // log2(e) / sqrt(head_dim)
@@ -88,7 +92,7 @@ struct AttnArgs {
 };
 
 // Per-pass row setup + embedding gather.
-enum SetupMode { SETUP_PREFILL = 0, SETUP_DRAFT = 1, SETUP_VERIFY = 2, SETUP_SPEC = 3 };
+enum SetupMode { SETUP_PREFILL = 0, SETUP_DRAFT = 1, SETUP_VERIFY = 2, SETUP_SPEC = 3, SETUP_TREE = 4 };
 
 struct SetupArgs {
   int mode;
@@ -107,6 +111,9 @@ struct SetupArgs {
   int H;
   int* row_seq;
   int* row_pos;
+  int* row_slot;          // [M] cache slot of the row's keys/values
+  const int* tree_tok;    // SETUP_TREE: node tokens [M] (node 0 = the pending token)
+  const int* tree_depth;  // SETUP_TREE: node depths [M] (rotary position t-1 + depth)
   // per-row KV block and RoPE row for the pass's QKV epilogues
   const int* bt;          // block tables [B][bt_stride]
   int bt_stride;
@@ -166,6 +173,12 @@ void launch_attn_combine(const AttnArgs& a, hipStream_t s, const LaunchEvents* e
 template <typename T>
 void launch_setup(const SetupArgs& a, hipStream_t s);
 void launch_accept(const DevState& st, int B, int k, hipStream_t s);
+// Tree acceptance for one sequence (packed tree of n nodes: tokens, parents, depths; the verifier
+// argmax per node in st.vtok) and the move of an accepted leaf's keys/values in every layer to the
+// cache position of its depth. out[0] = accepted path length, out[1] = bonus, out[2..] = path.
+void launch_accept_tree(const DevState& st, int n, const int* tree_tok, const int* tree_par, const int* tree_depth,
+                        int* out, void* kv, int n_layers, int n_blocks, int n_kv, int head_dim, int esize,
+                        const int* bt, hipStream_t s);
 // nll[r] = logsumexp(logits[r]) - logits[r][target[r]] for r < rows (row stride V)
 void launch_row_nll(const float* logits, int rows, int V, const int* target, float* nll, hipStream_t s);
 // Reduce the head's per-workgroup argmax partials of M rows; row m's token goes to

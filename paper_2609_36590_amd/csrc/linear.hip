@@ -68,7 +68,7 @@ __device__ __forceinline__ void epi_load(const LinArgs& a, Grp gr, int e, EpiPre
   } else if constexpr (EPI == EPI_QKV) {
     int sec, head, j;
     qkv_tile(a, nt, sec, head, j);
-    p.pos = a.row_pos[m];
+    p.pos = a.row_slot[m];   // the cache slot (the rotary position enters through row_rope)
     p.blk = a.row_blk[m];
     const int fi = 8 * j + (c & 7);
     p.cs = a.row_rope[(size_t)m * a.head_dim + fi];

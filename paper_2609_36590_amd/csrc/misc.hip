@@ -1,6 +1,8 @@
 // Row setup + embedding gather, acceptance/commit, and load-time helpers.
 #include "device_common.h"
 
+#include <algorithm>
+
 namespace seedk {
 
 // ---------------------------------------------------------------------------------------------
@@ -12,9 +14,9 @@ namespace seedk {
 template <typename T>
 __global__ void __launch_bounds__(256) k_setup(SetupArgs a) {
   const int m = blockIdx.x;
-  __shared__ int s_tok, s_pos, s_seq;
+  __shared__ int s_tok, s_pos, s_seq, s_slot;
   if (threadIdx.x == 0) {
-    int b, pos, tok;
+    int b, pos, tok, slot = -1;
     if (a.mode == SETUP_PREFILL || a.mode == SETUP_SPEC) {
       b = a.pf_seq;
       pos = a.pf_pos0 + m;
@@ -23,6 +25,13 @@ __global__ void __launch_bounds__(256) k_setup(SetupArgs a) {
       b = m;
       pos = a.t[b] - 1 + (a.step - 1);
       tok = a.drafts[b * a.dstride + a.step - 1];
+    } else if (a.mode == SETUP_TREE) {
+      // packed draft tree (Tree-Based Verification): node m at rotary position p + depth,
+      // cached at slot p + m
+      b = 0;
+      pos = a.t[0] - 1 + a.tree_depth[m];
+      slot = a.t[0] - 1 + m;
+      tok = a.tree_tok[m];
     } else {
       b = m / a.R;
       const int r = m - b * a.R;
@@ -34,20 +43,23 @@ __global__ void __launch_bounds__(256) k_setup(SetupArgs a) {
         a.drafts[b * a.dstride + r] = tok;
       }
     }
+    if (slot < 0) slot = pos;
     a.row_seq[m] = b;
     a.row_pos[m] = pos;
+    a.row_slot[m] = slot;
     s_tok = tok;
     s_pos = pos;
     s_seq = b;
+    s_slot = slot;
   }
   __syncthreads();
   const int tok = s_tok;
   {
     // the row's KV block and RoPE angles, read once per pass by every layer's QKV epilogue
-    const int pos = s_pos, half = a.head_dim >> 1;
-    // the block-causal drafter pass writes its keys/values to a cache of its own, indexed by
-    // position (block id = position / 16)
-    if (threadIdx.x == 0) a.row_blk[m] = a.mode == SETUP_SPEC ? (pos >> 4) : a.bt[s_seq * a.bt_stride + (pos >> 4)];
+    const int pos = s_pos, half = a.head_dim >> 1, slot = s_slot;
+    // keys/values go to the row's cache slot; the block-causal drafter pass writes to a cache of
+    // its own, indexed by position (block id = position / 16)
+    if (threadIdx.x == 0) a.row_blk[m] = a.mode == SETUP_SPEC ? (slot >> 4) : a.bt[s_seq * a.bt_stride + (slot >> 4)];
     for (int i = threadIdx.x; i < half; i += blockDim.x) {
       a.row_rope[(size_t)m * a.head_dim + i] = a.rope_cos[(size_t)pos * half + i];
       a.row_rope[(size_t)m * a.head_dim + half + i] = a.rope_sin[(size_t)pos * half + i];
@@ -118,6 +130,84 @@ __global__ void __launch_bounds__(64) k_accept(DevState st, int B, int k) {
 }
 
 // ---------------------------------------------------------------------------------------------
+// Tree acceptance and commit (Tree-Based Verification, one sequence): from the root, move to the
+// child whose token equals the verifier's argmax at the current node while one exists; append
+// the accepted tokens and the bonus token (the argmax at the last node reached). The nodes of the
+// top-1 chain are cached at the positions of their depths already (node d of the chain has
+// depth d); an accepted leaf is not, and k_kv_move copies its keys/values there in every layer.
+// out: [0] path length, [1] bonus, [2 + i] path nodes, [TREE_MOVE] leaf to move (0 = none),
+// [TREE_MOVE + 1] p = the old pending token's position.
+// ---------------------------------------------------------------------------------------------
+static constexpr int TREE_MOVE = 2 + 64;
+
+__global__ void __launch_bounds__(64) k_accept_tree(DevState st, int n, const int* tok, const int* par,
+                                                   const int* depth, int* out) {
+  if (threadIdx.x != 0) return;
+  const int s_round = *st.rounds;
+  int logv = -1;
+  out[0] = 0;
+  out[1] = -1;
+  out[TREE_MOVE] = 0;
+  if (st.active[0]) {
+    int t = st.t[0];
+    out[TREE_MOVE + 1] = t - 1;
+    int node = 0, len = 0;
+    for (;;) {
+      const int g = st.vtok[node];
+      int nxt = -1;
+      for (int c = 1; c < n; ++c)
+        if (par[c] == node && tok[c] == g) { nxt = c; break; }
+      if (nxt < 0) break;
+      out[2 + len] = nxt;
+      ++len;
+      node = nxt;
+    }
+    const int bonus = st.vtok[node];
+    if (node != depth[node]) out[TREE_MOVE] = node;
+    int* tk = st.tokens;
+    int stop = 0, ncommit = len + 1;
+    for (int i = 0; i < len + 1; ++i) {
+      const int tv = (i < len) ? tok[out[2 + i]] : bonus;
+      tk[t + i] = tv;
+      if (st.eos >= 0 && tv == st.eos) { ncommit = i + 1; stop = 1; break; }
+    }
+    t += ncommit;
+    st.t[0] = t;
+    st.drafts[0] = tk[t - 1];
+    st.nacc[0] = len;
+    st.bonus[0] = bonus;
+    if (stop || t >= st.limit[0]) st.active[0] = 0;
+    st.counters[0] += n - 1;
+    st.counters[1] += len;
+    out[0] = len;
+    out[1] = bonus;
+    logv = len;
+  }
+  if (s_round < st.log_cap) st.nacc_log[s_round] = logv;
+  *st.rounds = s_round + 1;
+}
+
+// Copies the keys/values of cache slot p + leaf to position p + depth(leaf) in every layer, when
+// k_accept_tree asked for it.
+template <typename T>
+__global__ void __launch_bounds__(256) k_kv_move(const int* depth, const int* out, T* kv, int n_layers, int n_blocks,
+                                                 int n_kv, int head_dim, const int* bt) {
+  const int leaf = out[TREE_MOVE];
+  if (leaf == 0) return;
+  const int p = out[TREE_MOVE + 1];
+  const int from = p + leaf, to = p + depth[leaf];
+  const int per_layer = 2 * n_kv * head_dim;   // K and V values of one position
+  for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < n_layers * per_layer; e += gridDim.x * blockDim.x) {
+    const int l = e / per_layer, r = e - l * per_layer;
+    const int kvs = r / (n_kv * head_dim), r2 = r - kvs * n_kv * head_dim, h = r2 / head_dim, d = r2 - h * head_dim;
+    const size_t fb = (((size_t)l * n_blocks + bt[from >> 4]) * 2 + kvs) * n_kv + h;
+    const size_t tb = (((size_t)l * n_blocks + bt[to >> 4]) * 2 + kvs) * n_kv + h;
+    if (kvs == 0) kv[tb * 16 * head_dim + (to & 15) * head_dim + d] = kv[fb * 16 * head_dim + (from & 15) * head_dim + d];
+    else kv[tb * head_dim * 16 + d * 16 + (to & 15)] = kv[fb * head_dim * 16 + d * 16 + (from & 15)];
+  }
+}
+
+// ---------------------------------------------------------------------------------------------
 // Negative log-likelihood of each row's target under the softmax of its logits (the per-position
 // term of L_spec, Algorithm 1): one workgroup per row; max, then the sum of exponentials, both
 // reduced with a fixed tree.
@@ -181,6 +271,19 @@ void launch_setup(const SetupArgs& a, hipStream_t s) {
 
 void launch_accept(const DevState& st, int B, int k, hipStream_t s) {
   hipLaunchKernelGGL(k_accept, dim3(1), dim3(64), 0, s, st, B, k);
+}
+
+void launch_accept_tree(const DevState& st, int n, const int* tree_tok, const int* tree_par, const int* tree_depth,
+                        int* out, void* kv, int n_layers, int n_blocks, int n_kv, int head_dim, int esize,
+                        const int* bt, hipStream_t s) {
+  hipLaunchKernelGGL(k_accept_tree, dim3(1), dim3(64), 0, s, st, n, tree_tok, tree_par, tree_depth, out);
+  const int blocks = std::max(1, std::min(256, (n_layers * 2 * n_kv * head_dim + 255) / 256));
+  if (esize == 2)
+    hipLaunchKernelGGL(k_kv_move<uint16_t>, dim3(blocks), dim3(256), 0, s, tree_depth, (const int*)out,
+                       reinterpret_cast<uint16_t*>(kv), n_layers, n_blocks, n_kv, head_dim, bt);
+  else
+    hipLaunchKernelGGL(k_kv_move<float>, dim3(blocks), dim3(256), 0, s, tree_depth, (const int*)out,
+                       reinterpret_cast<float*>(kv), n_layers, n_blocks, n_kv, head_dim, bt);
 }
 
 void launch_row_nll(const float* logits, int rows, int V, const int* target, float* nll, hipStream_t s) {

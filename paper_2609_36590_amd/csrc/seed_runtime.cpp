@@ -54,10 +54,10 @@ struct Plan {
   std::vector<size_t> w_attn_norm, w_mlp_norm, w_qkv, w_o, w_gu, w_down;
   size_t kv_total;
   // workspace
-  size_t o_h, o_xg, o_ssq, o_q, o_attn, o_act, o_part, o_row_seq, o_row_pos, o_row_blk, o_row_rope, o_amax_val,
+  size_t o_h, o_xg, o_ssq, o_q, o_attn, o_act, o_part, o_row_seq, o_row_pos, o_row_slot, o_row_blk, o_row_rope, o_amax_val,
       o_amax_idx, o_vtok;
   size_t o_t, o_len, o_limit, o_active, o_nacc, o_bonus, o_rounds, o_counters, o_drafts, o_tokens,
-      o_trace, o_log, o_bt, o_nll, o_splitk, o_splitk_rs, o_scratch, ws_total;
+      o_trace, o_log, o_bt, o_nll, o_splitk, o_splitk_rs, o_tree, o_tree_out, o_scratch, ws_total;
 };
 
 seed_status validate(const seed_config* c) {
@@ -94,8 +94,8 @@ Plan make_plan(const seed_config& c) {
   p.L = c.n_layers; p.LD = c.n_layers - c.n_dec_layers;
   p.QD = p.NQ * p.HD; p.KVD = p.NKV * p.HD; p.G = p.NQ / p.NKV;
   p.RB = std::max(1, 32 / p.G);
-  p.n_rb_max = cdiv(std::max(c.max_draft + 1, PREFILL_ROWS), p.RB);
-  p.max_rows = std::max(PREFILL_ROWS, c.max_batch * (c.max_draft + 1));
+  p.n_rb_max = cdiv(MAX_ROWS, p.RB);
+  p.max_rows = MAX_ROWS;   // decode passes (B (d+1) <= 64), 48-row passes, draft trees of <= 64 nodes
   p.blocks_per_seq = cdiv(c.max_ctx, 16);
   p.span = seedk::attention_span(c.max_ctx);
   p.bt_stride = cdiv(p.blocks_per_seq, p.span / 16) * (p.span / 16);   // whole groups, padded with block 0
@@ -136,6 +136,7 @@ Plan make_plan(const seed_config& c) {
   p.o_part = take(B * p.NKV * p.n_rb_max * (size_t)p.n_groups_max * 32 * (p.HD + 4) * 4);
   p.o_row_seq = take(R * 4);
   p.o_row_pos = take(R * 4);
+  p.o_row_slot = take(R * 4);
   p.o_row_blk = take(R * 4);
   p.o_row_rope = take(R * p.HD * 4);
   p.o_amax_val = take(R * (size_t)(p.V / 16) * 4);
@@ -155,6 +156,8 @@ Plan make_plan(const seed_config& c) {
   p.o_log = take((size_t)p.log_cap * B * 4);
   p.o_bt = take(B * (size_t)p.bt_stride * 4);
   p.o_nll = take((size_t)c.max_ctx * 4);
+  p.o_tree = take(3 * MAX_ROWS * 4);
+  p.o_tree_out = take((2 + MAX_ROWS + 2) * 4);
   {
     // k-range partials of the split-K path (passes of more than 16 rows): KS x rows x N floats
     size_t ksn = 0;
@@ -324,6 +327,7 @@ LinArgs lin_base(seed_ctx* c, int M) {
   a.q = c->ws<float>(p.o_q);
   a.kv = c->KV;
   a.row_pos = c->ws<int>(p.o_row_pos);
+  a.row_slot = c->ws<int>(p.o_row_slot);
   a.row_blk = c->ws<int>(p.o_row_blk);
   a.row_rope = c->ws<float>(p.o_row_rope);
   a.n_blocks = p.n_blocks;
@@ -366,7 +370,7 @@ struct SpecPass {
 // Layers [l0, l1) over M rows (B sequences x R rows each, consecutive positions per sequence).
 template <typename T>
 void run_layers(seed_ctx* c, int M, int B, int R, int l0, int l1, int phase,
-                const int* bt_override, bool cap, const SpecPass* spec = nullptr) {
+                const int* bt_override, bool cap, const SpecPass* spec = nullptr, bool tree = false) {
   const Plan& p = c->p;
   float* h = c->ws<float>(p.o_h);
   for (int li = l0; li < l1; ++li) {
@@ -391,6 +395,8 @@ void run_layers(seed_ctx* c, int M, int B, int R, int l0, int l1, int phase,
     at.bt = bt_override ? bt_override : c->ws<int>(p.o_bt);
     at.bt_stride = p.bt_stride;
     at.row_pos = c->ws<int>(p.o_row_pos);
+    at.row_slot = c->ws<int>(p.o_row_slot);
+    at.tree = tree ? 1 : 0;
     at.B = B; at.R = R;
     at.n_heads = p.NQ; at.n_kv = p.NKV; at.head_dim = p.HD; at.G = p.G;
     at.RB = p.RB; at.n_rb = cdiv(R, p.RB);
@@ -462,6 +468,7 @@ SetupArgs setup_base(seed_ctx* c, int l0) {
   s.H = p.H;
   s.row_seq = c->ws<int>(p.o_row_seq);
   s.row_pos = c->ws<int>(p.o_row_pos);
+  s.row_slot = c->ws<int>(p.o_row_slot);
   s.bt = c->ws<int>(p.o_bt);
   s.bt_stride = p.bt_stride;
   s.rope_cos = c->wf(p.w_rope_cos);
@@ -816,6 +823,27 @@ seed_status run_rounds(seed_ctx* c, int k, int n, bool use_graph) {
 // =============================================================================================
 // C ABI
 // =============================================================================================
+// Tree-based verification of one sequence's packed draft tree: node rows through every layer
+// with the tree attention mask, the LM head (logits optional), then tree acceptance, commit and
+// the move of an accepted leaf's cache entries.
+template <typename T>
+void enqueue_verify_tree(seed_ctx* c, int n, float* logits) {
+  const Plan& p = c->p;
+  SetupArgs s = setup_base(c, 0);
+  s.mode = SETUP_TREE; s.M = n; s.R = n;
+  s.tree_tok = c->ws<int>(p.o_tree);
+  s.tree_depth = c->ws<int>(p.o_tree) + 2 * MAX_ROWS;
+  timed(c, SEED_PHASE_VERIFY, SEED_OP_SETUP, false, [&](const LaunchEvents*) { launch_setup<T>(s, c->s); });
+  run_layers<T>(c, n, 1, n, 0, p.L, SEED_PHASE_VERIFY, nullptr, false, nullptr, true);
+  run_head<T>(c, n, c->ws<int>(p.o_vtok), 1, logits, (long long)p.V, SEED_PHASE_VERIFY, false);
+  DevState st = dev_state(c);
+  timed(c, SEED_PHASE_VERIFY, SEED_OP_ACCEPT, false, [&](const LaunchEvents*) {
+    launch_accept_tree(st, n, c->ws<int>(p.o_tree), c->ws<int>(p.o_tree) + MAX_ROWS, c->ws<int>(p.o_tree) + 2 * MAX_ROWS,
+                       c->ws<int>(p.o_tree_out), c->KV, p.L, p.n_blocks, p.NKV, p.HD, p.esize, c->ws<int>(p.o_bt),
+                       c->s);
+  });
+}
+
 extern "C" {
 
 const char* seed_last_error(void) { return g_err.c_str(); }
@@ -1109,6 +1137,47 @@ seed_status seed_generate(seed_ctx* c, int32_t B, const int32_t* tokens, const i
   hipEventDestroy(e1);
   hipEventDestroy(e2);
   c->sim_accept = -1;
+  c->drafts_k = -1;
+  return SEED_OK;
+}
+
+seed_status seed_verify_tree(seed_ctx* c, int32_t n, const int32_t* tokens, const int32_t* parents, int32_t* path,
+                             int32_t* path_len, int32_t* bonus, float* logits) {
+  seed_status st = check_ready(c);
+  if (st != SEED_OK) return st;
+  if (!c->prefilled) return fail(SEED_ERR_STATE, "call seed_prefill first");
+  if (c->B != 1) return fail(SEED_ERR_UNSUPPORTED, "tree verification runs one sequence (B = 1)");
+  const Plan& p = c->p;
+  if (n < 1 || n > MAX_ROWS) return fail(SEED_ERR_ARG, "the tree needs 1..64 nodes");
+  if (!tokens || !parents) return fail(SEED_ERR_ARG, "tokens and parents must not be NULL");
+  // shape: node 0 is the root; nodes 1..D the top-1 chain (parent i-1); later nodes are leaves
+  // whose parent is the root or a chain node
+  if (parents[0] != -1) return fail(SEED_ERR_ARG, "node 0 must be the root (parent -1)");
+  int D = 0;
+  while (D + 1 < n && parents[D + 1] == D) ++D;
+  std::vector<int> host(3 * MAX_ROWS, 0);
+  for (int i = 0; i < n; ++i) {
+    if (tokens[i] < 0 || tokens[i] >= p.V) return fail(SEED_ERR_ARG, "tree token out of range at node " + std::to_string(i));
+    if (i > D && (parents[i] < 0 || parents[i] >= D))
+      return fail(SEED_ERR_ARG, "node " + std::to_string(i) + ": a node after the chain must hang off the root or a chain node other than the last");
+    host[i] = tokens[i];
+    host[MAX_ROWS + i] = parents[i];
+    host[2 * MAX_ROWS + i] = i <= D ? i : parents[i] + 1;
+  }
+  if ((int64_t)c->t_upper[0] + n + 1 > p.cfg.max_ctx) return fail(SEED_ERR_CAPACITY, "the tree would pass max_ctx");
+  st = ensure_blocks(c, 0, c->t_upper[0] + n + 1);
+  if (st != SEED_OK) return st;
+  HIPCHK(hipMemcpyAsync(c->ws<int>(p.o_tree), host.data(), host.size() * 4, hipMemcpyHostToDevice, c->s));
+  if (p.cfg.dtype == SEED_BF16) enqueue_verify_tree<uint16_t>(c, n, logits);
+  else enqueue_verify_tree<float>(c, n, logits);
+  HIPCHK(hipGetLastError());
+  std::vector<int> out(2 + MAX_ROWS);
+  HIPCHK(hipMemcpyAsync(out.data(), c->ws<int>(p.o_tree_out), out.size() * 4, hipMemcpyDeviceToHost, c->s));
+  st = read_t(c);
+  if (st != SEED_OK) return st;
+  if (path_len) *path_len = out[0];
+  if (bonus) *bonus = out[1];
+  if (path) std::copy(out.begin() + 2, out.begin() + 2 + out[0], path);
   c->drafts_k = -1;
   return SEED_OK;
 }
