@@ -132,7 +132,7 @@ enum {
   SEED_PHASE_VERIFY = 0, SEED_PHASE_DRAFT = 1, SEED_PHASE_PREFILL = 2, SEED_PHASE_SPEC = 3,
   SEED_OP_SETUP = 0, SEED_OP_QKV = 1, SEED_OP_ATTN = 2, SEED_OP_COMBINE = 3, SEED_OP_O = 4,
   SEED_OP_GATEUP = 5, SEED_OP_DOWN = 6, SEED_OP_HEAD = 7, SEED_OP_ACCEPT = 8,
-  SEED_OP_HEAD_ARGMAX = 9
+  SEED_OP_HEAD_ARGMAX = 9, SEED_OP_TOPK = 10
 };
 
 /* Bytes the caller must provide for the weight arena, the KV pool and the workspace. */
@@ -227,6 +227,58 @@ seed_status seed_generate(seed_ctx* ctx, int32_t B, const int32_t* tokens, const
  */
 seed_status seed_verify_tree(seed_ctx* ctx, int32_t n, const int32_t* tokens, const int32_t* parents,
                              int32_t* path, int32_t* path_len, int32_t* bonus, float* logits);
+
+/*
+ * Options of confidence-aware dynamic drafting (Method, Adaptive Drafting with Tree-Based
+ * Verification; appendix "Confidence-Aware Dynamic Drafting"). Each drafting step runs the
+ * decoder-only step of Algorithm 2 on the current chain token; p0 is the softmax probability of
+ * its top-1 token. The step's candidates are its k highest-logit tokens (equal logits: lower id
+ * first), k = k[j] for the first level j with p0 > thr[j], else k_rest, cut to the node budget
+ * max_nodes. The top-1 candidate extends the chain, the others become leaves. Drafting stops
+ * after a step with p0 < tau, after max_depth steps, or when the tree holds max_nodes nodes.
+ * p0 and the decisions are taken in fp32.
+ */
+typedef struct seed_tree_opts {
+  float tau;             /* confidence threshold (the paper uses 0.7, or 0.5 for summarisation) */
+  int32_t max_depth;     /* drafting steps per round, 1 <= max_depth <= max_draft */
+  int32_t n_levels;      /* levels of the top-p table, 0..4 */
+  float thr[4];          /* strictly decreasing thresholds */
+  int32_t k[4];          /* fan-out of each level, 1..16 */
+  int32_t k_rest;        /* fan-out below every threshold, 1..16 */
+  int32_t max_nodes;     /* node budget of a tree (root included), max_depth + 1 .. 64 */
+} seed_tree_opts;
+
+/* The paper's table (p0 > 0.95: 1, > 0.8: 3, > 0.5: 5, else 10), tau = 0.7, 64 nodes. */
+void seed_tree_defaults(seed_tree_opts* opts, int32_t max_depth);
+
+/*
+ * One round's dynamic drafting for the context's single sequence (B = 1, after seed_prefill or
+ * seed_verify_tree), returning the packed tree that seed_verify_tree takes: node 0 the pending
+ * token, nodes 1..D the top-1 chain, then every step's other candidates by step and rank.
+ * tokens, parents: host [64]; n_nodes: host. p0: nullable host [max_depth], the top-1
+ * probability of each step run. logits: nullable device [max_depth * vocab], row i-1 = step i's
+ * drafter logits. Each step waits for the previous one on the host; seed_generate_tree runs the
+ * same kernels without waiting.
+ * Errors: SEED_ERR_STATE before seed_prefill; SEED_ERR_UNSUPPORTED if B != 1 or the vocabulary is
+ * outside 16..262144; SEED_ERR_ARG for invalid options; SEED_ERR_CAPACITY if t + max_nodes + 1 >
+ * max_ctx.
+ */
+seed_status seed_draft_tree(seed_ctx* ctx, const seed_tree_opts* opts, int32_t* tokens, int32_t* parents,
+                            int32_t* n_nodes, float* p0, float* logits);
+
+/*
+ * Dynamic drafting with tree-based verification end to end for one prompt (the decoding mode of
+ * the paper's main experiments): prefill, then rounds of seed_draft_tree + seed_verify_tree until
+ * max_new tokens (or eos_id) are committed. Lossless: every committed token is the verifier's
+ * greedy choice. out: host [max_new] (-1 past count); count: host. use_graph: 1 replays each
+ * drafting step and each tree size's verification from captured HIP graphs. stats: nullable;
+ * drafted counts tree nodes other than the root, n_accept_log the accepted path length per round.
+ * Errors as seed_generate and seed_draft_tree; the prompt needs len + max_new + 2 (max_nodes + 1)
+ * <= max_ctx.
+ */
+seed_status seed_generate_tree(seed_ctx* ctx, const int32_t* tokens, int32_t len, const seed_tree_opts* opts,
+                               int32_t max_new, int32_t eos_id, int32_t use_graph, int32_t* out, int32_t* count,
+                               seed_stats* stats);
 
 /*
  * Forward pass of the speculative drafting objective L_spec (Algorithm 1, Sec. 3.2, Fig. 2 right)

@@ -13,6 +13,8 @@ Readings (where the paper leaves the procedure open):
   further; the other candidates are leaves.
 * Stop rule: drafting stops after a step whose top-1 probability is below tau (that step's
   candidates are still verified), and after max_depth steps.
+* Node budget (the paper sets none): a tree holds at most max_nodes nodes, root included; a step's
+  fan-out is cut to the nodes left and drafting stops once none are left.
 * Packing: node 0 is the pending token X[p] (the root), then the top-1 chain in depth order, then
   the other candidates by depth and rank. Node i sits at rotary position p + depth(i).
 * Verification: one full-model pass over the packed nodes; node i attends to the committed prefix
@@ -67,13 +69,14 @@ def _ranked(logits):
     return np.lexsort((np.arange(len(z)), -z))
 
 
-def draft_tree(st, tau, max_depth, table=FANOUT, rest=FANOUT_REST):
+def draft_tree(st, tau, max_depth, table=FANOUT, rest=FANOUT_REST, max_nodes=64):
     """Dynamic drafting: decoder-only steps from the pending token (Eq. 5, as in Algorithm 2),
     each expanded into top-p candidates; stops by the confidence threshold tau or at max_depth."""
     m = st.model
     dec = range(m.first_decoder_layer, m.n_layers)
     chain = [st.tokens[-1]]
     steps, p0s, logits = [], [], []
+    nodes = 1
     for i in range(1, max_depth + 1):
         h = m.embed([chain[i - 1]])
         h = run_layers(m, st.cache, dec, h, st.p + i - 1)
@@ -83,12 +86,13 @@ def draft_tree(st, tau, max_depth, table=FANOUT, rest=FANOUT_REST):
         pr /= pr.sum()
         order = _ranked(q)
         p0 = float(pr[order[0]])
-        cands = [int(x) for x in order[:fanout(p0, table, rest)]]
+        cands = [int(x) for x in order[:min(fanout(p0, table, rest), max_nodes - nodes)]]
+        nodes += len(cands)
         steps.append(cands)
         p0s.append(p0)
         logits.append(q)
         chain.append(cands[0])
-        if p0 < tau:
+        if p0 < tau or nodes >= max_nodes:
             break
     tokens, parents, depths, chain_nodes = [chain[0]], [-1], [0], [0]
     for d, cands in enumerate(steps, 1):
@@ -201,14 +205,14 @@ class TreeRound:
 
 
 def generate_tree(model, prompt, tau, max_depth, max_new, table=FANOUT, rest=FANOUT_REST, record=False,
-                  capacity=None):
+                  capacity=None, max_nodes=64):
     """Dynamic drafting with tree verification end to end: returns (new tokens, rounds)."""
     t0 = len(prompt)
-    cap = capacity or (t0 + max_new + max_depth + 2)
+    cap = capacity or (t0 + max_new + max_nodes + 2)
     st = prefill(model, [int(x) for x in prompt], cap)
     rounds = []
     while st.t - t0 < max_new:
-        tree = draft_tree(st, tau, max_depth, table, rest)
+        tree = draft_tree(st, tau, max_depth, table, rest, max_nodes)
         logits, kv = verify_tree(st, tree)
         path, bonus = accept_tree(tree, logits)
         if record:

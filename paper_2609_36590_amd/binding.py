@@ -17,7 +17,7 @@ from . import build as _build
 F32, BF16 = 0, 1
 
 PHASE_VERIFY, PHASE_DRAFT, PHASE_PREFILL = 0, 1, 2
-OP_SETUP, OP_QKV, OP_ATTN, OP_COMBINE, OP_O, OP_GATEUP, OP_DOWN, OP_HEAD, OP_ACCEPT, OP_HEAD_ARGMAX = range(10)
+OP_SETUP, OP_QKV, OP_ATTN, OP_COMBINE, OP_O, OP_GATEUP, OP_DOWN, OP_HEAD, OP_ACCEPT, OP_HEAD_ARGMAX, OP_TOPK = range(11)
 
 
 def kernel_id(phase: int, op: int) -> int:
@@ -48,6 +48,31 @@ class SeedGenOpts(ctypes.Structure):
                 ("use_graph", ctypes.c_int32)]
 
 
+class SeedTreeOpts(ctypes.Structure):
+    _fields_ = [("tau", ctypes.c_float), ("max_depth", ctypes.c_int32), ("n_levels", ctypes.c_int32),
+                ("thr", ctypes.c_float * 4), ("k", ctypes.c_int32 * 4), ("k_rest", ctypes.c_int32),
+                ("max_nodes", ctypes.c_int32)]
+
+
+def tree_opts(max_depth: int, tau: float | None = None, table=None, rest: int | None = None,
+              max_nodes: int | None = None) -> SeedTreeOpts:
+    """The paper's dynamic-drafting options (seed_tree_defaults), with optional overrides; table is
+    a sequence of (threshold, fan-out) pairs."""
+    o = SeedTreeOpts()
+    load_library().seed_tree_defaults(ctypes.byref(o), max_depth)
+    if tau is not None:
+        o.tau = tau
+    if table is not None:
+        o.n_levels = len(table)
+        for j, (thr, k) in enumerate(table):
+            o.thr[j], o.k[j] = thr, k
+    if rest is not None:
+        o.k_rest = rest
+    if max_nodes is not None:
+        o.max_nodes = max_nodes
+    return o
+
+
 class SeedStats(ctypes.Structure):
     _fields_ = [("rounds", ctypes.c_int64), ("drafted", ctypes.c_int64), ("accepted", ctypes.c_int64),
                 ("prefill_ms", ctypes.c_double), ("decode_ms", ctypes.c_double),
@@ -57,7 +82,8 @@ class SeedStats(ctypes.Structure):
 EXPORTS = ("seed_arena_bytes", "seed_create", "seed_load_weights", "seed_prefill", "seed_draft",
            "seed_verify", "seed_rounds", "seed_generate", "seed_get_tokens", "seed_kernel_timing",
            "seed_kernel_timing_read", "seed_last_error", "seed_destroy", "seed_spec_kv_bytes",
-           "seed_spec_forward", "seed_verify_tree")
+           "seed_spec_forward", "seed_verify_tree", "seed_tree_defaults", "seed_draft_tree",
+           "seed_generate_tree")
 
 _LIB = None
 _P = ctypes.c_void_p
@@ -97,6 +123,10 @@ def load_library(path: str | None = None):
         "seed_kernel_timing_read": [_P, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_double)],
         "seed_spec_kv_bytes": [ctypes.POINTER(SeedConfig), ctypes.POINTER(ctypes.c_size_t)],
         "seed_verify_tree": [_P, ctypes.c_int32, _I32P, _I32P, _I32P, _I32P, _I32P, _P],
+        "seed_tree_defaults": [ctypes.POINTER(SeedTreeOpts), ctypes.c_int32],
+        "seed_draft_tree": [_P, ctypes.POINTER(SeedTreeOpts), _I32P, _I32P, _I32P, ctypes.POINTER(ctypes.c_float), _P],
+        "seed_generate_tree": [_P, _I32P, ctypes.c_int32, ctypes.POINTER(SeedTreeOpts), ctypes.c_int32, ctypes.c_int32,
+                               ctypes.c_int32, _I32P, _I32P, ctypes.POINTER(SeedStats)],
         "seed_spec_forward": [_P, ctypes.c_int32, _I32P, ctypes.c_int32, _P, _P, _P, ctypes.POINTER(ctypes.c_double)],
     }
     for name, args in sig.items():
@@ -107,6 +137,7 @@ def load_library(path: str | None = None):
     lib.seed_last_error.restype = ctypes.c_char_p
     lib.seed_destroy.argtypes = [_P]
     lib.seed_destroy.restype = None
+    lib.seed_tree_defaults.restype = None
     if path == lib_path():
         _LIB = lib
     return lib
@@ -257,6 +288,41 @@ def seed_verify_tree(ctx: int, tokens, parents, logits_ptr: int | None = None):
     return [int(x) for x in path[:n_path.value]], bonus.value
 
 
+def seed_draft_tree(ctx: int, opts: SeedTreeOpts, logits_ptr: int | None = None):
+    toks = np.zeros(64, dtype=np.int32)
+    par = np.zeros(64, dtype=np.int32)
+    p0 = np.zeros(opts.max_depth, dtype=np.float32)
+    n = ctypes.c_int32()
+    _check(load_library().seed_draft_tree(ctx, ctypes.byref(opts), toks.ctypes.data_as(_I32P), par.ctypes.data_as(_I32P),
+                                          ctypes.byref(n), p0.ctypes.data_as(ctypes.POINTER(ctypes.c_float)),
+                                          logits_ptr), "seed_draft_tree")
+    k = n.value
+    depth = 0
+    while depth + 1 < k and par[depth + 1] == depth:
+        depth += 1
+    return [int(x) for x in toks[:k]], [int(x) for x in par[:k]], p0[:depth]
+
+
+def seed_generate_tree(ctx: int, prompt, opts: SeedTreeOpts, max_new: int, eos_id: int = -1,
+                       use_graph: bool = False, log_cap: int = 0):
+    toks, tp = _i32(np.asarray(prompt))
+    out = np.zeros(max_new, dtype=np.int32)
+    count = ctypes.c_int32()
+    stats = SeedStats()
+    log = np.full(max(log_cap, 1), -2, dtype=np.int32)
+    if log_cap > 0:
+        stats.n_accept_log = log.ctypes.data_as(_I32P)
+        stats.n_accept_log_cap = log_cap
+    _check(load_library().seed_generate_tree(ctx, tp, len(toks), ctypes.byref(opts), max_new, eos_id, int(use_graph),
+                                             out.ctypes.data_as(_I32P), ctypes.byref(count), ctypes.byref(stats)),
+           "seed_generate_tree")
+    st = {"rounds": stats.rounds, "drafted": stats.drafted, "accepted": stats.accepted,
+          "prefill_ms": stats.prefill_ms, "decode_ms": stats.decode_ms}
+    if log_cap > 0:
+        st["n_accept_log"] = log[:min(stats.rounds, log_cap)]
+    return out[:count.value], st
+
+
 def seed_destroy(ctx: int):
     load_library().seed_destroy(ctx)
 
@@ -322,6 +388,17 @@ class Decoder:
 
     def tokens(self, b: int):
         return seed_get_tokens(self.ctx, b, self.cfg.max_ctx)
+
+    def draft_tree(self, opts: SeedTreeOpts, logits: bool = False):
+        """One round's dynamic drafting: (tokens, parents, p0 per step, logits [steps, vocab] or None)."""
+        lg = self._logits(opts.max_depth) if logits else None
+        toks, par, p0 = seed_draft_tree(self.ctx, opts, lg.data_ptr() if lg is not None else None)
+        return toks, par, p0, (self._host(lg, (opts.max_depth,))[:len(p0)] if logits else None)
+
+    def generate_tree(self, prompt, opts: SeedTreeOpts, max_new: int, **kw):
+        """Dynamic drafting with tree verification for one prompt: (tokens, stats)."""
+        self.B = 1
+        return seed_generate_tree(self.ctx, prompt, opts, max_new, **kw)
 
     def verify_tree(self, tokens, parents, logits: bool = False):
         """Tree-based verification of one packed draft tree: (accepted path nodes, bonus token,

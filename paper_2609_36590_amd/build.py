@@ -16,7 +16,7 @@ LIB_DIR = os.path.join(PKG, "_lib")
 LIB = os.path.join(LIB_DIR, "libseed_rocm.so")
 OBJ_DIR = os.path.join(ROOT, "_build")
 
-SOURCES = ["linear.hip", "attention.hip", "misc.hip", "seed_runtime.cpp"]
+SOURCES = ["linear.hip", "attention.hip", "misc.hip", "tree.hip", "seed_runtime.cpp"]
 
 # -packed-fp32-ops: keep the compiler from forming packed fp32 VALU instructions.
 FLAGS = [

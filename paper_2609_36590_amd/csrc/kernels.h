@@ -178,7 +178,43 @@ void launch_accept(const DevState& st, int B, int k, hipStream_t s);
 // cache position of its depth. out[0] = accepted path length, out[1] = bonus, out[2..] = path.
 void launch_accept_tree(const DevState& st, int n, const int* tree_tok, const int* tree_par, const int* tree_depth,
                         int* out, void* kv, int n_layers, int n_blocks, int n_kv, int head_dim, int esize,
-                        const int* bt, hipStream_t s);
+                        const int* bt, int* hstat, hipStream_t s);
+// Confidence-aware dynamic drafting (Method, Adaptive Drafting with Tree-Based Verification;
+// appendix "Confidence-Aware Dynamic Drafting"): after each drafting step, the top-1 probability
+// p0 of the step's logits and its ranked top candidates; the top-p table gives the fan-out, the
+// threshold tau the stop, and the tree is packed when drafting stops.
+constexpr int TOPK_MAX = 16;        // largest fan-out a table may ask for
+constexpr int TREE_MAX_STEPS = 16;  // drafting steps of one round (max_draft <= 15)
+constexpr int TOPK_PARTS = 256;     // first-stage waves (each covers a contiguous logit chunk)
+
+struct TreeDraftArgs {
+  const float* logits;   // [V] the step's drafter logits
+  int V, chunk;          // chunk: logits per first-stage wave (multiple of 64)
+  int step;              // drafting step i >= 1 (X_draft[i] is being chosen)
+  float* pval;           // first stage: [TOPK_PARTS][TOPK_MAX] candidate logits
+  int* pidx;             //   and token ids (-1 = none)
+  float* pmax;           //   [TOPK_PARTS] chunk maximum
+  float* psum;           //   [TOPK_PARTS] sum of exp(z - chunk maximum)
+  // fan-out rule: k = kk[j] for the first j with p0 > thr[j], else k_rest
+  float tau;
+  int n_levels;
+  float thr[4];
+  int kk[4];
+  int k_rest, k_max;     // k_max: the table's largest fan-out (candidates kept per wave)
+  int max_depth, max_nodes;
+  // the round's drafting state
+  int* cand;             // [TREE_MAX_STEPS][TOPK_MAX] ranked candidates of step i
+  int* kcnt;             // [TREE_MAX_STEPS] fan-out used at step i
+  float* p0;             // [TREE_MAX_STEPS] top-1 probability of step i
+  int* dstate;           // [0] drafting stopped, [1] nodes so far (root included)
+  int* drafts;           // sequence 0's drafts row: [0] the root X[p], [i] the chain token of step i
+  int* tree;             // packed tree: token [64], parent [64], depth [64]; tree[192] = node count
+  const int* rounds;     // rounds run so far: tags the status written when drafting stops
+  int* hstat;            // nullable host-visible status: [0] round tag, [1] nodes, [2] depth
+};
+void launch_tree_topk(const TreeDraftArgs& a, hipStream_t s);
+int tree_topk_chunk(int V);
+
 // nll[r] = logsumexp(logits[r]) - logits[r][target[r]] for r < rows (row stride V)
 void launch_row_nll(const float* logits, int rows, int V, const int* target, float* nll, hipStream_t s);
 // Reduce the head's per-workgroup argmax partials of M rows; row m's token goes to

@@ -141,7 +141,7 @@ __global__ void __launch_bounds__(64) k_accept(DevState st, int B, int k) {
 static constexpr int TREE_MOVE = 2 + 64;
 
 __global__ void __launch_bounds__(64) k_accept_tree(DevState st, int n, const int* tok, const int* par,
-                                                   const int* depth, int* out) {
+                                                   const int* depth, int* out, int* hstat) {
   if (threadIdx.x != 0) return;
   const int s_round = *st.rounds;
   int logv = -1;
@@ -185,6 +185,12 @@ __global__ void __launch_bounds__(64) k_accept_tree(DevState st, int n, const in
   }
   if (s_round < st.log_cap) st.nacc_log[s_round] = logv;
   *st.rounds = s_round + 1;
+  if (hstat) {   // host-visible: the sequence's length and liveness, tagged with the round count
+    hstat[5] = st.t[0];
+    hstat[6] = st.active[0];
+    __threadfence_system();
+    hstat[4] = s_round + 1;
+  }
 }
 
 // Copies the keys/values of cache slot p + leaf to position p + depth(leaf) in every layer, when
@@ -275,8 +281,8 @@ void launch_accept(const DevState& st, int B, int k, hipStream_t s) {
 
 void launch_accept_tree(const DevState& st, int n, const int* tree_tok, const int* tree_par, const int* tree_depth,
                         int* out, void* kv, int n_layers, int n_blocks, int n_kv, int head_dim, int esize,
-                        const int* bt, hipStream_t s) {
-  hipLaunchKernelGGL(k_accept_tree, dim3(1), dim3(64), 0, s, st, n, tree_tok, tree_par, tree_depth, out);
+                        const int* bt, int* hstat, hipStream_t s) {
+  hipLaunchKernelGGL(k_accept_tree, dim3(1), dim3(64), 0, s, st, n, tree_tok, tree_par, tree_depth, out, hstat);
   const int blocks = std::max(1, std::min(256, (n_layers * 2 * n_kv * head_dim + 255) / 256));
   if (esize == 2)
     hipLaunchKernelGGL(k_kv_move<uint16_t>, dim3(blocks), dim3(256), 0, s, tree_depth, (const int*)out,

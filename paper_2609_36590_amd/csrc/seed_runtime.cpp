@@ -58,6 +58,8 @@ struct Plan {
       o_amax_idx, o_vtok;
   size_t o_t, o_len, o_limit, o_active, o_nacc, o_bonus, o_rounds, o_counters, o_drafts, o_tokens,
       o_trace, o_log, o_bt, o_nll, o_splitk, o_splitk_rs, o_tree, o_tree_out, o_scratch, ws_total;
+  // dynamic drafting: top-k partials, the round's drafting state, one step's drafter logits
+  size_t o_topk, o_tdraft, o_dlog;
 };
 
 seed_status validate(const seed_config* c) {
@@ -156,7 +158,7 @@ Plan make_plan(const seed_config& c) {
   p.o_log = take((size_t)p.log_cap * B * 4);
   p.o_bt = take(B * (size_t)p.bt_stride * 4);
   p.o_nll = take((size_t)c.max_ctx * 4);
-  p.o_tree = take(3 * MAX_ROWS * 4);
+  p.o_tree = take((3 * MAX_ROWS + 1) * 4);
   p.o_tree_out = take((2 + MAX_ROWS + 2) * 4);
   {
     // k-range partials of the split-K path (passes of more than 16 rows): KS x rows x N floats
@@ -170,6 +172,9 @@ Plan make_plan(const seed_config& c) {
     p.o_splitk = take(ksn * R * 4);
     p.o_splitk_rs = take(R * 4);
   }
+  p.o_topk = take((size_t)TOPK_PARTS * (2 * TOPK_MAX + 2) * 4);
+  p.o_tdraft = take((size_t)TREE_MAX_STEPS * (TOPK_MAX + 2) * 4 + 16);
+  p.o_dlog = take((size_t)p.V * 4);
   p.o_scratch = take((size_t)std::max({p.V, p.QD + 2 * p.KVD, 2 * p.F, p.H}) * 4);
   p.ws_total = o;
   return p;
@@ -206,8 +211,15 @@ struct seed_ctx {
   std::vector<TimedLaunch> pool;
   int64_t timed_launches = 0;
   double timed_ms = 0.0;
-  // graphs: (B, k, sim_accept) -> exec
-  std::map<std::tuple<int, int, int>, hipGraphExec_t> graphs;
+  // graphs: (B, k, sim_accept, eos) -> exec (the eos id is a kernel argument of the acceptance)
+  std::map<std::tuple<int, int, int, int>, hipGraphExec_t> graphs;
+  // dynamic drafting: step graphs (for the options in tree_key), verification graphs by node
+  // count, and a pinned status the drafting/acceptance kernels write for the host loop
+  std::map<int, hipGraphExec_t> tree_step_graphs;
+  std::map<std::pair<int, int>, hipGraphExec_t> tree_verify_graphs;   // (nodes, eos)
+  seed_tree_opts tree_key{};
+  int* hstat = nullptr;       // host pointer
+  int* hstat_dev = nullptr;   // its device address
 
   template <typename X>
   X* ws(size_t off) { return reinterpret_cast<X*>(WS + off); }
@@ -802,7 +814,7 @@ seed_status run_rounds(seed_ctx* c, int k, int n, bool use_graph) {
     HIPCHK(hipGetLastError());
     return SEED_OK;
   }
-  const auto key = std::make_tuple(c->B, k, c->sim_accept);
+  const auto key = std::make_tuple(c->B, k, c->sim_accept, c->eos);
   auto it = c->graphs.find(key);
   if (it == c->graphs.end()) {
     hipGraph_t g;
@@ -823,25 +835,218 @@ seed_status run_rounds(seed_ctx* c, int k, int n, bool use_graph) {
 // =============================================================================================
 // C ABI
 // =============================================================================================
-// Tree-based verification of one sequence's packed draft tree: node rows through every layer
-// with the tree attention mask, the LM head (logits optional), then tree acceptance, commit and
-// the move of an accepted leaf's cache entries.
+// Tree-based verification of one sequence's packed draft tree (the tree arrays in the workspace):
+// node rows through every layer with the tree attention mask, the LM head (logits optional),
+// then tree acceptance, commit and the move of an accepted leaf's cache entries.
 template <typename T>
-void enqueue_verify_tree(seed_ctx* c, int n, float* logits) {
+void enqueue_verify_tree(seed_ctx* c, int n, float* logits, bool cap) {
   const Plan& p = c->p;
   SetupArgs s = setup_base(c, 0);
   s.mode = SETUP_TREE; s.M = n; s.R = n;
   s.tree_tok = c->ws<int>(p.o_tree);
   s.tree_depth = c->ws<int>(p.o_tree) + 2 * MAX_ROWS;
-  timed(c, SEED_PHASE_VERIFY, SEED_OP_SETUP, false, [&](const LaunchEvents*) { launch_setup<T>(s, c->s); });
-  run_layers<T>(c, n, 1, n, 0, p.L, SEED_PHASE_VERIFY, nullptr, false, nullptr, true);
-  run_head<T>(c, n, c->ws<int>(p.o_vtok), 1, logits, (long long)p.V, SEED_PHASE_VERIFY, false);
+  timed(c, SEED_PHASE_VERIFY, SEED_OP_SETUP, cap, [&](const LaunchEvents*) { launch_setup<T>(s, c->s); });
+  run_layers<T>(c, n, 1, n, 0, p.L, SEED_PHASE_VERIFY, nullptr, cap, nullptr, true);
+  run_head<T>(c, n, c->ws<int>(p.o_vtok), 1, logits, (long long)p.V, SEED_PHASE_VERIFY, cap);
   DevState st = dev_state(c);
-  timed(c, SEED_PHASE_VERIFY, SEED_OP_ACCEPT, false, [&](const LaunchEvents*) {
+  timed(c, SEED_PHASE_VERIFY, SEED_OP_ACCEPT, cap, [&](const LaunchEvents*) {
     launch_accept_tree(st, n, c->ws<int>(p.o_tree), c->ws<int>(p.o_tree) + MAX_ROWS, c->ws<int>(p.o_tree) + 2 * MAX_ROWS,
                        c->ws<int>(p.o_tree_out), c->KV, p.L, p.n_blocks, p.NKV, p.HD, p.esize, c->ws<int>(p.o_bt),
-                       c->s);
+                       c->hstat_dev, c->s);
   });
+}
+
+seed_status check_tree_opts(const seed_ctx* c, const seed_tree_opts* o) {
+  const Plan& p = c->p;
+  if (!o) return fail(SEED_ERR_ARG, "tree options must not be NULL");
+  if (o->max_depth < 1 || o->max_depth > p.cfg.max_draft)
+    return fail(SEED_ERR_ARG, "max_depth must be in [1, max_draft]");
+  if (o->max_nodes < o->max_depth + 1 || o->max_nodes > MAX_ROWS)
+    return fail(SEED_ERR_ARG, "max_nodes must be in [max_depth + 1, 64]");
+  if (o->n_levels < 0 || o->n_levels > 4) return fail(SEED_ERR_ARG, "n_levels must be in [0, 4]");
+  for (int j = 0; j < o->n_levels; ++j) {
+    if (o->k[j] < 1 || o->k[j] > TOPK_MAX) return fail(SEED_ERR_ARG, "every fan-out must be in [1, 16]");
+    if (j > 0 && !(o->thr[j] < o->thr[j - 1])) return fail(SEED_ERR_ARG, "thresholds must decrease");
+  }
+  if (o->k_rest < 1 || o->k_rest > TOPK_MAX) return fail(SEED_ERR_ARG, "k_rest must be in [1, 16]");
+  if (!(o->tau >= 0.f && o->tau <= 1.f)) return fail(SEED_ERR_ARG, "tau must be in [0, 1]");
+  if (c->B != 1) return fail(SEED_ERR_UNSUPPORTED, "dynamic drafting runs one sequence (B = 1)");
+  if (p.V < TOPK_MAX || p.V > TOPK_PARTS * 64 * 16)
+    return fail(SEED_ERR_UNSUPPORTED, "dynamic drafting needs 16 <= vocab <= 262144");
+  return SEED_OK;
+}
+
+TreeDraftArgs tree_args(seed_ctx* c, const seed_tree_opts& o, int step, const float* logits) {
+  const Plan& p = c->p;
+  TreeDraftArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.logits = logits;
+  a.V = p.V;
+  a.chunk = tree_topk_chunk(p.V);
+  a.step = step;
+  float* tk = c->ws<float>(p.o_topk);
+  a.pval = tk;
+  a.pidx = reinterpret_cast<int*>(tk + TOPK_PARTS * TOPK_MAX);
+  a.pmax = tk + 2 * TOPK_PARTS * TOPK_MAX;
+  a.psum = a.pmax + TOPK_PARTS;
+  a.tau = o.tau;
+  a.n_levels = o.n_levels;
+  a.k_rest = a.k_max = o.k_rest;
+  for (int j = 0; j < o.n_levels; ++j) {
+    a.thr[j] = o.thr[j];
+    a.kk[j] = o.k[j];
+    a.k_max = std::max(a.k_max, o.k[j]);
+  }
+  a.max_depth = o.max_depth;
+  a.max_nodes = o.max_nodes;
+  int* td = c->ws<int>(p.o_tdraft);
+  a.cand = td;
+  a.kcnt = td + TREE_MAX_STEPS * TOPK_MAX;
+  a.p0 = reinterpret_cast<float*>(a.kcnt + TREE_MAX_STEPS);
+  a.dstate = a.kcnt + 2 * TREE_MAX_STEPS;
+  a.drafts = c->ws<int>(p.o_drafts);
+  a.tree = c->ws<int>(p.o_tree);
+  a.rounds = c->ws<int>(p.o_rounds);
+  a.hstat = c->hstat_dev;
+  return a;
+}
+
+// Drafting step i of dynamic drafting: the decoder-only step of Algorithm 2 (Eq. 5) from the
+// chain token X_draft[i-1], its logits, then the top-1 probability, fan-out, candidates and stop.
+template <typename T>
+void enqueue_tree_step(seed_ctx* c, const seed_tree_opts& o, int step, float* logits, bool cap) {
+  const Plan& p = c->p;
+  SetupArgs s = setup_base(c, p.LD);
+  s.mode = SETUP_DRAFT; s.M = 1; s.R = 1; s.step = step;
+  timed(c, SEED_PHASE_DRAFT, SEED_OP_SETUP, cap, [&](const LaunchEvents*) { launch_setup<T>(s, c->s); });
+  run_layers<T>(c, 1, 1, 1, p.LD, p.L, SEED_PHASE_DRAFT, nullptr, cap);
+  run_head<T>(c, 1, c->ws<int>(p.o_drafts) + step, p.dstride, logits, (long long)p.V, SEED_PHASE_DRAFT, cap);
+  const TreeDraftArgs a = tree_args(c, o, step, logits);
+  timed(c, SEED_PHASE_DRAFT, SEED_OP_TOPK, cap, [&](const LaunchEvents*) { launch_tree_topk(a, c->s); });
+}
+
+template <typename F>
+seed_status capture_graph(seed_ctx* c, F&& fn, hipGraphExec_t* ex) {
+  hipGraph_t g;
+  HIPCHK(hipStreamBeginCapture(c->s, hipStreamCaptureModeThreadLocal));
+  fn();
+  HIPCHK(hipStreamEndCapture(c->s, &g));
+  HIPCHK(hipGraphInstantiate(ex, g, nullptr, nullptr, 0));
+  HIPCHK(hipGraphDestroy(g));
+  return SEED_OK;
+}
+
+template <typename T>
+seed_status launch_tree_step(seed_ctx* c, const seed_tree_opts& o, int step, bool use_graph) {
+  float* lg = c->ws<float>(c->p.o_dlog);
+  if (!use_graph) {
+    enqueue_tree_step<T>(c, o, step, lg, false);
+    HIPCHK(hipGetLastError());
+    return SEED_OK;
+  }
+  if (std::memcmp(&c->tree_key, &o, sizeof(o)) != 0) {
+    for (auto& kv : c->tree_step_graphs) HIPCHK(hipGraphExecDestroy(kv.second));
+    c->tree_step_graphs.clear();
+    c->tree_key = o;
+  }
+  auto it = c->tree_step_graphs.find(step);
+  if (it == c->tree_step_graphs.end()) {
+    hipGraphExec_t ex;
+    seed_status st = capture_graph(c, [&] { enqueue_tree_step<T>(c, o, step, lg, true); }, &ex);
+    if (st != SEED_OK) return st;
+    it = c->tree_step_graphs.emplace(step, ex).first;
+  }
+  HIPCHK(hipGraphLaunch(it->second, c->s));
+  return SEED_OK;
+}
+
+template <typename T>
+seed_status launch_tree_verify(seed_ctx* c, int n, bool use_graph) {
+  if (!use_graph) {
+    enqueue_verify_tree<T>(c, n, nullptr, false);
+    HIPCHK(hipGetLastError());
+    return SEED_OK;
+  }
+  auto it = c->tree_verify_graphs.find({n, c->eos});
+  if (it == c->tree_verify_graphs.end()) {
+    hipGraphExec_t ex;
+    seed_status st = capture_graph(c, [&] { enqueue_verify_tree<T>(c, n, nullptr, true); }, &ex);
+    if (st != SEED_OK) return st;
+    it = c->tree_verify_graphs.emplace(std::make_pair(n, c->eos), ex).first;
+  }
+  HIPCHK(hipGraphLaunch(it->second, c->s));
+  return SEED_OK;
+}
+
+// Busy-wait for an event (the host reacts within microseconds; the stream keeps running the
+// work queued behind it).
+seed_status spin_event(hipEvent_t e) {
+  for (;;) {
+    const hipError_t r = hipEventQuery(e);
+    if (r == hipSuccess) return SEED_OK;
+    if (r != hipErrorNotReady) return fail(SEED_ERR_HIP, std::string("hipEventQuery: ") + hipGetErrorString(r));
+  }
+}
+
+int read_host_int(const int* p) { return __atomic_load_n(p, __ATOMIC_ACQUIRE); }
+
+// Dynamic drafting + tree verification rounds of the single sequence until it is no longer live.
+// Pipelined: drafting step i+1 is queued before the host learns whether step i stopped (a stopped
+// round turns it into a no-op after its decoder pass), and the next round's first step before the
+// host learns whether this round finished the sequence; the host reads the kernels' pinned status
+// after each event, so the GPU never waits for it.
+template <typename T>
+seed_status tree_rounds(seed_ctx* c, const seed_tree_opts& o, bool use_graph, int round0, int* rounds_run) {
+  std::vector<hipEvent_t> ev(TREE_MAX_STEPS + 2, nullptr);
+  seed_status st = SEED_OK;
+  for (auto& e : ev)
+    if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) st = fail(SEED_ERR_HIP, "hipEventCreate failed");
+  auto done = [&](seed_status r) {
+    for (auto& e : ev)
+      if (e) hipEventDestroy(e);
+    return r;
+  };
+  if (st != SEED_OK) return done(st);
+  const int D = o.max_depth;
+  hipEvent_t ev_v = ev[TREE_MAX_STEPS + 1];
+  int r = round0;
+  c->hstat[0] = c->hstat[4] = -1;
+  st = launch_tree_step<T>(c, o, 1, use_graph);
+  if (st != SEED_OK) return done(st);
+  if (hipEventRecord(ev[1], c->s) != hipSuccess) return done(fail(SEED_ERR_HIP, "hipEventRecord failed"));
+  for (;;) {
+    int n = -1;
+    for (int i = 1;; ++i) {
+      if (i < D) {
+        st = launch_tree_step<T>(c, o, i + 1, use_graph);
+        if (st != SEED_OK) return done(st);
+        if (hipEventRecord(ev[i + 1], c->s) != hipSuccess) return done(fail(SEED_ERR_HIP, "hipEventRecord failed"));
+      }
+      st = spin_event(ev[i]);
+      if (st != SEED_OK) return done(st);
+      if (read_host_int(c->hstat) == r) {
+        n = read_host_int(c->hstat + 1);
+        break;
+      }
+      if (i >= D) return done(fail(SEED_ERR_HIP, "drafting did not stop at max_depth"));
+    }
+    if (n < 1 || n > o.max_nodes) return done(fail(SEED_ERR_HIP, "drafted tree size out of range"));
+    st = launch_tree_verify<T>(c, n, use_graph);
+    if (st != SEED_OK) return done(st);
+    if (hipEventRecord(ev_v, c->s) != hipSuccess) return done(fail(SEED_ERR_HIP, "hipEventRecord failed"));
+    st = launch_tree_step<T>(c, o, 1, use_graph);   // the next round's first step
+    if (st != SEED_OK) return done(st);
+    if (hipEventRecord(ev[1], c->s) != hipSuccess) return done(fail(SEED_ERR_HIP, "hipEventRecord failed"));
+    st = spin_event(ev_v);
+    if (st != SEED_OK) return done(st);
+    ++r;
+    if (read_host_int(c->hstat + 4) != r) return done(fail(SEED_ERR_HIP, "tree acceptance status missing"));
+    if (!read_host_int(c->hstat + 6)) break;
+  }
+  // let the speculative first step of the round that will not run finish
+  if (hipStreamSynchronize(c->s) != hipSuccess) return done(fail(SEED_ERR_HIP, "hipStreamSynchronize failed"));
+  *rounds_run = r - round0;
+  return done(SEED_OK);
 }
 
 extern "C" {
@@ -895,7 +1100,10 @@ seed_status seed_create(const seed_config* cfg, void* hip_stream, void* weight_a
   hipError_t e = hipMemcpyAsync(c->wf(p.w_rope_cos), cs.data(), cs.size() * 4, hipMemcpyHostToDevice, c->s);
   if (e == hipSuccess) e = hipMemcpyAsync(c->wf(p.w_rope_sin), sn.data(), sn.size() * 4, hipMemcpyHostToDevice, c->s);
   if (e == hipSuccess) e = hipStreamSynchronize(c->s);
+  if (e == hipSuccess) e = hipHostMalloc((void**)&c->hstat, 256, hipHostMallocCoherent);
+  if (e == hipSuccess) e = hipHostGetDevicePointer((void**)&c->hstat_dev, c->hstat, 0);
   if (e != hipSuccess) {
+    if (c->hstat) hipHostFree(c->hstat);
     delete c;
     return fail(SEED_ERR_HIP, std::string("seed_create: ") + hipGetErrorString(e));
   }
@@ -1168,8 +1376,8 @@ seed_status seed_verify_tree(seed_ctx* c, int32_t n, const int32_t* tokens, cons
   st = ensure_blocks(c, 0, c->t_upper[0] + n + 1);
   if (st != SEED_OK) return st;
   HIPCHK(hipMemcpyAsync(c->ws<int>(p.o_tree), host.data(), host.size() * 4, hipMemcpyHostToDevice, c->s));
-  if (p.cfg.dtype == SEED_BF16) enqueue_verify_tree<uint16_t>(c, n, logits);
-  else enqueue_verify_tree<float>(c, n, logits);
+  if (p.cfg.dtype == SEED_BF16) enqueue_verify_tree<uint16_t>(c, n, logits, false);
+  else enqueue_verify_tree<float>(c, n, logits, false);
   HIPCHK(hipGetLastError());
   std::vector<int> out(2 + MAX_ROWS);
   HIPCHK(hipMemcpyAsync(out.data(), c->ws<int>(p.o_tree_out), out.size() * 4, hipMemcpyDeviceToHost, c->s));
@@ -1178,6 +1386,131 @@ seed_status seed_verify_tree(seed_ctx* c, int32_t n, const int32_t* tokens, cons
   if (path_len) *path_len = out[0];
   if (bonus) *bonus = out[1];
   if (path) std::copy(out.begin() + 2, out.begin() + 2 + out[0], path);
+  c->drafts_k = -1;
+  return SEED_OK;
+}
+
+void seed_tree_defaults(seed_tree_opts* o, int32_t max_depth) {
+  if (!o) return;
+  std::memset(o, 0, sizeof(*o));
+  o->tau = 0.7f;
+  o->max_depth = max_depth;
+  o->n_levels = 3;
+  o->thr[0] = 0.95f; o->thr[1] = 0.8f; o->thr[2] = 0.5f;
+  o->k[0] = 1; o->k[1] = 3; o->k[2] = 5;
+  o->k_rest = 10;
+  o->max_nodes = MAX_ROWS;
+}
+
+seed_status seed_draft_tree(seed_ctx* c, const seed_tree_opts* opts, int32_t* tokens, int32_t* parents,
+                            int32_t* n_nodes, float* p0, float* logits) {
+  seed_status st = check_ready(c);
+  if (st != SEED_OK) return st;
+  if (!c->prefilled) return fail(SEED_ERR_STATE, "call seed_prefill first");
+  st = check_tree_opts(c, opts);
+  if (st != SEED_OK) return st;
+  if (!tokens || !parents || !n_nodes) return fail(SEED_ERR_ARG, "tokens, parents and n_nodes must not be NULL");
+  const Plan& p = c->p;
+  const seed_tree_opts o = *opts;
+  if ((int64_t)c->t_upper[0] + o.max_nodes + 1 > p.cfg.max_ctx) return fail(SEED_ERR_CAPACITY, "the tree would pass max_ctx");
+  st = ensure_blocks(c, 0, c->t_upper[0] + o.max_nodes + 1);
+  if (st != SEED_OK) return st;
+  int depth = 0;
+  for (int i = 1; i <= o.max_depth; ++i) {
+    float* lg = logits ? logits + (size_t)(i - 1) * p.V : c->ws<float>(p.o_dlog);
+    if (p.cfg.dtype == SEED_BF16) enqueue_tree_step<uint16_t>(c, o, i, lg, false);
+    else enqueue_tree_step<float>(c, o, i, lg, false);
+    HIPCHK(hipGetLastError());
+    int stopped = 0;
+    HIPCHK(hipMemcpyAsync(&stopped, c->ws<int>(p.o_tdraft) + TREE_MAX_STEPS * (TOPK_MAX + 2), 4, hipMemcpyDeviceToHost, c->s));
+    HIPCHK(hipStreamSynchronize(c->s));
+    depth = i;
+    if (stopped) break;
+  }
+  std::vector<int> tree(3 * MAX_ROWS + 1);
+  std::vector<float> pr(TREE_MAX_STEPS);
+  HIPCHK(hipMemcpyAsync(tree.data(), c->ws<int>(p.o_tree), tree.size() * 4, hipMemcpyDeviceToHost, c->s));
+  HIPCHK(hipMemcpyAsync(pr.data(), c->ws<int>(p.o_tdraft) + TREE_MAX_STEPS * (TOPK_MAX + 1), TREE_MAX_STEPS * 4,
+                        hipMemcpyDeviceToHost, c->s));
+  HIPCHK(hipStreamSynchronize(c->s));
+  const int n = tree[3 * MAX_ROWS];
+  if (n < depth + 1 || n > o.max_nodes) return fail(SEED_ERR_HIP, "drafted tree size out of range");
+  *n_nodes = n;
+  std::copy(tree.begin(), tree.begin() + n, tokens);
+  std::copy(tree.begin() + MAX_ROWS, tree.begin() + MAX_ROWS + n, parents);
+  if (p0) std::copy(pr.begin() + 1, pr.begin() + 1 + depth, p0);
+  c->drafts_k = -1;
+  return SEED_OK;
+}
+
+seed_status seed_generate_tree(seed_ctx* c, const int32_t* tokens, int32_t len, const seed_tree_opts* opts,
+                               int32_t max_new, int32_t eos_id, int32_t use_graph, int32_t* out, int32_t* count,
+                               seed_stats* stats) {
+  seed_status st = check_ready(c);
+  if (st != SEED_OK) return st;
+  if (!opts || !out || !count) return fail(SEED_ERR_ARG, "opts, out and count must not be NULL");
+  const Plan& p = c->p;
+  if (max_new < 1) return fail(SEED_ERR_ARG, "max_new must be >= 1");
+  if (eos_id < -1 || eos_id >= p.V) return fail(SEED_ERR_ARG, "eos_id out of range");
+  if (opts->max_nodes < 2 || opts->max_nodes > MAX_ROWS) return fail(SEED_ERR_ARG, "max_nodes must be in [2, 64]");
+  std::vector<int> packed;
+  // a finished sequence may still draft one more round's first step: room for two trees
+  const int extra = max_new + 2 * (opts->max_nodes + 1);
+  st = check_prompts(c, 1, tokens, &len, extra, packed);
+  if (st != SEED_OK) return st;
+  st = start_sequences(c, 1, &len, extra);
+  if (st != SEED_OK) return st;
+  st = check_tree_opts(c, opts);
+  if (st != SEED_OK) return st;
+  c->eos = eos_id;
+  c->sim_accept = -1;
+  hipEvent_t e0, e1, e2;
+  HIPCHK(hipEventCreate(&e0));
+  HIPCHK(hipEventCreate(&e1));
+  HIPCHK(hipEventCreate(&e2));
+  HIPCHK(hipEventRecord(e0, c->s));
+  st = p.cfg.dtype == SEED_BF16 ? do_prefill<uint16_t>(c, packed) : do_prefill<float>(c, packed);
+  if (st != SEED_OK) return st;
+  c->prefilled = true;
+  const int limit = len + max_new;
+  HIPCHK(hipMemcpyAsync(c->ws<int>(p.o_limit), &limit, 4, hipMemcpyHostToDevice, c->s));
+  HIPCHK(hipEventRecord(e1, c->s));
+  HIPCHK(hipStreamSynchronize(c->s));
+  int rounds_run = 0;
+  st = p.cfg.dtype == SEED_BF16 ? tree_rounds<uint16_t>(c, *opts, use_graph != 0, 0, &rounds_run)
+                                : tree_rounds<float>(c, *opts, use_graph != 0, 0, &rounds_run);
+  if (st != SEED_OK) return st;
+  HIPCHK(hipEventRecord(e2, c->s));
+  HIPCHK(hipEventSynchronize(e2));
+  std::vector<int> tok(p.tstride);
+  int t = 0;
+  HIPCHK(hipMemcpy(tok.data(), c->ws<int>(p.o_tokens), tok.size() * 4, hipMemcpyDeviceToHost));
+  HIPCHK(hipMemcpy(&t, c->ws<int>(p.o_t), 4, hipMemcpyDeviceToHost));
+  c->t_upper.assign(1, t);
+  const int n = std::min(t - len, max_new);
+  *count = n;
+  for (int i = 0; i < max_new; ++i) out[i] = i < n ? tok[len + i] : -1;
+  if (stats) {
+    int rounds = 0;
+    long long cnt[2];
+    HIPCHK(hipMemcpy(&rounds, c->ws<int>(p.o_rounds), 4, hipMemcpyDeviceToHost));
+    HIPCHK(hipMemcpy(cnt, c->ws<long long>(p.o_counters), 16, hipMemcpyDeviceToHost));
+    stats->rounds = rounds;
+    stats->drafted = cnt[0];
+    stats->accepted = cnt[1];
+    float ms1 = 0.f, ms2 = 0.f;
+    HIPCHK(hipEventElapsedTime(&ms1, e0, e1));
+    HIPCHK(hipEventElapsedTime(&ms2, e1, e2));
+    stats->prefill_ms = ms1;
+    stats->decode_ms = ms2;
+    if (stats->n_accept_log && stats->n_accept_log_cap > 0) {
+      const int64_t rows = std::min<int64_t>({(int64_t)rounds, stats->n_accept_log_cap, (int64_t)p.log_cap});
+      HIPCHK(hipMemcpy(stats->n_accept_log, c->ws<int>(p.o_log), rows * 4, hipMemcpyDeviceToHost));
+    }
+  }
+  hipEventDestroy(e0);
+  hipEventDestroy(e1);
+  hipEventDestroy(e2);
   c->drafts_k = -1;
   return SEED_OK;
 }
@@ -1264,6 +1597,9 @@ void seed_destroy(seed_ctx* c) {
   if (!c) return;
   hipStreamSynchronize(c->s);
   for (auto& kv : c->graphs) hipGraphExecDestroy(kv.second);
+  for (auto& kv : c->tree_step_graphs) hipGraphExecDestroy(kv.second);
+  for (auto& kv : c->tree_verify_graphs) hipGraphExecDestroy(kv.second);
+  if (c->hstat) hipHostFree(c->hstat);
   for (auto& t : c->pending) { hipEventDestroy(t.a); hipEventDestroy(t.b); }
   for (auto& t : c->pool) { hipEventDestroy(t.a); hipEventDestroy(t.b); }
   delete c;

@@ -13,6 +13,7 @@ import numpy as np
 import pytest
 
 from gpu_common import decoder, oracle_model, say, top2_gap
+from oracle import model as om
 from oracle import seed as os_
 from oracle import tree as ot
 from paper_2609_36590_amd import binding, synth
@@ -109,5 +110,159 @@ def test_tree_argument_errors():
             with pytest.raises(binding.SeedError):
                 dec.verify_tree(toks, par)
         assert len(dec.tokens(0)) == t0
+    finally:
+        dec.close()
+
+
+# ---------------------------------------------------------------------------------------------
+# dynamic drafting (Confidence-Aware Dynamic Drafting) and the end-to-end tree decoding loop
+# ---------------------------------------------------------------------------------------------
+THRESHOLDS = tuple(t for t, _ in ot.FANOUT)
+GAIN = 20.0   # sharpened logits are GAIN times larger, and so are their absolute errors
+
+
+def _sharp_weights(cfg, gain=GAIN, enc=0.3, std=0.05, seed=0):
+    """Random weights whose final-norm gain sharpens the softmax, so that the top-1 probabilities
+    spread over every level of the top-p table."""
+    w = synth.make_weights(cfg, seed=seed, std=std, enc_out_scale=enc)
+    g = np.full(w["final_norm"].shape, gain, dtype=np.float32)
+    w["final_norm"] = synth.f32_to_bf16_bits(g) if cfg.dtype == synth.BF16 else g
+    return w
+
+
+def _step_ambiguous(logits, p0, k, tau, tol, order=True):
+    """Could logits within tol of these change the step's decisions: fan-out, stop, the top-1
+    token, which tokens are candidates and (order=True) their ranking?"""
+    if min(abs(p0 - x) for x in THRESHOLDS + (tau,)) <= 4 * tol:
+        return True
+    top = np.sort(np.asarray(logits, dtype=np.float64))[::-1][:k + 1]
+    gaps = -np.diff(top)
+    if order:
+        return bool(np.any(gaps <= 2 * tol))
+    return bool(gaps[0] <= 2 * tol or gaps[k - 1] <= 2 * tol)
+
+
+def _tree_ambiguous(tree, tau, tol, order=True):
+    return any(_step_ambiguous(tree.draft_logits[i], tree.p0[i], ot.fanout(tree.p0[i]), tau, tol, order)
+               for i in range(len(tree.p0)))
+
+
+@pytest.mark.parametrize("cfg,tol,tau,depth", [
+    (synth.C1_TINY, 1e-4, 0.0, 6), (synth.C1_TINY, 1e-4, 0.7, 8), (TINY_BF16, 2e-2, 0.5, 6),
+], ids=["f32-tau0-d6", "f32-tau0.7-d8", "bf16-tau0.5-d6"])
+def test_drafting_matches_oracle(cfg, tol, tau, depth):
+    """Teacher-forced rounds: the GPU drafts from the same committed state as the oracle (both
+    then verify the oracle's tree); drafter logits, p0 and, where no decision is within the
+    tolerance of a boundary, the packed tree must match."""
+    tol = tol * GAIN
+    w = _sharp_weights(cfg)
+    prompt = synth.make_prompts(cfg)[0]
+    m = oracle_model(cfg, w)
+    n_rounds = 10
+    cap = len(prompt) + n_rounds * (depth + 1) + 70
+    st = os_.prefill(m, [int(x) for x in prompt], cap)
+    dec = decoder(cfg, w, max_batch=1, max_ctx=cap, max_draft=depth)
+    opts = binding.tree_opts(depth, tau=tau)
+    try:
+        dec.prefill([prompt])
+        same_trees, levels, worst = 0, set(), 0.0
+        for r in range(n_rounds):
+            tree = ot.draft_tree(st, tau, depth)
+            toks, par, p0, lg = dec.draft_tree(opts, logits=True)
+            say(f"[gpu] round {r}: oracle {len(tree.tokens)} nodes / {len(tree.p0)} steps, "
+                f"GPU {len(toks)} nodes / {len(p0)} steps")
+            # drafter logits of the steps fed the same chain tokens
+            same = 1
+            while (same < min(len(p0), len(tree.p0)) and toks[same] == tree.tokens[same]):
+                same += 1
+            worst = max(worst, float(np.abs(lg[:same] - tree.draft_logits[:same]).max()))
+            np.testing.assert_allclose(p0[:same], tree.p0[:same], rtol=4 * tol, atol=1e-7)
+            if not _tree_ambiguous(tree, tau, tol):
+                assert toks == tree.tokens and par == tree.parents, r
+                same_trees += 1
+                levels |= {ot.fanout(x) for x in tree.p0}
+            # both sides verify the oracle's tree
+            logits, kv = ot.verify_tree(st, tree)
+            path, bonus = ot.accept_tree(tree, logits)
+            ot.commit_tree(st, tree, kv, path, bonus)
+            dec.verify_tree(tree.tokens, tree.parents)
+        say(f"[gpu] {same_trees}/{n_rounds} trees compared, fan-outs {sorted(levels)}, max |logits - oracle| = {worst:.3g}")
+        assert worst <= tol
+        if cfg.dtype == synth.F32:   # bf16's tolerance leaves few decisions unambiguous
+            assert same_trees >= n_rounds // 2 and len(levels) >= 3
+    finally:
+        dec.close()
+
+
+def _oracle_ok_prefix(m, prompt, toks, tol):
+    """Length of the greedy continuation whose every choice has a top-2 gap above 2 tol."""
+    lg = om.full_forward(m, list(prompt) + [int(x) for x in toks])[len(prompt) - 1:-1]
+    amb = np.nonzero(top2_gap(lg) <= 2 * tol)[0]
+    return int(amb[0]) if len(amb) else len(toks)
+
+
+@pytest.mark.parametrize("cfg,tol,tau,depth,graph", [
+    (synth.C1_TINY, 1e-4, 0.7, 8, False), (synth.C1_TINY, 1e-4, 0.7, 8, True),
+    (synth.C1_TINY, 1e-4, 0.0, 5, True), (TINY_BF16, 2e-2, 0.5, 6, True),
+], ids=["f32-tau0.7-eager", "f32-tau0.7-graph", "f32-tau0-graph", "bf16-tau0.5-graph"])
+def test_generate_tree_is_lossless(cfg, tol, tau, depth, graph):
+    """End to end: the committed tokens are the GPU's plain greedy decode (up to the first near
+    tie of the oracle's greedy logits), and each round's accepted path length equals the oracle's
+    tree decoding while no decision is ambiguous."""
+    tol = tol * GAIN
+    w = _sharp_weights(cfg, enc=0.05)
+    prompt = synth.make_prompts(cfg)[0]
+    m = oracle_model(cfg, w)
+    max_new = 64
+    dec = decoder(cfg, w, max_batch=1, max_ctx=len(prompt) + max_new + 2 * 65 + 8, max_draft=depth)
+    try:
+        ref, _, _ = dec.generate([prompt], 0, max_new)
+        opts = binding.tree_opts(depth, tau=tau)
+        toks, st = dec.generate_tree(prompt, opts, max_new, use_graph=graph, log_cap=256)
+        n_ok = _oracle_ok_prefix(m, prompt, ref[0], tol)
+        say(f"[gpu] {st['rounds']} rounds, {st['accepted']} accepted of {st['drafted']} drafted nodes, "
+            f"{n_ok} unambiguous tokens")
+        assert len(toks) == max_new
+        np.testing.assert_array_equal(toks[:n_ok], ref[0][:n_ok])
+        assert st["accepted"] > 0
+        # the oracle's rounds, compared while every draft and verification decision is clear
+        _, rounds = ot.generate_tree(m, prompt, tau, depth, max_new, record=True)
+        log = st["n_accept_log"]
+        compared, t_gpu, t_or = 0, 0, 0
+        for i, rd in enumerate(rounds):
+            if i >= len(log) or t_gpu != t_or:   # both sides must start the round at the same position
+                break
+            visited = [0] + list(rd.path)   # the nodes whose argmax the acceptance reads
+            if not (_tree_ambiguous(rd.tree, tau, tol, order=False)
+                    or np.any(top2_gap(rd.verify_logits[visited]) <= 2 * tol)):
+                assert log[i] == len(rd.path), (i, list(log[:i + 1]), [len(x.path) for x in rounds[:i + 1]])
+                compared += 1
+            t_gpu += int(log[i]) + 1
+            t_or += len(rd.path) + 1
+        say(f"[gpu] {compared} rounds match the oracle's accepted lengths")
+        if cfg.dtype == synth.F32:   # bf16's tolerance leaves few decisions unambiguous
+            assert compared >= 3
+    finally:
+        dec.close()
+
+
+def test_generate_tree_eos_and_short_runs():
+    cfg = synth.C1_TINY
+    w = _sharp_weights(cfg, enc=0.05)
+    prompt = synth.make_prompts(cfg)[0]
+    dec = decoder(cfg, w, max_batch=1, max_ctx=len(prompt) + 40 + 2 * 65 + 8, max_draft=6)
+    try:
+        ref, _, _ = dec.generate([prompt], 0, 40)
+        opts = binding.tree_opts(6, tau=0.5)
+        one, st = dec.generate_tree(prompt, opts, 1, use_graph=True)
+        np.testing.assert_array_equal(one, ref[0][:1])
+        eos = int(ref[0][17])
+        first = int(np.nonzero(ref[0] == eos)[0][0])
+        toks, st = dec.generate_tree(prompt, opts, 40, eos_id=eos, use_graph=True)
+        np.testing.assert_array_equal(toks, ref[0][:first + 1])
+        with pytest.raises(binding.SeedError):
+            dec.generate_tree(prompt, binding.tree_opts(7), 8)        # max_depth > max_draft
+        with pytest.raises(binding.SeedError):
+            dec.generate_tree(prompt, binding.tree_opts(4, table=((0.5, 1), (0.6, 3))), 8)   # increasing
     finally:
         dec.close()
