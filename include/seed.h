@@ -269,16 +269,18 @@ seed_status seed_draft_tree(seed_ctx* ctx, const seed_tree_opts* opts, int32_t* 
 /*
  * Dynamic drafting with tree-based verification end to end for one prompt (the decoding mode of
  * the paper's main experiments): prefill, then rounds of seed_draft_tree + seed_verify_tree until
- * max_new tokens (or eos_id) are committed. Lossless: every committed token is the verifier's
- * greedy choice. out: host [max_new] (-1 past count); count: host. use_graph: 1 replays each
- * drafting step and each tree size's verification from captured HIP graphs. stats: nullable;
- * drafted counts tree nodes other than the root, n_accept_log the accepted path length per round.
- * Errors as seed_generate and seed_draft_tree; the prompt needs len + max_new + 2 (max_nodes + 1)
- * <= max_ctx.
+ * opts->max_new tokens (or opts->eos_id) are committed. Lossless: every committed token is the
+ * verifier's greedy choice. opts: as for seed_generate, except that k is not used and
+ * sim_accept (0..max_depth) replaces chain nodes 1..sim_accept of every drafted tree with the
+ * forced trace and the next chain node with another token (a benchmark of acceptance lengths
+ * that random weights do not reach); use_graph replays each drafting step and each tree size's
+ * verification from captured HIP graphs. out: host [max_new] (-1 past count); count: host.
+ * stats: nullable; drafted counts tree nodes other than the root, n_accept_log the accepted path
+ * length per round. Errors as seed_generate and seed_draft_tree; the prompt needs
+ * len + max_new + 2 (max_nodes + 1) <= max_ctx.
  */
-seed_status seed_generate_tree(seed_ctx* ctx, const int32_t* tokens, int32_t len, const seed_tree_opts* opts,
-                               int32_t max_new, int32_t eos_id, int32_t use_graph, int32_t* out, int32_t* count,
-                               seed_stats* stats);
+seed_status seed_generate_tree(seed_ctx* ctx, const int32_t* tokens, int32_t len, const seed_tree_opts* topts,
+                               const seed_gen_opts* opts, int32_t* out, int32_t* count, seed_stats* stats);
 
 /*
  * Forward pass of the speculative drafting objective L_spec (Algorithm 1, Sec. 3.2, Fig. 2 right)

@@ -125,8 +125,8 @@ def load_library(path: str | None = None):
         "seed_verify_tree": [_P, ctypes.c_int32, _I32P, _I32P, _I32P, _I32P, _I32P, _P],
         "seed_tree_defaults": [ctypes.POINTER(SeedTreeOpts), ctypes.c_int32],
         "seed_draft_tree": [_P, ctypes.POINTER(SeedTreeOpts), _I32P, _I32P, _I32P, ctypes.POINTER(ctypes.c_float), _P],
-        "seed_generate_tree": [_P, _I32P, ctypes.c_int32, ctypes.POINTER(SeedTreeOpts), ctypes.c_int32, ctypes.c_int32,
-                               ctypes.c_int32, _I32P, _I32P, ctypes.POINTER(SeedStats)],
+        "seed_generate_tree": [_P, _I32P, ctypes.c_int32, ctypes.POINTER(SeedTreeOpts), ctypes.POINTER(SeedGenOpts),
+                               _I32P, _I32P, ctypes.POINTER(SeedStats)],
         "seed_spec_forward": [_P, ctypes.c_int32, _I32P, ctypes.c_int32, _P, _P, _P, ctypes.POINTER(ctypes.c_double)],
     }
     for name, args in sig.items():
@@ -304,8 +304,13 @@ def seed_draft_tree(ctx: int, opts: SeedTreeOpts, logits_ptr: int | None = None)
 
 
 def seed_generate_tree(ctx: int, prompt, opts: SeedTreeOpts, max_new: int, eos_id: int = -1,
-                       use_graph: bool = False, log_cap: int = 0):
+                       use_graph: bool = False, log_cap: int = 0, sim_accept: int = -1, forced_trace=None):
     toks, tp = _i32(np.asarray(prompt))
+    g = SeedGenOpts()
+    g.k, g.max_new, g.eos_id, g.sim_accept, g.use_graph = 0, max_new, eos_id, sim_accept, int(use_graph)
+    if forced_trace is not None:
+        tr, trp = _i32(np.asarray(forced_trace).reshape(-1))
+        g.forced_trace = trp
     out = np.zeros(max_new, dtype=np.int32)
     count = ctypes.c_int32()
     stats = SeedStats()
@@ -313,7 +318,7 @@ def seed_generate_tree(ctx: int, prompt, opts: SeedTreeOpts, max_new: int, eos_i
     if log_cap > 0:
         stats.n_accept_log = log.ctypes.data_as(_I32P)
         stats.n_accept_log_cap = log_cap
-    _check(load_library().seed_generate_tree(ctx, tp, len(toks), ctypes.byref(opts), max_new, eos_id, int(use_graph),
+    _check(load_library().seed_generate_tree(ctx, tp, len(toks), ctypes.byref(opts), ctypes.byref(g),
                                              out.ctypes.data_as(_I32P), ctypes.byref(count), ctypes.byref(stats)),
            "seed_generate_tree")
     st = {"rounds": stats.rounds, "drafted": stats.drafted, "accepted": stats.accepted,

@@ -104,7 +104,7 @@ struct SetupArgs {
   const int* tokens;      // committed tokens [B][tstride]
   int tstride;
   int pf_seq, pf_pos0;    // SETUP_PREFILL, SETUP_SPEC (rows at positions pf_pos0..)
-  int sim_accept;         // SETUP_VERIFY: -1 or forced acceptance length
+  int sim_accept;         // SETUP_VERIFY / SETUP_TREE: -1 or forced acceptance length
   const int* trace;       // [B][tstride] greedy trace by absolute position
   int vocab;
   const void* E;          // packed embedding
@@ -112,7 +112,7 @@ struct SetupArgs {
   int* row_seq;
   int* row_pos;
   int* row_slot;          // [M] cache slot of the row's keys/values
-  const int* tree_tok;    // SETUP_TREE: node tokens [M] (node 0 = the pending token)
+  int* tree_tok;          // SETUP_TREE: node tokens [M] (node 0 = the pending token)
   const int* tree_depth;  // SETUP_TREE: node depths [M] (rotary position t-1 + depth)
   // per-row KV block and RoPE row for the pass's QKV epilogues
   const int* bt;          // block tables [B][bt_stride]

@@ -32,6 +32,12 @@ __global__ void __launch_bounds__(256) k_setup(SetupArgs a) {
       pos = a.t[0] - 1 + a.tree_depth[m];
       slot = a.t[0] - 1 + m;
       tok = a.tree_tok[m];
+      // benchmark mode: chain nodes 1..a take the greedy trace, node a+1 a token that is not it
+      if (a.sim_accept >= 0 && m >= 1 && a.tree_depth[m] == m && m <= a.sim_accept + 1) {
+        const int tr = a.trace[pos];
+        tok = (m <= a.sim_accept) ? tr : (tr + 1) % a.vocab;
+        a.tree_tok[m] = tok;
+      }
     } else {
       b = m / a.R;
       const int r = m - b * a.R;

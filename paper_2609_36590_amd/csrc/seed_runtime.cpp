@@ -216,7 +216,7 @@ struct seed_ctx {
   // dynamic drafting: step graphs (for the options in tree_key), verification graphs by node
   // count, and a pinned status the drafting/acceptance kernels write for the host loop
   std::map<int, hipGraphExec_t> tree_step_graphs;
-  std::map<std::pair<int, int>, hipGraphExec_t> tree_verify_graphs;   // (nodes, eos)
+  std::map<std::tuple<int, int, int>, hipGraphExec_t> tree_verify_graphs;   // (nodes, eos, sim_accept)
   seed_tree_opts tree_key{};
   int* hstat = nullptr;       // host pointer
   int* hstat_dev = nullptr;   // its device address
@@ -842,7 +842,7 @@ template <typename T>
 void enqueue_verify_tree(seed_ctx* c, int n, float* logits, bool cap) {
   const Plan& p = c->p;
   SetupArgs s = setup_base(c, 0);
-  s.mode = SETUP_TREE; s.M = n; s.R = n;
+  s.mode = SETUP_TREE; s.M = n; s.R = n; s.sim_accept = c->sim_accept;
   s.tree_tok = c->ws<int>(p.o_tree);
   s.tree_depth = c->ws<int>(p.o_tree) + 2 * MAX_ROWS;
   timed(c, SEED_PHASE_VERIFY, SEED_OP_SETUP, cap, [&](const LaunchEvents*) { launch_setup<T>(s, c->s); });
@@ -967,12 +967,13 @@ seed_status launch_tree_verify(seed_ctx* c, int n, bool use_graph) {
     HIPCHK(hipGetLastError());
     return SEED_OK;
   }
-  auto it = c->tree_verify_graphs.find({n, c->eos});
+  const auto key = std::make_tuple(n, c->eos, c->sim_accept);
+  auto it = c->tree_verify_graphs.find(key);
   if (it == c->tree_verify_graphs.end()) {
     hipGraphExec_t ex;
     seed_status st = capture_graph(c, [&] { enqueue_verify_tree<T>(c, n, nullptr, true); }, &ex);
     if (st != SEED_OK) return st;
-    it = c->tree_verify_graphs.emplace(std::make_pair(n, c->eos), ex).first;
+    it = c->tree_verify_graphs.emplace(key, ex).first;
   }
   HIPCHK(hipGraphLaunch(it->second, c->s));
   return SEED_OK;
@@ -1443,26 +1444,29 @@ seed_status seed_draft_tree(seed_ctx* c, const seed_tree_opts* opts, int32_t* to
   return SEED_OK;
 }
 
-seed_status seed_generate_tree(seed_ctx* c, const int32_t* tokens, int32_t len, const seed_tree_opts* opts,
-                               int32_t max_new, int32_t eos_id, int32_t use_graph, int32_t* out, int32_t* count,
-                               seed_stats* stats) {
+seed_status seed_generate_tree(seed_ctx* c, const int32_t* tokens, int32_t len, const seed_tree_opts* topts,
+                               const seed_gen_opts* opts, int32_t* out, int32_t* count, seed_stats* stats) {
   seed_status st = check_ready(c);
   if (st != SEED_OK) return st;
-  if (!opts || !out || !count) return fail(SEED_ERR_ARG, "opts, out and count must not be NULL");
+  if (!topts || !opts || !out || !count) return fail(SEED_ERR_ARG, "topts, opts, out and count must not be NULL");
   const Plan& p = c->p;
+  const int max_new = opts->max_new;
   if (max_new < 1) return fail(SEED_ERR_ARG, "max_new must be >= 1");
-  if (eos_id < -1 || eos_id >= p.V) return fail(SEED_ERR_ARG, "eos_id out of range");
-  if (opts->max_nodes < 2 || opts->max_nodes > MAX_ROWS) return fail(SEED_ERR_ARG, "max_nodes must be in [2, 64]");
+  if (opts->eos_id < -1 || opts->eos_id >= p.V) return fail(SEED_ERR_ARG, "eos_id out of range");
+  if (topts->max_nodes < 2 || topts->max_nodes > MAX_ROWS) return fail(SEED_ERR_ARG, "max_nodes must be in [2, 64]");
+  if (opts->sim_accept < -1 || opts->sim_accept > topts->max_depth)
+    return fail(SEED_ERR_ARG, "sim_accept must be -1 or in [0, max_depth]");
+  if (opts->sim_accept >= 0 && !opts->forced_trace) return fail(SEED_ERR_ARG, "sim_accept needs forced_trace");
   std::vector<int> packed;
   // a finished sequence may still draft one more round's first step: room for two trees
-  const int extra = max_new + 2 * (opts->max_nodes + 1);
+  const int extra = max_new + 2 * (topts->max_nodes + 1);
   st = check_prompts(c, 1, tokens, &len, extra, packed);
   if (st != SEED_OK) return st;
   st = start_sequences(c, 1, &len, extra);
   if (st != SEED_OK) return st;
-  st = check_tree_opts(c, opts);
+  st = check_tree_opts(c, topts);
   if (st != SEED_OK) return st;
-  c->eos = eos_id;
+  c->eos = opts->eos_id;
   c->sim_accept = -1;
   hipEvent_t e0, e1, e2;
   HIPCHK(hipEventCreate(&e0));
@@ -1474,11 +1478,23 @@ seed_status seed_generate_tree(seed_ctx* c, const int32_t* tokens, int32_t len, 
   c->prefilled = true;
   const int limit = len + max_new;
   HIPCHK(hipMemcpyAsync(c->ws<int>(p.o_limit), &limit, 4, hipMemcpyHostToDevice, c->s));
+  std::vector<int> tr;
+  if (opts->sim_accept >= 0) {
+    tr.assign(p.tstride, 0);
+    for (int i = 0; i < max_new; ++i) {
+      const int v = opts->forced_trace[i];
+      if (v < 0 || v >= p.V) return fail(SEED_ERR_ARG, "forced_trace token out of range");
+      tr[len + i] = v;
+    }
+    HIPCHK(hipMemcpyAsync(c->ws<int>(p.o_trace), tr.data(), tr.size() * 4, hipMemcpyHostToDevice, c->s));
+    c->sim_accept = opts->sim_accept;
+  }
   HIPCHK(hipEventRecord(e1, c->s));
   HIPCHK(hipStreamSynchronize(c->s));
   int rounds_run = 0;
-  st = p.cfg.dtype == SEED_BF16 ? tree_rounds<uint16_t>(c, *opts, use_graph != 0, 0, &rounds_run)
-                                : tree_rounds<float>(c, *opts, use_graph != 0, 0, &rounds_run);
+  st = p.cfg.dtype == SEED_BF16 ? tree_rounds<uint16_t>(c, *topts, opts->use_graph != 0, 0, &rounds_run)
+                                : tree_rounds<float>(c, *topts, opts->use_graph != 0, 0, &rounds_run);
+  c->sim_accept = -1;
   if (st != SEED_OK) return st;
   HIPCHK(hipEventRecord(e2, c->s));
   HIPCHK(hipEventSynchronize(e2));

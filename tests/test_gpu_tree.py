@@ -266,3 +266,29 @@ def test_generate_tree_eos_and_short_runs():
             dec.generate_tree(prompt, binding.tree_opts(4, table=((0.5, 1), (0.6, 3))), 8)   # increasing
     finally:
         dec.close()
+
+
+@pytest.mark.parametrize("table,depth", [(((-1.0, 1),), 4), (((-1.0, 3),), 5)], ids=["chain-d4", "fan3-d5"])
+def test_generate_tree_forced_acceptance(table, depth):
+    """Benchmark mode: with the greedy continuation as the forced trace, every round accepts
+    exactly sim_accept chain nodes (random weights accept almost nothing by themselves), and the
+    output is still the greedy decode."""
+    cfg = synth.C1_TINY
+    w = synth.make_weights(cfg, seed=3)
+    prompt = synth.make_prompts(cfg, seed=2)[0]
+    max_new = 48
+    dec = decoder(cfg, w, max_batch=1, max_ctx=len(prompt) + max_new + 2 * 65 + 8, max_draft=depth)
+    try:
+        ref, _, _ = dec.generate([prompt], 0, max_new)
+        opts = binding.tree_opts(depth, tau=0.0, table=table, rest=1)
+        for a in (0, 2, depth):
+            for graph in (False, True):
+                toks, st = dec.generate_tree(prompt, opts, max_new, use_graph=graph, log_cap=256,
+                                             sim_accept=a, forced_trace=ref[0])
+                np.testing.assert_array_equal(toks, ref[0])
+                log = st["n_accept_log"]
+                say(f"[gpu] {table} a={a} graph={graph}: {st['rounds']} rounds, log {list(log)}")
+                assert np.all(log[:-2] >= a)   # a leaf may extend a path by the trace's next token
+                assert st["rounds"] <= -(-max_new // (a + 1))
+    finally:
+        dec.close()
