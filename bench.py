@@ -377,6 +377,118 @@ def spec_sweep(torch, out_md, reps=5):
 
 
 # ------------------------------------------------------------------------------------------
+# dynamic drafting + tree verification
+# ------------------------------------------------------------------------------------------
+# emulated tree shapes (label, top-p table, fan-out below it, depth, forced accepted lengths): tau
+# = 0 keeps drafting to the depth, the table fixes the fan-out of every step
+TREE_SHAPES = [("chain, depth 4", ((-1.0, 1),), 1, 4, (0, 2, 4)),
+               ("fan-out 3, depth 4", ((-1.0, 3),), 3, 4, (0, 2, 4)),
+               ("chain, depth 8", ((-1.0, 1),), 1, 8, (4, 8)),
+               ("fan-out 3, depth 6", ((-1.0, 3),), 3, 6, (4, 6))]
+TREE_OPS = (binding.OP_SETUP, binding.OP_QKV, binding.OP_ATTN, binding.OP_COMBINE, binding.OP_O, binding.OP_GATEUP,
+            binding.OP_DOWN, binding.OP_HEAD, binding.OP_HEAD_ARGMAX, binding.OP_ACCEPT, binding.OP_TOPK)
+OP_NAMES = {binding.OP_SETUP: "setup", binding.OP_QKV: "qkv", binding.OP_ATTN: "attn", binding.OP_COMBINE: "combine",
+            binding.OP_O: "o", binding.OP_GATEUP: "gateup", binding.OP_DOWN: "down", binding.OP_HEAD: "head",
+            binding.OP_ACCEPT: "accept", binding.OP_HEAD_ARGMAX: "argmax", binding.OP_TOPK: "topk"}
+
+
+def tree_bench(torch, out_md):
+    cfg = synth.C3_4B
+    gen = cfg.gen_len
+    log(f"[tree] weights for {cfg.name}")
+    weights = synth.make_weights(cfg)
+    prompt = synth.make_prompts(cfg)[0]
+    P = len(prompt)
+    max_depth = max(s[3] for s in TREE_SHAPES)
+    dec = binding.Decoder(cfg, max_batch=1, max_ctx=P + gen + 2 * 65 + 8, max_draft=max_depth)
+    dec.load_weights(weights)
+    out0, _, st0 = dec.generate([prompt], 0, gen, use_graph=True)
+    trace = out0[0]
+    res = {"workload": cfg.name, "prompt_len": P, "gen": gen, "ar_tokens_per_s": round(gen / (st0["decode_ms"] * 1e-3), 2)}
+    # the paper's options, acceptance as random weights give it
+    rows = []
+    for depth in (4, 8):
+        opts = binding.tree_opts(depth)
+        toks, st = dec.generate_tree(prompt, opts, gen, use_graph=True)   # warm-up (graph capture)
+        toks, st = dec.generate_tree(prompt, opts, gen, use_graph=True)
+        r = {"shape": f"paper table, tau 0.7, depth <= {depth}", "forced": None,
+             "tokens_per_s": round(gen / (st["decode_ms"] * 1e-3), 2), "rounds": st["rounds"],
+             "nodes_per_round": round(1 + st["drafted"] / st["rounds"], 2),
+             "accepted_per_round": round(st["accepted"] / st["rounds"], 3),
+             "output_equals_greedy": bool(np.array_equal(toks, trace))}
+        log(f"[tree] {json.dumps(r)}")
+        rows.append(r)
+    for label, table, rest, depth, accepts in TREE_SHAPES:
+        opts = binding.tree_opts(depth, tau=0.0, table=table, rest=rest)
+        for a in accepts:
+            kw = dict(use_graph=True, sim_accept=a, forced_trace=trace, log_cap=gen + 8)
+            dec.generate_tree(prompt, opts, gen, **kw)
+            toks, st = dec.generate_tree(prompt, opts, gen, **kw)
+            r = {"shape": label, "forced": a, "tokens_per_s": round(gen / (st["decode_ms"] * 1e-3), 2),
+                 "rounds": st["rounds"], "nodes_per_round": round(1 + st["drafted"] / st["rounds"], 2),
+                 "accepted_per_round": round(st["accepted"] / st["rounds"], 3),
+                 "output_equals_greedy": bool(np.array_equal(toks, trace))}
+            log(f"[tree] {json.dumps(r)}")
+            rows.append(r)
+    res["runs"] = rows
+    # per-kernel time of one emulated shape (eager launches with HIP events around each operation)
+    label, table, rest, depth, _ = TREE_SHAPES[1]
+    a = 4
+    opts = binding.tree_opts(depth, tau=0.0, table=table, rest=rest)
+    n_nodes = 1 + depth * rest
+    kw = dict(use_graph=False, sim_accept=a, forced_trace=trace, log_cap=gen + 8)
+    _, st = dec.generate_tree(prompt, opts, gen, **kw)
+    rounds = st["rounds"]
+    L = P + gen // 2
+    per_kernel = {}
+    for phase, M, layers in ((binding.PHASE_VERIFY, n_nodes, cfg.n_layers), (binding.PHASE_DRAFT, 1, cfg.n_dec_layers)):
+        for op in TREE_OPS:
+            binding.seed_kernel_timing(dec.ctx, binding.kernel_id(phase, op), True)
+            dec.generate_tree(prompt, opts, gen, **kw)
+            n, ms = binding.seed_kernel_timing_read(dec.ctx)
+            binding.seed_kernel_timing(dec.ctx, 0, False)
+            if n == 0:
+                continue
+            name = ("verify_" if phase == binding.PHASE_VERIFY else "draft_") + OP_NAMES[op]
+            b = kernel_bytes(cfg, op, M, L)
+            per_kernel[name] = {"launches_per_round": round(n / rounds, 2), "avg_us": round(ms / n * 1e3, 3),
+                                "us_per_round": round(ms * 1e3 / rounds, 2),
+                                "gbps": round(b / (ms / n * 1e-3) / 1e9, 1) if b else None}
+    dom = max(per_kernel, key=lambda kk: per_kernel[kk]["us_per_round"])
+    res["per_kernel_shape"] = f"{label}, forced {a}, {n_nodes} nodes"
+    res["per_kernel"] = per_kernel
+    res["dominant"] = dom
+    dec.close()
+    lines = ["# Dynamic drafting + tree verification (one MI355X)", "",
+             f"Command: `python3 bench.py --tree {out_md}` (repository root, library built by",
+             "`__graft_entry__.build()`). Model " + cfg.name + f", bf16, one {P}-token prompt, {gen} generated",
+             "tokens, random-init weights (seed 0). `seed_generate_tree` runs confidence-aware dynamic drafting",
+             "(per step: decoder layers, LM head, top-k/p0 kernels) and tree verification (one full-model pass",
+             "over the packed tree, acceptance, leaf cache move), each drafting step and each tree size's",
+             "verification replayed from a HIP graph; decode time from HIP events. Random weights put p0 near",
+             "1/vocab, so the paper's options stop after one step with 10 candidates and accept nothing; the",
+             "emulated shapes set tau = 0 and a one-level table (fixed fan-out per step) and force the",
+             "accepted chain length with the greedy trace (chain nodes 1..a take it, node a+1 does not).",
+             f"Plain greedy decoding (AR): {res['ar_tokens_per_s']:.1f} tok/s.", "",
+             "| shape | forced accept | nodes/round | accepted/round | tok/s | x AR | output = greedy |",
+             "|---|---|---|---|---|---|---|"]
+    for r in rows:
+        lines.append(f"| {r['shape']} | {r['forced'] if r['forced'] is not None else 'measured'} | {r['nodes_per_round']} | "
+                     f"{r['accepted_per_round']} | {r['tokens_per_s']:.1f} | {r['tokens_per_s'] / res['ar_tokens_per_s']:.2f} | "
+                     f"{r['output_equals_greedy']} |")
+    lines += ["", f"Per-operation time, {res['per_kernel_shape']} (eager launches, HIP events around each",
+              f"operation, mean over the run; GB/s = algorithmic bytes at {L} cached positions / time):", "",
+              "| operation | launches/round | avg us | us/round | GB/s |", "|---|---|---|---|---|"]
+    for kk, v in sorted(per_kernel.items(), key=lambda x: -x[1]["us_per_round"]):
+        lines.append(f"| {kk} | {v['launches_per_round']} | {v['avg_us']:.2f} | {v['us_per_round']:.1f} | "
+                     f"{v['gbps'] if v['gbps'] is not None else '-'} |")
+    lines += ["", "Raw results:", "", "```json", json.dumps(res), "```"]
+    with open(out_md, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print(json.dumps({"tree": out_md, "runs": len(rows), "dominant": dom}), flush=True)
+
+
+# ------------------------------------------------------------------------------------------
 # CPU oracle baseline
 # ------------------------------------------------------------------------------------------
 def cpu_baseline(cfg, weights, prompt, k, rounds):
@@ -423,6 +535,9 @@ def main():
     ap.add_argument("--split-sweep", metavar="OUT_MD",
                     help="draft-step cost of the 28-layer model for n_dec in 1..14 decoder layers "
                          "(measured and forced acceptance); write a summary to OUT_MD")
+    ap.add_argument("--tree", metavar="OUT_MD",
+                    help="dynamic drafting + tree verification on the 4B-scale model: measured and "
+                         "forced-acceptance tree shapes, per-operation time; writes OUT_MD")
     ap.add_argument("--spec-forward", metavar="OUT_MD",
                     help="time the forward pass of the speculative drafting objective (4B model, "
                          "1024 tokens, block sizes 4 and 16) and write a summary to OUT_MD")
@@ -441,6 +556,9 @@ def main():
         return
     if args.split_sweep:
         split_sweep(torch, args.split_sweep)
+        return
+    if args.tree:
+        tree_bench(torch, args.tree)
         return
     if args.spec_forward:
         spec_sweep(torch, args.spec_forward)

@@ -225,7 +225,6 @@ __host__ __device__ inline size_t lds_x_bytes(int M, int nkt) { return (size_t)n
 template <typename T, int PRO, int EPI>
 __global__ void __launch_bounds__(1024) k_linear_lds(LinArgs a) {
   extern __shared__ __attribute__((aligned(16))) char lds[];
-  __shared__ float s_rs[16];
   constexpr int P = 8;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int NW = a.NT * a.KS;
@@ -259,7 +258,11 @@ __global__ void __launch_bounds__(1024) k_linear_lds(LinArgs a) {
 
   // ---- stage X into LDS (loads first, then the LDS writes) ----
   const size_t zero_off = (size_t)KT * 4 * M * 32;
-  float* part = reinterpret_cast<float*>(lds + lds_x_bytes(M, KT));  // [NJ][NW][M][16]
+  // partials [NJ][NW][M][16] and the row scales: after the staged rows, or (when both do not fit)
+  // over them once the stream is done
+  const bool alias = a.lds_alias;
+  float* part = reinterpret_cast<float*>(alias ? lds : lds + lds_x_bytes(M, KT));
+  float* s_rs = part + (size_t)a.NJ * NW * M * 16;
   {
     const int row_items = KT * 4, items = M * row_items;
     for (int q0 = 0; q0 < items; q0 += 2 * (int)blockDim.x) {
@@ -290,13 +293,20 @@ __global__ void __launch_bounds__(1024) k_linear_lds(LinArgs a) {
   const char* xa = lds + (live_col ? ((size_t)kt0 * 4 * M + (size_t)kg * M + tl) * 32 : zero_off);
   const size_t xs = live_col ? (size_t)4 * M * 32 : 0;  // bytes per k-tile
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  f32x4 done[LDS_MAX_PASSES];   // finished passes, kept until the staged rows are no longer read
   int jC = 0, iC = 0;  // pass / k-tile of the next tile to consume
   auto consume = [&](int slot) {
     ET<T>::mma(acc, wb[slot], ET<T>::from_lds(xa + iC * xs));
     if (++iC == nk) {
-      if (live_col) {
-        float* dst = part + ((size_t)(jC * NW + wave) * M + tl) * 16 + 4 * kg;
-        dst[0] = acc[0]; dst[1] = acc[1]; dst[2] = acc[2]; dst[3] = acc[3];
+      if (!alias) {
+        if (live_col) {
+          float* dst = part + ((size_t)(jC * NW + wave) * M + tl) * 16 + 4 * kg;
+          dst[0] = acc[0]; dst[1] = acc[1]; dst[2] = acc[2]; dst[3] = acc[3];
+        }
+      } else {
+#pragma unroll
+        for (int q = 0; q < LDS_MAX_PASSES; ++q)
+          if (q == jC) done[q] = acc;
       }
       acc = f32x4{0.f, 0.f, 0.f, 0.f};
       iC = 0;
@@ -324,6 +334,18 @@ __global__ void __launch_bounds__(1024) k_linear_lds(LinArgs a) {
 #pragma unroll
   for (int p = 0; p < P; ++p)
     if (s0 + P + p < Sw) consume(p);
+
+  if (alias) {
+    __syncthreads();   // every wave is done with the staged rows
+    if (live_col) {
+#pragma unroll
+      for (int q = 0; q < LDS_MAX_PASSES; ++q)
+        if (q < nj) {
+          float* dst = part + ((size_t)(q * NW + wave) * M + tl) * 16 + 4 * kg;
+          dst[0] = done[q][0]; dst[1] = done[q][1]; dst[2] = done[q][2]; dst[3] = done[q][3];
+        }
+    }
+  }
 
   // ---- sums over the K-splits (in ks order), RMSNorm row scale, epilogue ----
   if constexpr (PRO == PRO_NORM) {
@@ -641,7 +663,10 @@ static constexpr int SPLITK_NT = 8;
 
 size_t linear_lds_bytes(int M, int K, int NT, int KS, int S, int NJ, int kind) {
   (void)S;
-  if (kind == LIN_LDS) return lds_x_bytes(M, K >> 5) + (size_t)NJ * NT * KS * M * 16 * sizeof(float);
+  if (kind == LIN_LDS) {
+    const size_t x = lds_x_bytes(M, K >> 5), part = (size_t)(NJ * NT * KS * M + 1) * 16 * sizeof(float);
+    return x + part <= linear_lds_limit() ? x + part : std::max(x, part);
+  }
   if (kind == LIN_SPLITK) {
     const int nk_max = ((K >> 5) + KS - 1) / KS;
     return (size_t)nk_max * 4 * M * 32 + 64;
@@ -665,6 +690,7 @@ static void launch_linear_pe(const LinArgs& a0, int kind, hipStream_t s, const L
     const dim3 grid((n_groups + a.NJ - 1) / a.NJ);
     const dim3 block(64 * a.NT * a.KS);
     const size_t lds = linear_lds_bytes(a.M, a.K, a.NT, a.KS, a.S, a.NJ, kind);
+    a.lds_alias = lds < lds_x_bytes(a.M, a.K >> 5) + (size_t)(a.NJ * a.NT * a.KS * a.M + 1) * 16 * sizeof(float);
     launch(k_linear_lds<T, PRO, EPI>, grid, block, lds, s, ev, a);
     return;
   }

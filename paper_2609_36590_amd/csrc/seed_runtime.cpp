@@ -295,7 +295,7 @@ void tile_policy(int N, int K, bool head, int& NT, int& KS, int& S, int& NJ) {
   if (n_tiles >= 256) {
     KS = std::min(8, KT);
     NT = 2;
-    NJ = std::max(1, (cdiv(n_tiles, NT) + 100) / 200);
+    NJ = std::min(LDS_MAX_PASSES, std::max(1, (cdiv(n_tiles, NT) + 100) / 200));
     return;
   }
   KS = std::min(16, std::max(1, KT / 16));
@@ -357,9 +357,14 @@ LinArgs lin_base(seed_ctx* c, int M) {
 // Kernel for one linear launch: activation rows staged in LDS when they fit (M <= 16); passes of
 // more rows split K across workgroups (each stages its k-range only) and add the range partials
 // in a second kernel; otherwise activation fragments are read from global memory.
+// Measured on MI355X (4B-scale shapes, M = 1..16): staging the rows in LDS wins while a workgroup
+// stages at most 9 x 4096 activations; beyond that the split-K kernel (each workgroup stages one
+// k-range) is faster than both the LDS kernel and the global-fragment kernel.
 int linear_kind(const LinArgs& a, bool head) {
-  if (a.M <= 16 && linear_lds_bytes(a.M, a.K, a.NT, a.KS, a.S, a.NJ, LIN_LDS) <= linear_lds_limit()) return LIN_LDS;
-  if (a.M > 16 && !head && linear_lds_bytes(a.M, a.K, a.NT, a.KS, a.S, a.NJ, LIN_SPLITK) <= linear_lds_limit())
+  if (a.M <= 16 && (head || (long long)a.M * a.K <= 9 * 4096) &&
+      linear_lds_bytes(a.M, a.K, a.NT, a.KS, a.S, a.NJ, LIN_LDS) <= linear_lds_limit())
+    return LIN_LDS;
+  if (!head && linear_lds_bytes(a.M, a.K, a.NT, a.KS, a.S, a.NJ, LIN_SPLITK) <= linear_lds_limit())
     return LIN_SPLITK;
   return LIN_GLOBAL;
 }
