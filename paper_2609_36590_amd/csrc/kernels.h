@@ -63,7 +63,6 @@ struct LinArgs {
   int amax_stride;
   float* part;            // LIN_SPLITK: k-range partials [KS][M][N]
   float* part_rs;         // LIN_SPLITK with the RMSNorm prologue: row scales [M]
-  int lds_alias;          // LIN_LDS: partials overwrite the staged rows after the stream (set by the launcher)
 };
 
 // Arguments of the split-KV paged attention kernel and its combine kernel.
@@ -152,7 +151,7 @@ struct DevState {
 // Kernel choice for a linear launch: weights streamed with the activation rows staged in LDS as
 // MFMA fragments (M <= 16 and the rows fit), else the activation fragments come from global memory.
 enum LinearKind { LIN_LDS = 0, LIN_GLOBAL = 1, LIN_SPLITK = 2 };
-constexpr int LDS_MAX_PASSES = 4;   // n-tile passes (NJ) of one k_linear_lds workgroup
+constexpr int LDS_MAX_PASSES = 8;   // n-tile passes (NJ) of one k_linear_lds workgroup
 
 // Optional timing events stamped by the launches themselves (hipExtLaunchKernel): `start` at the
 // start of the first kernel of the operation, `stop` at the end of its last kernel.

@@ -222,7 +222,7 @@ __host__ __device__ inline size_t lds_x_bytes(int M, int nkt) { return (size_t)n
 // wave (nl, ks) covers k-range ks of n-tile nl of every pass, as one continuous stream. All KS
 // K-splits of an n-tile run in one workgroup (the runtime uses this kernel only with S == 1).
 // ---------------------------------------------------------------------------------------------
-template <typename T, int PRO, int EPI>
+template <typename T, int PRO, int EPI, bool ALIAS>
 __global__ void __launch_bounds__(1024) k_linear_lds(LinArgs a) {
   extern __shared__ __attribute__((aligned(16))) char lds[];
   constexpr int P = 8;
@@ -260,7 +260,7 @@ __global__ void __launch_bounds__(1024) k_linear_lds(LinArgs a) {
   const size_t zero_off = (size_t)KT * 4 * M * 32;
   // partials [NJ][NW][M][16] and the row scales: after the staged rows, or (when both do not fit)
   // over them once the stream is done
-  const bool alias = a.lds_alias;
+  constexpr bool alias = ALIAS;
   float* part = reinterpret_cast<float*>(alias ? lds : lds + lds_x_bytes(M, KT));
   float* s_rs = part + (size_t)a.NJ * NW * M * 16;
   {
@@ -293,19 +293,19 @@ __global__ void __launch_bounds__(1024) k_linear_lds(LinArgs a) {
   const char* xa = lds + (live_col ? ((size_t)kt0 * 4 * M + (size_t)kg * M + tl) * 32 : zero_off);
   const size_t xs = live_col ? (size_t)4 * M * 32 : 0;  // bytes per k-tile
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  f32x4 done[LDS_MAX_PASSES];   // finished passes, kept until the staged rows are no longer read
+  f32x4 done[ALIAS ? LDS_MAX_PASSES : 1];   // finished passes, kept until the staged rows are no longer read
   int jC = 0, iC = 0;  // pass / k-tile of the next tile to consume
   auto consume = [&](int slot) {
     ET<T>::mma(acc, wb[slot], ET<T>::from_lds(xa + iC * xs));
     if (++iC == nk) {
-      if (!alias) {
+      if constexpr (!ALIAS) {
         if (live_col) {
           float* dst = part + ((size_t)(jC * NW + wave) * M + tl) * 16 + 4 * kg;
           dst[0] = acc[0]; dst[1] = acc[1]; dst[2] = acc[2]; dst[3] = acc[3];
         }
       } else {
 #pragma unroll
-        for (int q = 0; q < LDS_MAX_PASSES; ++q)
+        for (int q = 0; q < (ALIAS ? LDS_MAX_PASSES : 1); ++q)
           if (q == jC) done[q] = acc;
       }
       acc = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -335,11 +335,11 @@ __global__ void __launch_bounds__(1024) k_linear_lds(LinArgs a) {
   for (int p = 0; p < P; ++p)
     if (s0 + P + p < Sw) consume(p);
 
-  if (alias) {
+  if constexpr (ALIAS) {
     __syncthreads();   // every wave is done with the staged rows
     if (live_col) {
 #pragma unroll
-      for (int q = 0; q < LDS_MAX_PASSES; ++q)
+      for (int q = 0; q < (ALIAS ? LDS_MAX_PASSES : 1); ++q)
         if (q < nj) {
           float* dst = part + ((size_t)(q * NW + wave) * M + tl) * 16 + 4 * kg;
           dst[0] = done[q][0]; dst[1] = done[q][1]; dst[2] = done[q][2]; dst[3] = done[q][3];
@@ -690,8 +690,9 @@ static void launch_linear_pe(const LinArgs& a0, int kind, hipStream_t s, const L
     const dim3 grid((n_groups + a.NJ - 1) / a.NJ);
     const dim3 block(64 * a.NT * a.KS);
     const size_t lds = linear_lds_bytes(a.M, a.K, a.NT, a.KS, a.S, a.NJ, kind);
-    a.lds_alias = lds < lds_x_bytes(a.M, a.K >> 5) + (size_t)(a.NJ * a.NT * a.KS * a.M + 1) * 16 * sizeof(float);
-    launch(k_linear_lds<T, PRO, EPI>, grid, block, lds, s, ev, a);
+    const bool alias = lds < lds_x_bytes(a.M, a.K >> 5) + (size_t)(a.NJ * a.NT * a.KS * a.M + 1) * 16 * sizeof(float);
+    if (alias) launch(k_linear_lds<T, PRO, EPI, true>, grid, block, lds, s, ev, a);
+    else launch(k_linear_lds<T, PRO, EPI, false>, grid, block, lds, s, ev, a);
     return;
   }
   if (kind == LIN_SPLITK) {
@@ -755,7 +756,8 @@ void launch_argmax_finalize(const float* val, const int* idx, int stride, int n_
 
 template <typename T, int PRO, int EPI>
 static bool allow_big_lds(int bytes) {
-  const void* fns[] = {reinterpret_cast<const void*>(&k_linear_lds<T, PRO, EPI>),
+  const void* fns[] = {reinterpret_cast<const void*>(&k_linear_lds<T, PRO, EPI, false>),
+                       reinterpret_cast<const void*>(&k_linear_lds<T, PRO, EPI, true>),
                        reinterpret_cast<const void*>(&k_linear_splitk<T, 1, 4, PRO>),
                        reinterpret_cast<const void*>(&k_linear_splitk<T, 1, 8, PRO>),
                        reinterpret_cast<const void*>(&k_linear_splitk<T, 2, 4, PRO>),

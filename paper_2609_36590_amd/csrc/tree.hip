@@ -100,17 +100,39 @@ __global__ void __launch_bounds__(256) k_topk_finalize(TreeDraftArgs a, int G) {
   __shared__ float s_f[4];
   __shared__ float s_v[4];
   __shared__ int s_i[4];
-  __shared__ float c_v[TOPK_PARTS * TOPK_MAX];
-  __shared__ int c_i[TOPK_PARTS * TOPK_MAX];
   __shared__ int s_win[TOPK_MAX];
+  __shared__ int s_cand[TREE_MAX_STEPS * TOPK_MAX];
+  __shared__ int s_kcnt[TREE_MAX_STEPS];
+  __shared__ int s_root, s_tag;
+  // every global input is requested up front, in one round trip: the partials (thread t holds
+  // candidates t, t + 256, ... of the G x TOPK_MAX table), chunk maxima and sums, and for the
+  // packing the earlier steps' candidates and fan-outs, the root and the round tag
+  constexpr int PER = TOPK_PARTS * TOPK_MAX / 256;
+  const int nc = G * TOPK_MAX;
+  float cv[PER];
+  int ci[PER];
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int c = tid + 256 * u;
+    const bool ok = c < nc && (c & (TOPK_MAX - 1)) < a.k_max;
+    cv[u] = ok ? a.pval[c] : NEG_INF;
+    ci[u] = ok ? a.pidx[c] : -1;
+  }
+  const float pm = tid < G ? a.pmax[tid] : NEG_INF;
+  const float ps = tid < G ? a.psum[tid] : 0.f;
+  for (int i = tid; i < a.step * TOPK_MAX; i += 256) s_cand[i] = a.cand[i];
+  if (tid < a.step) s_kcnt[tid] = a.kcnt[tid];
+  if (tid == 0) {
+    s_root = a.drafts[0];
+    s_tag = *a.rounds;
+  }
   // global maximum, then the sum of exponentials (waves and partials in a fixed order)
-  float m = tid < G ? a.pmax[tid] : NEG_INF;
-  m = wave_max(m);
+  float m = wave_max(pm);
   if (lane == 0) s_f[w] = m;
   __syncthreads();
   const float M = fmaxf(fmaxf(s_f[0], s_f[1]), fmaxf(s_f[2], s_f[3]));
   __syncthreads();
-  float sv = tid < G ? a.psum[tid] * expf(a.pmax[tid] - M) : 0.f;
+  float sv = tid < G ? ps * expf(pm - M) : 0.f;
   sv = wave_sum(sv);
   if (lane == 0) s_f[w] = sv;
   __syncthreads();
@@ -123,22 +145,15 @@ __global__ void __launch_bounds__(256) k_topk_finalize(TreeDraftArgs a, int G) {
       break;
     }
   k = min(k, a.max_nodes - nodes0);
-  // the k best of G * k_max partial candidates
-  const int nc = G * TOPK_MAX;
-  for (int c = tid; c < nc; c += 256) {
-    const bool ok = (c & (TOPK_MAX - 1)) < a.k_max;
-    c_v[c] = ok ? a.pval[c] : NEG_INF;
-    c_i[c] = ok ? a.pidx[c] : -1;
-  }
-  __syncthreads();
+  // the k best of the partial candidates, one block-wide arg-max per rank
   for (int r = 0; r < k; ++r) {
     float bv = NEG_INF;
-    int bi = -1, bc = -1;
-    for (int c = tid; c < nc; c += 256)
-      if (c_i[c] >= 0 && ranks_before(c_v[c], c_i[c], bv, bi)) {
-        bv = c_v[c];
-        bi = c_i[c];
-        bc = c;
+    int bi = -1;
+#pragma unroll
+    for (int u = 0; u < PER; ++u)
+      if (ci[u] >= 0 && ranks_before(cv[u], ci[u], bv, bi)) {
+        bv = cv[u];
+        bi = ci[u];
       }
     float wv = bv;
     int wi = bi;
@@ -156,7 +171,9 @@ __global__ void __launch_bounds__(256) k_topk_finalize(TreeDraftArgs a, int G) {
         xv = s_v[q];
         xi = s_i[q];
       }
-    if (bc >= 0 && bi == xi) c_i[bc] = -1;
+#pragma unroll
+    for (int u = 0; u < PER; ++u)
+      if (ci[u] == xi) ci[u] = -1;   // token ids are unique: only the winner's holder matches
     if (tid == 0) s_win[r] = xi;
     __syncthreads();
   }
@@ -175,19 +192,19 @@ __global__ void __launch_bounds__(256) k_topk_finalize(TreeDraftArgs a, int G) {
   int* tok = a.tree;
   int* par = a.tree + 64;
   int* dep = a.tree + 128;
-  tok[0] = a.drafts[0];
+  tok[0] = s_root;
   par[0] = -1;
   dep[0] = 0;
   for (int d = 1; d <= step; ++d) {
-    tok[d] = (d == step) ? s_win[0] : a.cand[d * TOPK_MAX];
+    tok[d] = (d == step) ? s_win[0] : s_cand[d * TOPK_MAX];
     par[d] = d - 1;
     dep[d] = d;
   }
   int n = step + 1;
   for (int d = 1; d <= step; ++d) {
-    const int kd = (d == step) ? k : a.kcnt[d];
+    const int kd = (d == step) ? k : s_kcnt[d];
     for (int r = 1; r < kd; ++r) {
-      tok[n] = (d == step) ? s_win[r] : a.cand[d * TOPK_MAX + r];
+      tok[n] = (d == step) ? s_win[r] : s_cand[d * TOPK_MAX + r];
       par[n] = d - 1;
       dep[n] = d;
       ++n;
@@ -198,7 +215,7 @@ __global__ void __launch_bounds__(256) k_topk_finalize(TreeDraftArgs a, int G) {
     a.hstat[1] = n;
     a.hstat[2] = step;
     __threadfence_system();
-    a.hstat[0] = *a.rounds;
+    a.hstat[0] = s_tag;
   }
 }
 
