@@ -488,6 +488,24 @@ def tree_bench(torch, out_md):
     print(json.dumps({"tree": out_md, "runs": len(rows), "dominant": dom}), flush=True)
 
 
+def copy_ceiling(torch, n=1 << 30, reps=5):
+    """Bytes read + written per second by a plain device-to-device copy of n bytes (median)."""
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        b.copy_(a)
+        e1.record()
+        e1.synchronize()
+        ts.append(e0.elapsed_time(e1) * 1e-3)
+    del a, b
+    return 2 * n / statistics.median(ts)
+
+
 # ------------------------------------------------------------------------------------------
 # CPU oracle baseline
 # ------------------------------------------------------------------------------------------
@@ -498,20 +516,31 @@ def cpu_baseline(cfg, weights, prompt, k, rounds):
     cores = len(os.sched_getaffinity(0))
     log(f"[cpu] widening weights to fp32 ({cores} host cores)")
     model = om.Model(cfg, synth.weights_as_f32(cfg, weights), np.float32)
-    log("[cpu] oracle prefill (untimed)")
-    st = os_.prefill(model, prompt, len(prompt) + (k + 1) * rounds + 2)
-    log(f"[cpu] timing {rounds} oracle rounds")
+    log("[cpu] oracle prefill")
     t0 = time.perf_counter()
+    st = os_.prefill(model, prompt, len(prompt) + (k + 1) * rounds + 2)
+    t_prefill = time.perf_counter() - t0
+    log(f"[cpu] timing {rounds} oracle rounds")
     before = st.t
+    t_draft, t_verify = [], []
+    t0 = time.perf_counter()
     for _ in range(rounds):
+        a = time.perf_counter()
         d, _ = os_.draft(st, k)
-        n, b = os_.accept(d, os_.verify(st, d))
-        os_.commit(st, d, n, b)
+        b = time.perf_counter()
+        n, bonus = os_.accept(d, os_.verify(st, d))
+        os_.commit(st, d, n, bonus)
+        c = time.perf_counter()
+        t_draft.append((b - a) / max(k, 1))
+        t_verify.append(c - b)
     dt = time.perf_counter() - t0
     return {"value": (st.t - before) / dt, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "verify_ms": round(statistics.median(t_verify) * 1e3, 1),
+            "draft_step_ms": round(statistics.median(t_draft) * 1e3, 1),
+            "prefill_s": round(t_prefill, 2),
             "sample": f"{rounds} rounds of Algorithm 2 (k={k}) on the same model and 1024-token prompt "
-                      f"after an untimed oracle prefill; {dt:.1f} s, {st.t - before} tokens, "
-                      f"{dt / rounds * 1e3:.0f} ms per round"}
+                      f"after the oracle prefill (timed apart); {dt:.1f} s, {st.t - before} tokens, "
+                      f"{dt / rounds * 1e3:.0f} ms per round; fp32 NumPy with BLAS on {cores} host threads"}
 
 
 # ------------------------------------------------------------------------------------------
@@ -522,7 +551,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--k", type=int, default=4)
     ap.add_argument("--config", default=synth.C3_4B.name, choices=sorted(synth.CONFIGS))
-    ap.add_argument("--cpu-rounds", type=int, default=2)
+    ap.add_argument("--cpu-rounds", type=int, default=40, help="oracle rounds timed on the host (about 13 s)")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--profile-run", action="store_true",
@@ -736,6 +765,8 @@ def main():
 
     dec.close()
     del dec
+    torch.cuda.empty_cache()
+    result["copy_ceiling_gbps"] = round(copy_ceiling(torch) / 1e9, 1)
     torch.cuda.empty_cache()
     if not args.no_cpu:
         result["cpu_baseline"] = cpu_baseline(cfg, weights, prompt, k, args.cpu_rounds)

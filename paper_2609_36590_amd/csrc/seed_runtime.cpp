@@ -462,6 +462,7 @@ void run_head(seed_ctx* c, int M, int* tok_out, int tok_stride, float* logits, l
   int NT, KS, S, NJ;
   tile_policy(a.N, a.K, true, NT, KS, S, NJ);
   const int parts = cdiv(p.V / 16, NT);   // one argmax partial per n-group
+  if (!tok_out) return;   // the caller ranks the logits itself (dynamic drafting)
   timed(c, phase, SEED_OP_HEAD_ARGMAX, cap, [&](const LaunchEvents*) {
     launch_argmax_finalize(a.amax_val, a.amax_idx, a.amax_stride, parts, M, tok_out, tok_stride, c->s);
   });
@@ -925,7 +926,7 @@ void enqueue_tree_step(seed_ctx* c, const seed_tree_opts& o, int step, float* lo
   s.mode = SETUP_DRAFT; s.M = 1; s.R = 1; s.step = step;
   timed(c, SEED_PHASE_DRAFT, SEED_OP_SETUP, cap, [&](const LaunchEvents*) { launch_setup<T>(s, c->s); });
   run_layers<T>(c, 1, 1, 1, p.LD, p.L, SEED_PHASE_DRAFT, nullptr, cap);
-  run_head<T>(c, 1, c->ws<int>(p.o_drafts) + step, p.dstride, logits, (long long)p.V, SEED_PHASE_DRAFT, cap);
+  run_head<T>(c, 1, nullptr, p.dstride, logits, (long long)p.V, SEED_PHASE_DRAFT, cap);
   const TreeDraftArgs a = tree_args(c, o, step, logits);
   timed(c, SEED_PHASE_DRAFT, SEED_OP_TOPK, cap, [&](const LaunchEvents*) { launch_tree_topk(a, c->s); });
 }

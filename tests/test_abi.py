@@ -92,3 +92,15 @@ def test_spec_cache_bytes_cover_the_decoder_layers(lib):
     # 2 decoder layers x 2 (K, V) x 8 heads x 128 dims x 2 bytes per position
     assert n >= 2 * 2 * 8 * 128 * 2 * 1545
     assert n < 1.1 * 2 * 2 * 8 * 128 * 2 * (1545 + 16)
+
+
+def test_tree_options_layout_and_paper_defaults(lib):
+    # float tau, int max_depth, int n_levels, float thr[4], int k[4], int k_rest, int max_nodes
+    assert ctypes.sizeof(binding.SeedTreeOpts) == 4 * (3 + 4 + 4 + 2)
+    o = binding.tree_opts(6)
+    assert o.tau == pytest.approx(0.7) and o.max_depth == 6 and o.n_levels == 3
+    assert [o.thr[j] for j in range(3)] == pytest.approx([0.95, 0.8, 0.5])
+    assert list(o.k[:3]) == [1, 3, 5] and o.k_rest == 10 and o.max_nodes == 64
+    o2 = binding.tree_opts(3, tau=0.5, table=((0.9, 2),), rest=4, max_nodes=20)
+    assert (o2.tau, o2.n_levels, o2.k[0], o2.k_rest, o2.max_nodes) == (pytest.approx(0.5), 1, 2, 4, 20)
+    assert o2.thr[0] == pytest.approx(0.9)
