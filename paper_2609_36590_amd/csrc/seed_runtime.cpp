@@ -180,6 +180,22 @@ Plan make_plan(const seed_config& c) {
   return p;
 }
 
+// Timing events of one call, destroyed on every return path.
+struct CallEvents {
+  hipEvent_t e[3] = {nullptr, nullptr, nullptr};
+  hipError_t create() {
+    for (auto& x : e) {
+      const hipError_t r = hipEventCreate(&x);
+      if (r != hipSuccess) return r;
+    }
+    return hipSuccess;
+  }
+  ~CallEvents() {
+    for (auto& x : e)
+      if (x) hipEventDestroy(x);
+  }
+};
+
 struct TimedLaunch {
   hipEvent_t a, b;
 };
@@ -1271,10 +1287,9 @@ seed_status seed_generate(seed_ctx* c, int32_t B, const int32_t* tokens, const i
   c->eos = opts->eos_id;
   c->sim_accept = -1;
 
-  hipEvent_t e0, e1, e2;
-  HIPCHK(hipEventCreate(&e0));
-  HIPCHK(hipEventCreate(&e1));
-  HIPCHK(hipEventCreate(&e2));
+  CallEvents ce;
+  HIPCHK(ce.create());
+  hipEvent_t e0 = ce.e[0], e1 = ce.e[1], e2 = ce.e[2];
   HIPCHK(hipEventRecord(e0, c->s));
   st = p.cfg.dtype == SEED_BF16 ? do_prefill<uint16_t>(c, packed) : do_prefill<float>(c, packed);
   if (st != SEED_OK) return st;
@@ -1348,9 +1363,6 @@ seed_status seed_generate(seed_ctx* c, int32_t B, const int32_t* tokens, const i
       HIPCHK(hipMemcpy(stats->n_accept_log, c->ws<int>(p.o_log), rows * B * 4, hipMemcpyDeviceToHost));
     }
   }
-  hipEventDestroy(e0);
-  hipEventDestroy(e1);
-  hipEventDestroy(e2);
   c->sim_accept = -1;
   c->drafts_k = -1;
   return SEED_OK;
@@ -1474,10 +1486,9 @@ seed_status seed_generate_tree(seed_ctx* c, const int32_t* tokens, int32_t len, 
   if (st != SEED_OK) return st;
   c->eos = opts->eos_id;
   c->sim_accept = -1;
-  hipEvent_t e0, e1, e2;
-  HIPCHK(hipEventCreate(&e0));
-  HIPCHK(hipEventCreate(&e1));
-  HIPCHK(hipEventCreate(&e2));
+  CallEvents ce;
+  HIPCHK(ce.create());
+  hipEvent_t e0 = ce.e[0], e1 = ce.e[1], e2 = ce.e[2];
   HIPCHK(hipEventRecord(e0, c->s));
   st = p.cfg.dtype == SEED_BF16 ? do_prefill<uint16_t>(c, packed) : do_prefill<float>(c, packed);
   if (st != SEED_OK) return st;
@@ -1530,9 +1541,6 @@ seed_status seed_generate_tree(seed_ctx* c, const int32_t* tokens, int32_t len, 
       HIPCHK(hipMemcpy(stats->n_accept_log, c->ws<int>(p.o_log), rows * 4, hipMemcpyDeviceToHost));
     }
   }
-  hipEventDestroy(e0);
-  hipEventDestroy(e1);
-  hipEventDestroy(e2);
   c->drafts_k = -1;
   return SEED_OK;
 }
