@@ -165,3 +165,54 @@ def test_spec_forward_28l_matches_oracle():
     say(f"[gpu] max |logits - oracle| = {err:.3g}; L_spec {loss:.6g} vs {ref_loss:.6g}")
     assert err <= TOL
     assert abs(loss - ref_loss) <= 2 * TOL * (len(x) - 1)
+
+
+@pytest.mark.timeout(900)
+def test_tree_round_matches_oracle_at_full_size(weights_4b):
+    """Dynamic drafting and tree verification on the 4B model after the 1024-token prefill: the
+    first step's drafter logits and p0 against the oracle's, the drafted tree where no decision is
+    near a boundary; then a 31-node tree (depth 3, fan-out 10: the split-K and wide-head launch
+    shapes) verified by the GPU, every node's logits within 2e-2 of the oracle's tree verification,
+    path and bonus where the visited nodes' top-2 gaps leave no doubt; finally tree decoding commits
+    the GPU's plain greedy tokens."""
+    from oracle import tree as ot
+    from paper_2609_36590_amd import binding
+    cfg = synth.C3_4B
+    w = weights_4b
+    prompt = synth.make_prompts(cfg)[0]
+    dec = decoder(cfg, w, max_batch=1, max_ctx=len(prompt) + N_NEW + 2 * 65 + 2, max_draft=K)
+    m = oracle_model(cfg, w)
+    try:
+        dec.prefill([prompt])
+        toks, par, p0, dlog = dec.draft_tree(binding.tree_opts(K), logits=True)
+        say(f"[gpu] oracle prefill {cfg.name} over {len(prompt)} tokens")
+        st = os_.prefill(m, prompt, len(prompt) + 70)
+        tree = ot.draft_tree(st, 0.7, K)
+        derr = float(np.abs(dlog[0] - tree.draft_logits[0]).max())
+        say(f"[gpu] step 1: p0 {p0[0]:.4g} vs {tree.p0[0]:.4g}, max |draft - oracle| = {derr:.3g}, "
+            f"{len(toks)} vs {len(tree.tokens)} nodes")
+        assert derr <= TOL and abs(p0[0] - tree.p0[0]) <= 4 * TOL * tree.p0[0] + 1e-6
+        top = np.sort(tree.draft_logits[0].astype(np.float64))[::-1][:11]
+        if len(tree.p0) == 1 and np.all(-np.diff(top) > 2 * TOL) and min(
+                abs(tree.p0[0] - x) for x in (0.95, 0.8, 0.5, 0.7)) > 4 * TOL:
+            assert toks == tree.tokens and par == tree.parents
+        # a wide tree through the GPU's verification (drafting again from the committed prefix)
+        st.cache.truncate(st.t - 1)
+        wide = ot.draft_tree(st, 0.0, 3)
+        assert len(wide.tokens) == 31
+        logits, _ = ot.verify_tree(st, wide)
+        path, bonus = ot.accept_tree(wide, logits)
+        dec.prefill([prompt])
+        gpath, gbonus, glog = dec.verify_tree(wide.tokens, wide.parents, logits=True)
+        verr = float(np.abs(glog - logits).max())
+        say(f"[gpu] 31-node tree: max |verify - oracle| = {verr:.3g}; path {gpath} vs {path}")
+        assert verr <= TOL
+        visited = [0] + list(path)
+        if np.all(top2_gap(logits[visited]) > 2 * TOL):
+            assert gpath == path and gbonus == bonus
+        say(f"[gpu] {cfg.name}: tree decoding of {N_NEW} tokens vs plain greedy")
+        out0, _, _ = dec.generate([prompt], 0, N_NEW, use_graph=True)
+        out_t, _ = dec.generate_tree(prompt, binding.tree_opts(K), N_NEW, use_graph=True)
+        np.testing.assert_array_equal(out_t, out0[0])
+    finally:
+        dec.close()
