@@ -674,6 +674,120 @@ size_t linear_lds_bytes(int M, int K, int NT, int KS, int S, int NJ, int kind) {
   return (size_t)(NT * KS * M * 16) * sizeof(float);
 }
 
+// ---------------------------------------------------------------------------------------------
+// LM head for 16 < M <= 64 rows (batched verification, draft trees of more than 16 nodes): the
+// activation rows of all M tokens do not fit LDS whole (4 bytes per element as MFMA B slots), so
+// they are staged in chunks of HEAD_CK k-tiles, double-buffered: the loads of chunk c+1 are issued
+// before chunk c is consumed and written to the other buffer after it. Each of the 8 waves
+// streams one n-tile over all of K in k order (KS = 1, as the narrow kernel does for any M), for TT
+// token tiles of 16 rows, so every row's logits are bit-identical to a pass of fewer rows.
+// ---------------------------------------------------------------------------------------------
+constexpr int HEAD_CK = 8;   // k-tiles per staged chunk (= the weight ring depth)
+static size_t g_lds_limit = 65536;   // dynamic LDS one workgroup may use (set by configure_kernels)
+
+template <typename T, int TT>
+__global__ void __launch_bounds__(512) k_linear_head_chunked(LinArgs a) {
+  extern __shared__ __attribute__((aligned(16))) char lds[];
+  __shared__ float s_rs[64];
+  constexpr int P = HEAD_CK;
+  constexpr int XI = (HEAD_CK * 4 * 16 * TT + 511) / 512;   // staged items per thread and chunk
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int KT = a.K >> 5, n_tiles = a.N >> 4, M = a.M;
+  const int tl = lane & 15, kg = lane >> 4;
+  const Grp gr{(int)blockIdx.x, (int)gridDim.x};
+  const int nt = blockIdx.x * a.NT + wave;
+  const T* w0 = reinterpret_cast<const T*>(a.W) + (size_t)(nt < n_tiles ? nt : 0) * KT * 512 + lane * 8;
+  const size_t chunk_bytes = (size_t)HEAD_CK * 4 * M * 32;
+  const size_t zero_off = 2 * chunk_bytes;
+  const int NC = (KT + HEAD_CK - 1) / HEAD_CK;
+
+  EpiPre epre{};
+  epi_load<EPI_HEAD>(a, gr, tid, epre);
+  float ssv[4] = {0.f, 0.f, 0.f, 0.f};
+  const bool pre = preload_row_ssq(a, wave, ssv);
+
+  // chunk c's items q = (ktl*4 + kg)*M + r hold x[r][32(c*CK + ktl) + 8kg .. +7]; loaded branch-free
+  // (items past the chunk reload item 0 and are not written)
+  float xv[XI][8];
+  auto stage_load = [&](int c) {
+    const int nkc = min(HEAD_CK, KT - c * HEAD_CK), items = nkc * 4 * M;
+#pragma unroll
+    for (int u = 0; u < XI; ++u) {
+      const int q = u * 512 + tid, qc = q < items ? q : 0;
+      const int r = qc % M, rest = qc / M;
+      load8(a.X + (size_t)r * a.ldx + (size_t)c * HEAD_CK * 32 + rest * 8, xv[u]);
+    }
+  };
+  auto stage_store = [&](int c) {
+    const int nkc = min(HEAD_CK, KT - c * HEAD_CK), items = nkc * 4 * M;
+    char* buf = lds + (c & 1) * chunk_bytes;
+#pragma unroll
+    for (int u = 0; u < XI; ++u) {
+      const int q = u * 512 + tid;
+      if (q < items) ET<T>::to_lds(buf + (size_t)q * 32, xv[u]);
+    }
+  };
+
+  stage_load(0);
+  typename ET<T>::A wb[P];
+#pragma unroll
+  for (int p = 0; p < P; ++p) wb[p] = ET<T>::load_nt(w0 + (size_t)min(p, KT - 1) * 512);
+  stage_store(0);
+  if (tid < 2) *reinterpret_cast<float4*>(lds + zero_off + tid * 16) = make_float4(0.f, 0.f, 0.f, 0.f);
+  __syncthreads();
+
+  f32x4 acc[TT];
+#pragma unroll
+  for (int tt = 0; tt < TT; ++tt) acc[tt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int c = 0; c < NC; ++c) {
+    if (c + 1 < NC) stage_load(c + 1);
+    const char* buf = lds + (c & 1) * chunk_bytes;
+    const int nkc = min(HEAD_CK, KT - c * HEAD_CK);
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+      if (p < nkc) {
+#pragma unroll
+        for (int tt = 0; tt < TT; ++tt) {
+          const int m = tt * 16 + tl;
+          const char* xb = m < M ? buf + ((size_t)(p * 4 + kg) * M + m) * 32 : lds + zero_off;
+          ET<T>::mma(acc[tt], wb[p], ET<T>::from_lds(xb));
+        }
+        const int nxt = c * HEAD_CK + p + P;
+        wb[p] = ET<T>::load_nt(w0 + (size_t)min(nxt, KT - 1) * 512);   // past the end: never consumed
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (c + 1 < NC) stage_store(c + 1);
+    __syncthreads();
+  }
+
+  // lane (tl, kg) holds features 4kg..4kg+3 of token tt*16+tl: Y[wave][m][16] over the buffers
+  float* Y = reinterpret_cast<float*>(lds);
+#pragma unroll
+  for (int tt = 0; tt < TT; ++tt) {
+    const int m = tt * 16 + tl;
+    if (m < M) {
+      float* dst = Y + ((size_t)wave * M + m) * 16 + 4 * kg;
+      dst[0] = acc[tt][0]; dst[1] = acc[tt][1]; dst[2] = acc[tt][2]; dst[3] = acc[tt][3];
+    }
+  }
+  for (int m = wave; m < M; m += a.NT) {
+    const float r = wave_row_scale(a, m, ssv, pre && m == wave);
+    if (lane == 0) s_rs[m] = r;
+  }
+  __syncthreads();
+  const int per = M * 16;
+  for (int e = tid; e < a.NT * per; e += blockDim.x) {
+    float y = sum_partials(Y + e, 1, per);   // the one k-range, as the narrow kernel adds it
+    y *= s_rs[(e % per) >> 4];
+    Y[e] = y;
+  }
+  __syncthreads();
+  linear_epilogue<T, EPI_HEAD>(a, gr, Y, per, epre);
+}
+
+size_t head_chunked_lds(int M) { return 2 * (size_t)HEAD_CK * 4 * M * 32 + 32; }
+
 // a launch, optionally stamping timing events at the kernel's start and end
 template <typename K, typename... Args>
 static void launch(K kernel, dim3 grid, dim3 block, size_t lds, hipStream_t s, const LaunchEvents* ev, Args... args) {
@@ -726,8 +840,19 @@ static void launch_linear_pe(const LinArgs& a0, int kind, hipStream_t s, const L
   }
   a.NJ = 1;
   const dim3 grid(n_groups), block(64 * a.NT * a.KS);
-  const size_t lds = linear_lds_bytes(a.M, a.K, a.NT, a.KS, a.S, 1, kind);
   const int TT = (a.M + 15) / 16;
+  if constexpr (EPI == EPI_HEAD) {
+    if (a.M > 16 && a.KS == 1 && a.NT == 8 && a.S == 1 && head_chunked_lds(a.M) <= g_lds_limit) {
+      const size_t lds_h = head_chunked_lds(a.M);
+      switch (TT) {
+        case 2: launch(k_linear_head_chunked<T, 2>, grid, block, lds_h, s, ev, a); break;
+        case 3: launch(k_linear_head_chunked<T, 3>, grid, block, lds_h, s, ev, a); break;
+        default: launch(k_linear_head_chunked<T, 4>, grid, block, lds_h, s, ev, a); break;
+      }
+      return;
+    }
+  }
+  const size_t lds = linear_lds_bytes(a.M, a.K, a.NT, a.KS, a.S, 1, kind);
   switch (TT) {
     case 1: launch(k_linear_mfma<T, PRO, EPI, 1>, grid, block, lds, s, ev, a); break;
     case 2: launch(k_linear_mfma<T, PRO, EPI, 2>, grid, block, lds, s, ev, a); break;
@@ -766,6 +891,9 @@ static bool allow_big_lds(int bytes) {
                        reinterpret_cast<const void*>(&k_linear_splitk<T, 3, 8, PRO>),
                        reinterpret_cast<const void*>(&k_linear_splitk<T, 4, 4, PRO>),
                        reinterpret_cast<const void*>(&k_linear_splitk<T, 4, 8, PRO>),
+                       reinterpret_cast<const void*>(&k_linear_head_chunked<T, 2>),
+                       reinterpret_cast<const void*>(&k_linear_head_chunked<T, 3>),
+                       reinterpret_cast<const void*>(&k_linear_head_chunked<T, 4>),
                        reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 1>),
                        reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 2>),
                        reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 3>),
@@ -775,7 +903,6 @@ static bool allow_big_lds(int bytes) {
   return ok;
 }
 
-static size_t g_lds_limit = 65536;
 
 // Dynamic LDS available to one linear workgroup: the device's per-block limit, raised to the
 // opt-in limit when every linear kernel accepted it (failed opt-ins are cleared and ignored).
