@@ -36,6 +36,11 @@
 extern "C" {
 #endif
 
+/* the library is built with hidden host symbols: only the functions declared here are exported */
+#if defined(__GNUC__)
+#pragma GCC visibility push(default)
+#endif
+
 typedef struct seed_ctx seed_ctx;
 
 typedef enum seed_status {
@@ -319,6 +324,10 @@ const char* seed_last_error(void);
 
 /* Release the context (not the caller's buffers). NULL is ignored. */
 void seed_destroy(seed_ctx* ctx);
+
+#if defined(__GNUC__)
+#pragma GCC visibility pop
+#endif
 
 #ifdef __cplusplus
 }

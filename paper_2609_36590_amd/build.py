@@ -19,9 +19,11 @@ OBJ_DIR = os.path.join(ROOT, "_build")
 SOURCES = ["linear.hip", "attention.hip", "misc.hip", "tree.hip", "seed_runtime.cpp"]
 
 # -packed-fp32-ops: keep the compiler from forming packed fp32 VALU instructions.
+# Host symbols are hidden by default: the library exports only the C ABI of include/seed.h.
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-value",
     "-Wno-unused-result", "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-Xarch_host", "-fvisibility=hidden",
     "-I" + os.path.join(ROOT, "include"), "-I" + CSRC,
 ]
 

@@ -829,6 +829,19 @@ seed_status start_sequences(seed_ctx* c, int32_t B, const int32_t* lens, int ext
   return SEED_OK;
 }
 
+// Captures the launches fn() enqueues on the context's stream into an executable graph.
+template <typename F>
+seed_status capture_graph(seed_ctx* c, F&& fn, hipGraphExec_t* ex) {
+  hipGraph_t g = nullptr;
+  HIPCHK(hipStreamBeginCapture(c->s, hipStreamCaptureModeThreadLocal));
+  fn();
+  HIPCHK(hipStreamEndCapture(c->s, &g));
+  const hipError_t e = hipGraphInstantiate(ex, g, nullptr, nullptr, 0);
+  hipGraphDestroy(g);
+  if (e != hipSuccess) return fail(SEED_ERR_HIP, std::string("hipGraphInstantiate: ") + hipGetErrorString(e));
+  return SEED_OK;
+}
+
 template <typename T>
 seed_status run_rounds(seed_ctx* c, int k, int n, bool use_graph) {
   if (!use_graph) {
@@ -839,24 +852,15 @@ seed_status run_rounds(seed_ctx* c, int k, int n, bool use_graph) {
   const auto key = std::make_tuple(c->B, k, c->sim_accept, c->eos);
   auto it = c->graphs.find(key);
   if (it == c->graphs.end()) {
-    hipGraph_t g;
-    HIPCHK(hipStreamBeginCapture(c->s, hipStreamCaptureModeThreadLocal));
-    enqueue_round<T>(c, k, c->sim_accept, true);
-    HIPCHK(hipStreamEndCapture(c->s, &g));
     hipGraphExec_t ex;
-    HIPCHK(hipGraphInstantiate(&ex, g, nullptr, nullptr, 0));
-    HIPCHK(hipGraphDestroy(g));
+    seed_status st = capture_graph(c, [&] { enqueue_round<T>(c, k, c->sim_accept, true); }, &ex);
+    if (st != SEED_OK) return st;
     it = c->graphs.emplace(key, ex).first;
   }
   for (int r = 0; r < n; ++r) HIPCHK(hipGraphLaunch(it->second, c->s));
   return SEED_OK;
 }
 
-}  // namespace
-
-// =============================================================================================
-// C ABI
-// =============================================================================================
 // Tree-based verification of one sequence's packed draft tree (the tree arrays in the workspace):
 // node rows through every layer with the tree attention mask, the LM head (logits optional),
 // then tree acceptance, commit and the move of an accepted leaf's cache entries.
@@ -945,17 +949,6 @@ void enqueue_tree_step(seed_ctx* c, const seed_tree_opts& o, int step, float* lo
   run_head<T>(c, 1, nullptr, p.dstride, logits, (long long)p.V, SEED_PHASE_DRAFT, cap);
   const TreeDraftArgs a = tree_args(c, o, step, logits);
   timed(c, SEED_PHASE_DRAFT, SEED_OP_TOPK, cap, [&](const LaunchEvents*) { launch_tree_topk(a, c->s); });
-}
-
-template <typename F>
-seed_status capture_graph(seed_ctx* c, F&& fn, hipGraphExec_t* ex) {
-  hipGraph_t g;
-  HIPCHK(hipStreamBeginCapture(c->s, hipStreamCaptureModeThreadLocal));
-  fn();
-  HIPCHK(hipStreamEndCapture(c->s, &g));
-  HIPCHK(hipGraphInstantiate(ex, g, nullptr, nullptr, 0));
-  HIPCHK(hipGraphDestroy(g));
-  return SEED_OK;
 }
 
 template <typename T>
@@ -1072,6 +1065,11 @@ seed_status tree_rounds(seed_ctx* c, const seed_tree_opts& o, bool use_graph, in
   return done(SEED_OK);
 }
 
+}  // namespace
+
+// =============================================================================================
+// C ABI
+// =============================================================================================
 extern "C" {
 
 const char* seed_last_error(void) { return g_err.c_str(); }
