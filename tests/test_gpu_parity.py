@@ -13,12 +13,18 @@ from paper_2609_36590_amd import synth
 pytestmark = pytest.mark.gpu
 
 K = 4
+WIDE = synth.C1_TINY.replace(name="wide-4L-h256-f8192", ffn=8192, n_heads=32, n_kv_heads=8, head_dim=128)
 CASES = {
     # name: (config, enc_out_scale, tolerance)
     "tiny-f32": (synth.C1_TINY, 1.0, 1e-4),
     "tiny-f32-damped": (synth.C1_TINY, 0.1, 1e-4),
     "tiny-bf16": (synth.C1_TINY.replace(name="tiny-4L-h256-bf16", dtype=synth.BF16), 1.0, 2e-2),
     "tiny-bf16-damped": (synth.C1_TINY.replace(name="tiny-4L-h256-bf16", dtype=synth.BF16), 0.1, 2e-2),
+    # a wide FFN and 32 query heads: the verification rows' down projection (5 x 8192 and 7 x 8192
+    # activations) is past what the narrow kernel stages whole and runs split-K, while the draft
+    # and plain greedy rows (1 x 8192) stay in the narrow kernel: the bit-exact test compares the two
+    "wide-f32": (WIDE, 1.0, 1e-4),
+    "wide-bf16": (WIDE.replace(name="wide-4L-h256-f8192-bf16", dtype=synth.BF16), 1.0, 2e-2),
 }
 
 

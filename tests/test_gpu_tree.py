@@ -21,6 +21,8 @@ from paper_2609_36590_amd import binding, synth
 pytestmark = pytest.mark.gpu
 
 TINY_BF16 = synth.C1_TINY.replace(name="tiny-4L-h256-bf16", dtype=synth.BF16)
+# a wide FFN and 32 query heads: a depth-1 tree of 11 nodes runs the O and down projections split-K
+WIDE = synth.C1_TINY.replace(name="wide-4L-h256-f8192", ffn=8192, n_heads=32, n_kv_heads=8, head_dim=128)
 
 
 def _swap_chain_with_sibling(tree, d):
@@ -48,7 +50,8 @@ def _oracle_rounds(m, prompt, depth, n_rounds, schedule):
     (synth.C1_TINY, 1e-4, 3, (0, 1, 3, 2)),
     (synth.C1_TINY, 1e-4, 6, (2, 0, 6, 4, 1)),
     (TINY_BF16, 2e-2, 4, (3, 1, 0, 4)),
-], ids=["f32-d3", "f32-d6", "bf16-d4"])
+    (WIDE, 1e-4, 1, (1, 0, 1, 1)),
+], ids=["f32-d3", "f32-d6", "bf16-d4", "wide-f32-d1"])
 def test_tree_rounds_match_oracle(cfg, tol, depth, schedule):
     w = synth.make_weights(cfg, seed=0, enc_out_scale=0.1)
     prompt = synth.make_prompts(cfg)[0]
