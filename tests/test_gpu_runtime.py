@@ -106,6 +106,29 @@ def test_rounds_and_stepwise_calls_agree_with_generate(batch_dec):
         np.testing.assert_array_equal(toks[len(prompts[b]):], ref[b, :total[b]])
 
 
+@pytest.mark.parametrize("B,k", [(4, 15), (64, 0)], ids=["4x16-rows", "64x1-rows"])
+def test_maximum_rows_per_pass(B, k):
+    """Passes of the maximum 64 rows (max_batch * (max_draft + 1)): 4 sequences drafting 15 tokens,
+    and 64 sequences of plain greedy decoding, each against its own decode alone."""
+    cfg = BF16_TINY
+    w = synth.make_weights(cfg, seed=3, enc_out_scale=0.1)
+    dec = decoder(cfg, w, max_batch=B, max_ctx=160, max_draft=k)
+    try:
+        rng = np.random.default_rng(12)
+        prompts = _prompts(cfg, [int(x) for x in rng.integers(1, 100, size=B)], seed=13)
+        say(f"[gpu] {B} sequences, k={k}: {B * (k + 1)} rows per verification")
+        out, cnt, st = dec.generate(prompts, k, 24, log_cap=64)
+        assert (cnt == 24).all()
+        if k:
+            log = st["n_accept_log"]
+            assert log[log >= 0].max() >= 2, "some rounds should accept several drafts"
+        for b in ([0, 1, 2, 3] if B == 4 else [0, 17, 40, 63]):
+            alone, _, _ = dec.generate([prompts[b]], 0, 24)
+            np.testing.assert_array_equal(out[b], alone[0])
+    finally:
+        dec.close()
+
+
 def test_long_context_spans_several_attention_groups():
     """A 700-token context crosses two 256-position group boundaries (cross-group merge)."""
     cfg = synth.C1_TINY
