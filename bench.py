@@ -762,6 +762,15 @@ def main():
         result["measured_acceptance"] = {"tokens_per_s": round(gen / (st4["decode_ms"] * 1e-3), 2),
                                          "mean_accept": round(st4["accepted"] / max(1, st4["rounds"]), 4),
                                          "output_equals_greedy": bool(np.array_equal(out4[0], trace))}
+        # end to end through the C ABI with host buffers: the prompt goes in from host memory and the
+        # tokens come back to it; prefill, every round and both PCIe copies inside the wall clock
+        sync()
+        w0 = time.perf_counter()
+        out5, _, st5 = dec.generate([prompt], k, gen, use_graph=True)
+        w1 = time.perf_counter()
+        result["end_to_end"] = {"tokens_per_s": round(gen / (w1 - w0), 2), "wall_s": round(w1 - w0, 4),
+                                "prefill_ms": round(st5["prefill_ms"], 2), "decode_ms": round(st5["decode_ms"], 2),
+                                "what": f"seed_generate, {P}-token host prompt -> {gen} tokens to host, graph replay"}
 
     dec.close()
     del dec
