@@ -311,6 +311,20 @@ seed_status seed_spec_forward(seed_ctx* ctx, int32_t n, const int32_t* tokens, i
 seed_status seed_get_tokens(seed_ctx* ctx, int32_t b, int32_t* out, int32_t cap, int32_t* len);
 
 /*
+ * Read back the cached keys/values KV^layer of sequence b at positions pos0 .. pos0+n-1 (the
+ * per-layer cache of the Inference Algorithm; inspection and testing, not on the decode path).
+ * k_out, v_out: host [n][n_kv_heads][head_dim], caller-owned, in the cache's element type
+ * (bf16 bit patterns as uint16 for SEED_BF16, float for SEED_F32). Synchronises the context's
+ * stream first, so every queued pass has written its entries. Positions below t_b - 1 hold the
+ * committed deep keys/values; later positions hold whatever the last pass wrote there (draft
+ * entries in the decoder layers, keys/values of rejected verification rows).
+ * Errors: SEED_ERR_STATE before seed_prefill; SEED_ERR_ARG if b or layer is out of range, an
+ * output pointer is NULL, or a position lies outside the cache blocks the sequence holds.
+ */
+seed_status seed_read_kv(seed_ctx* ctx, int32_t b, int32_t layer, int32_t pos0, int32_t n, void* k_out,
+                         void* v_out);
+
+/*
  * Kernel timing for benchmarks: while enabled, every launch of kernel_id (phase * 16 + op) is
  * bracketed by HIP events on the context's stream. seed_kernel_timing_read synchronises the
  * stream and returns the number of timed launches and their summed duration since enabling.

@@ -110,6 +110,23 @@ class Model:
         c = self.cfg
         return rmsnorm(h, self.w["final_norm"], c.rms_eps) @ self.w["embed"].T
 
+    def kv(self, i, h, pos):
+        """Keys and values [n, n_kv, d] that layer f_i produces for rows h [n, H] at absolute
+        positions ``pos``: RMSNorm, the key/value projections, rotary embedding of the keys, and
+        the cache's storage rounding. They depend on the row alone, not on the context."""
+        c = self.cfg
+        W = self.w
+        p = f"layers.{i}."
+        n = h.shape[0]
+        a = rmsnorm(h, W[p + "attn_norm"], c.rms_eps)
+        k = (a @ W[p + "wk"].T).reshape(n, c.n_kv_heads, c.head_dim)
+        v = (a @ W[p + "wv"].T).reshape(n, c.n_kv_heads, c.head_dim)
+        cos, sin = rope_cos_sin(np.asarray(pos, dtype=np.int64), c.head_dim, c.rope_base)
+        k = apply_rope(k, cos, sin)
+        if self.kv_bf16:
+            k, v = round_to_bf16(k), round_to_bf16(v)
+        return k, v
+
     def block(self, i, h, pos, K_prefix, V_prefix):
         """Layer f_i on rows h [n, H] at consecutive absolute positions ``pos``.
 
@@ -205,3 +222,25 @@ def full_forward(model, tokens, return_kv=False, row_block=256):
     if return_kv:
         return logits, Ks, Vs
     return logits
+
+
+def sampled_kv_first_layers(model, tokens, positions):
+    """Keys/values of layers 0 and 1 at a few positions of one sequence, one position at a time.
+
+    Layer 0's keys/values depend on each token alone, so they are formed for every position of
+    the prefix; layer 1's at position j need layer 0's output at j, i.e. one row of layer 0
+    attending to positions 0..j. This reaches long prefixes (16k tokens) that a full forward
+    pass could not. Returns four arrays [len(positions), n_kv, d]: K0, V0, K1, V1.
+    """
+    positions = [int(j) for j in positions]
+    tokens = np.asarray(tokens, dtype=np.int64)
+    n = max(positions) + 1
+    h0 = model.embed(tokens[:n])
+    K0, V0 = model.kv(0, h0, np.arange(n))
+    out = [[], [], [], []]
+    for j in positions:
+        h1, _, _ = model.block(0, h0[j:j + 1], [j], K0[:j], V0[:j])
+        k1, v1 = model.kv(1, h1, [j])
+        for lst, x in zip(out, (K0[j], V0[j], k1[0], v1[0])):
+            lst.append(x)
+    return tuple(np.stack(x) for x in out)

@@ -80,7 +80,7 @@ class SeedStats(ctypes.Structure):
 
 
 EXPORTS = ("seed_arena_bytes", "seed_create", "seed_load_weights", "seed_prefill", "seed_draft",
-           "seed_verify", "seed_rounds", "seed_generate", "seed_get_tokens", "seed_kernel_timing",
+           "seed_verify", "seed_rounds", "seed_generate", "seed_get_tokens", "seed_read_kv", "seed_kernel_timing",
            "seed_kernel_timing_read", "seed_last_error", "seed_destroy", "seed_spec_kv_bytes",
            "seed_spec_forward", "seed_verify_tree", "seed_tree_defaults", "seed_draft_tree",
            "seed_generate_tree")
@@ -119,6 +119,7 @@ def load_library(path: str | None = None):
         "seed_generate": [_P, ctypes.c_int32, _I32P, _I32P, ctypes.POINTER(SeedGenOpts), _I32P, _I32P,
                           ctypes.POINTER(SeedStats)],
         "seed_get_tokens": [_P, ctypes.c_int32, _I32P, ctypes.c_int32, _I32P],
+        "seed_read_kv": [_P, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, _P, _P],
         "seed_kernel_timing": [_P, ctypes.c_int32, ctypes.c_int32],
         "seed_kernel_timing_read": [_P, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_double)],
         "seed_spec_kv_bytes": [ctypes.POINTER(SeedConfig), ctypes.POINTER(ctypes.c_size_t)],
@@ -251,6 +252,20 @@ def seed_get_tokens(ctx: int, b: int, cap: int):
     n = ctypes.c_int32()
     _check(load_library().seed_get_tokens(ctx, b, out.ctypes.data_as(_I32P), cap, ctypes.byref(n)), "seed_get_tokens")
     return out[:min(cap, n.value)]
+
+
+def seed_read_kv(cfg: SeedConfig, ctx: int, b: int, layer: int, pos0: int, n: int):
+    """Cached keys and values of sequence b, layer ``layer``, positions pos0..pos0+n-1, as float32
+    arrays [n, n_kv_heads, head_dim] (bf16 caches are widened exactly)."""
+    shape = (n, cfg.n_kv_heads, cfg.head_dim)
+    dt = np.uint16 if cfg.dtype == BF16 else np.float32
+    k = np.zeros(shape, dtype=dt)
+    v = np.zeros(shape, dtype=dt)
+    _check(load_library().seed_read_kv(ctx, b, layer, pos0, n, k.ctypes.data_as(_P), v.ctypes.data_as(_P)),
+           "seed_read_kv")
+    if dt is np.uint16:
+        return ((k.astype(np.uint32) << 16).view(np.float32), (v.astype(np.uint32) << 16).view(np.float32))
+    return k, v
 
 
 def seed_kernel_timing(ctx: int, kid: int, enable: bool):
@@ -393,6 +408,10 @@ class Decoder:
 
     def tokens(self, b: int):
         return seed_get_tokens(self.ctx, b, self.cfg.max_ctx)
+
+    def read_kv(self, b: int, layer: int, pos0: int, n: int):
+        """Keys, values [n, n_kv_heads, head_dim] (float32) cached for sequence b, layer ``layer``."""
+        return seed_read_kv(self.cfg, self.ctx, b, layer, pos0, n)
 
     def draft_tree(self, opts: SeedTreeOpts, logits: bool = False):
         """One round's dynamic drafting: (tokens, parents, p0 per step, logits [steps, vocab] or None)."""

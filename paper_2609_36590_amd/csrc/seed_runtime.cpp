@@ -1604,6 +1604,40 @@ seed_status seed_get_tokens(seed_ctx* c, int32_t b, int32_t* out, int32_t cap, i
   return SEED_OK;
 }
 
+seed_status seed_read_kv(seed_ctx* c, int32_t b, int32_t layer, int32_t pos0, int32_t n, void* k_out, void* v_out) {
+  if (!c) return fail(SEED_ERR_ARG, "ctx is NULL");
+  if (!c->prefilled) return fail(SEED_ERR_STATE, "call seed_prefill first");
+  const Plan& p = c->p;
+  if (b < 0 || b >= c->B) return fail(SEED_ERR_ARG, "sequence index out of range");
+  if (layer < 0 || layer >= p.L) return fail(SEED_ERR_ARG, "layer out of range");
+  if (!k_out || !v_out) return fail(SEED_ERR_ARG, "k_out and v_out must not be NULL");
+  const int have = (int)c->seq_blocks[b].size() * 16;
+  if (pos0 < 0 || n < 0 || (int64_t)pos0 + n > have)
+    return fail(SEED_ERR_ARG, "positions [" + std::to_string(pos0) + ", " + std::to_string((int64_t)pos0 + n) +
+                                  ") exceed the sequence's cache blocks (" + std::to_string(have) + " positions)");
+  // one block holds K [n_kv][16][hd] then V^T [n_kv][hd][16] of 16 positions
+  const size_t es = p.esize, per = (size_t)p.NKV * 16 * p.HD * es;
+  std::vector<char> blk(2 * per);
+  char* ko = static_cast<char*>(k_out);
+  char* vo = static_cast<char*>(v_out);
+  for (int pos = pos0; pos < pos0 + n;) {
+    const int bi = pos >> 4, id = c->seq_blocks[b][bi];
+    const char* src = c->KV + ((size_t)layer * p.n_blocks + id) * 2 * per;
+    HIPCHK(hipMemcpyAsync(blk.data(), src, 2 * per, hipMemcpyDeviceToHost, c->s));
+    HIPCHK(hipStreamSynchronize(c->s));
+    for (; pos < pos0 + n && (pos >> 4) == bi; ++pos) {
+      const int s = pos & 15;
+      const size_t row = (size_t)(pos - pos0) * p.NKV * p.HD * es;
+      for (int h = 0; h < p.NKV; ++h) {
+        std::memcpy(ko + row + (size_t)h * p.HD * es, blk.data() + ((size_t)h * 16 + s) * p.HD * es, p.HD * es);
+        for (int d = 0; d < p.HD; ++d)
+          std::memcpy(vo + row + ((size_t)h * p.HD + d) * es, blk.data() + per + (((size_t)h * p.HD + d) * 16 + s) * es, es);
+      }
+    }
+  }
+  return SEED_OK;
+}
+
 seed_status seed_kernel_timing(seed_ctx* c, int32_t kernel_id, int32_t enable) {
   if (!c) return fail(SEED_ERR_ARG, "ctx is NULL");
   HIPCHK(drain_timing(c));

@@ -68,3 +68,29 @@ def check_round(dec, prompt, toks, rd, tol, k):
     if np.all(top2_gap(rd.verify_logits) > 2 * tol):
         assert na[0] == rd.n_accept and bo[0] == rd.bonus, (rd.p, na, rd.n_accept, bo, rd.bonus)
     return derr, verr
+
+
+def bf16_ulp(x):
+    """Spacing of bfloat16 values at |x| (8 significand bits): 2^(e - 8) for |x| = m 2^e."""
+    _, e = np.frexp(np.abs(np.asarray(x, dtype=np.float64)))
+    return np.ldexp(1.0, e - 8)
+
+
+def compare_kv(got, ref, bf16, tol32=1e-4, what=""):
+    """Cached keys/values of the GPU against the oracle's. A bf16 cache rounds both sides' fp32
+    values to bfloat16, so an element may differ by one bf16 step where the unrounded values
+    straddle a rounding boundary (plus 1e-3 for the rounding-order noise of values near zero);
+    an fp32 cache is compared within tol32. Returns (max abs error, fraction exactly equal)."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert got.shape == ref.shape, (got.shape, ref.shape)
+    d = np.abs(got - ref)
+    if bf16:
+        bound = bf16_ulp(np.maximum(np.abs(got), np.abs(ref))) + 1e-3
+        worst = float((d - bound).max())
+        assert worst <= 0, (what, worst, float(d.max()))
+    else:
+        assert float(d.max()) <= tol32, (what, float(d.max()))
+    same = float(np.mean(d == 0))
+    say(f"[gpu] {what}: max |kv - oracle| = {d.max():.3g}, {100 * same:.2f}% identical")
+    return float(d.max()), same

@@ -83,6 +83,7 @@ def test_null_arguments(lib):
     assert lib.seed_draft(None, 1, None, None) == -1
     assert lib.seed_verify(None, 1, None, None, None, None) == -1
     assert lib.seed_generate(None, 1, None, None, None, None, None, None) == -1
+    assert lib.seed_read_kv(None, 0, 0, 0, 1, None, None) == -1
     lib.seed_destroy(None)
 
 

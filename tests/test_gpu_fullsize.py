@@ -7,16 +7,22 @@
 * 4B at batch 8 with ragged prompt lengths (uniform in [256, 2048]): the shortest sequence's first
   round against the oracle inside the batch, and every sequence's batched decode bit-exact to the
   same sequence decoded alone and to plain greedy decoding.
-* 4B with a 16384-token prompt: the oracle cannot follow a 16k-token prefill within a test, so
-  this case is checked by properties that hold at any size: the speculative decode equals plain
-  greedy decoding bit for bit, and every verify logit is finite.
+* 4B with a 16384-token prompt: the oracle cannot follow a 16k-token prefill through all 36
+  layers within a test. It forms the first two layers' keys/values at sampled positions one
+  position at a time (layer 1's need one row of layer 0 attending to the whole prefix), and
+  those are compared with the GPU's cache after prefill and one verification: prefill rows and
+  the verification rows at positions 16383..16387, whose layer-1 entries pass through the
+  decode attention over the 16k-token cache. Beyond that, properties that hold at any size:
+  the speculative decode equals plain greedy decoding bit for bit, and every verify logit is
+  finite. The batch-8 case gets the same sampled cache check for its longest sequence.
 
 The oracle runs in float32 on the host; its inputs come from ``synth`` only.
 """
 import numpy as np
 import pytest
 
-from gpu_common import decoder, oracle_model, say, top2_gap
+from gpu_common import compare_kv, decoder, oracle_model, say, top2_gap
+from oracle import model as om
 from oracle import seed as os_
 from paper_2609_36590_amd import synth
 
@@ -61,6 +67,19 @@ def compare_round(rd, d, qlog, na, bo, vlog):
     assert derr <= TOL and verr <= TOL
     if np.all(top2_gap(rd.verify_logits) > 2 * TOL):
         assert na == rd.n_accept and bo == rd.bonus, (na, rd.n_accept, bo, rd.bonus)
+
+
+def check_sampled_kv(cfg, w, dec, b, tokens, positions, m=None):
+    """Layers 0 and 1 of sequence b's cache at ``positions`` against the oracle's, formed one
+    position at a time from ``tokens`` (the committed prefix and the verified drafts)."""
+    m = m if m is not None else oracle_model(cfg, w)
+    say(f"[gpu] oracle layer-0/1 keys/values at {len(positions)} positions of {len(tokens)} tokens")
+    ref = om.sampled_kv_first_layers(m, tokens, positions)
+    for layer in (0, 1):
+        got_k = np.stack([dec.read_kv(b, layer, j, 1)[0][0] for j in positions])
+        got_v = np.stack([dec.read_kv(b, layer, j, 1)[1][0] for j in positions])
+        compare_kv(got_k, ref[2 * layer], True, what=f"layer {layer} keys")
+        compare_kv(got_v, ref[2 * layer + 1], True, what=f"layer {layer} values")
 
 
 def spec_equals_greedy(dec, prompts):
@@ -114,6 +133,10 @@ def test_batch8_ragged_matches_alone_greedy_and_oracle(weights_4b):
         drafts[b] = rd.drafts[1:]
         na, bo, vlog = dec.verify(K, drafts=drafts.astype(np.int32), logits=True)
         compare_round(rd, d[b], qlog[b], int(na[b]), int(bo[b]), vlog[b])
+        bl = int(np.argmax(lens))
+        pl = lens[bl] - 1
+        check_sampled_kv(cfg, weights_4b, dec, bl, np.concatenate([prompts[bl], drafts[bl]]),
+                         [0, 17, pl // 2, pl - 1] + list(range(pl, pl + K + 1)))
         say(f"[gpu] batch generate {N_NEW} tokens each, k={K}")
         out_b, cnt, _ = dec.generate(prompts, K, N_NEW, use_graph=True)
         assert np.all(cnt == N_NEW)
@@ -141,6 +164,9 @@ def test_long_context_16k_spec_equals_greedy(weights_4b):
         d, _ = dec.draft(K)
         _, _, vlog = dec.verify(K, logits=True)
         assert np.all(np.isfinite(vlog))
+        p = len(prompt) - 1
+        check_sampled_kv(cfg, weights_4b, dec, 0, np.concatenate([prompt, d[0]]),
+                         [0, 15, 16, 4095, 8192, 12289, p - 1] + list(range(p, p + K + 1)))
         say(f"[gpu] 16k: generate {N_NEW} tokens, k={K} vs k=0")
         spec_equals_greedy(dec, [prompt])
     finally:

@@ -4,7 +4,8 @@ step-wise calls, and the error paths of the C ABI (state is left unchanged after
 import numpy as np
 import pytest
 
-from gpu_common import decoder, oracle_model, say, top2_gap
+from gpu_common import compare_kv, decoder, oracle_model, say, top2_gap
+from oracle import model as om
 from oracle import seed as os_
 from paper_2609_36590_amd import binding, synth
 
@@ -154,6 +155,38 @@ def test_long_context_spans_several_attention_groups():
         gap_ok = all(top2_gap(vlog) > 2e-4)
         if gap_ok:
             assert g4[0, 0] == ref[0]
+    finally:
+        dec.close()
+
+
+@pytest.mark.parametrize("cfg", [synth.C1_TINY, BF16_TINY], ids=["fp32", "bf16"])
+def test_cache_contents_match_oracle(cfg):
+    """After prefill, a draft and a verification of the oracle's drafts, every layer's cached keys
+    and values of every position 0..p+k (the deep entries verification wrote over the drafts'
+    shallow ones included) equal those of the oracle's full forward over the same tokens; the
+    sequences are ragged and batched, so their blocks interleave in the paged pool."""
+    k = 4
+    w = synth.make_weights(cfg, seed=6)
+    m = oracle_model(cfg, w)
+    prompts = _prompts(cfg, [37, 70, 21], seed=14)
+    dec = decoder(cfg, w, max_batch=3, max_ctx=100, max_draft=k)
+    try:
+        dec.prefill(prompts)
+        d, _ = dec.draft(k)
+        dec.verify(k)
+        for b, pr in enumerate(prompts):
+            toks = np.concatenate([pr, d[b]])
+            _, Ks, Vs = om.full_forward(m, toks, return_kv=True)
+            for layer in range(cfg.n_layers):
+                kg, vg = dec.read_kv(b, layer, 0, len(toks))
+                compare_kv(kg, Ks[layer], cfg.dtype == synth.BF16, what=f"seq {b} layer {layer} keys")
+                compare_kv(vg, Vs[layer], cfg.dtype == synth.BF16, what=f"seq {b} layer {layer} values")
+        with pytest.raises(binding.SeedError) as e:
+            dec.read_kv(0, 0, 0, 1000)
+        assert e.value.status == -1
+        with pytest.raises(binding.SeedError) as e:
+            dec.read_kv(0, cfg.n_layers, 0, 1)
+        assert e.value.status == -1
     finally:
         dec.close()
 

@@ -180,3 +180,34 @@ def test_bf16_model_rounds_kv_only():
     np.testing.assert_array_equal(om.round_to_bf16(V), V)
     d = np.abs(om.full_forward(rounded, toks) - om.full_forward(exact, toks)).max()
     assert 0 < d < 0.2  # bf16 storage is a small but visible perturbation
+
+
+def test_sampled_first_layer_kv_match_hf_llama_cache():
+    # Layer 0 and 1 keys/values formed one position at a time (the route the full-size GPU tests
+    # take at 16k tokens) against the key/value cache of the independent implementation.
+    cfg = TINY_GQA
+    w = synth.make_weights(cfg, seed=5, std=0.2)
+    tokens = np.random.default_rng(6).integers(0, cfg.vocab, size=40)
+    pos = [0, 1, 16, 17, 39]
+    got = om.sampled_kv_first_layers(om.Model(cfg, w, np.float64), tokens, pos)
+    with torch.no_grad():
+        pkv = _hf_llama(cfg, w)(torch.from_numpy(tokens)[None], use_cache=True).past_key_values
+    for layer in (0, 1):
+        for j, name in ((0, "keys"), (1, "values")):
+            t = getattr(pkv.layers[layer], name)                     # [1, n_kv, seq, d]
+            ref = t[0].numpy().transpose(1, 0, 2)[pos]                  # [n, n_kv, d]
+            ours = got[2 * layer + j]
+            err = np.abs(ours - ref).max()
+            assert err <= 2e-5 * max(1.0, np.abs(ref).max()), (layer, name, err)
+
+
+def test_layer_kv_equals_block_keys_values():
+    cfg = TINY_MHA.replace(dtype=synth.BF16)
+    w = synth.weights_as_f32(cfg, synth.make_weights(cfg, seed=2, std=0.2))
+    m = om.Model(cfg, w, np.float64)
+    h = m.embed(np.random.default_rng(4).integers(0, cfg.vocab, size=6))
+    empty = np.zeros((3, cfg.n_kv_heads, cfg.head_dim))
+    _, k, v = m.block(1, h, np.arange(3, 9), empty, empty)
+    k2, v2 = m.kv(1, h, np.arange(3, 9))
+    np.testing.assert_array_equal(k2, k)
+    np.testing.assert_array_equal(v2, v)
