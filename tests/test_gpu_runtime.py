@@ -191,6 +191,30 @@ def test_cache_contents_match_oracle(cfg):
         dec.close()
 
 
+WIDE = synth.C1_TINY.replace(name="wide-4L-h256-f8192", ffn=8192, n_heads=32, n_kv_heads=8, head_dim=128)
+
+
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16], ids=["fp32", "bf16"])
+def test_wide_batch_equals_each_sequence_alone(dtype):
+    """A wide FFN (8192): the batch's verification passes (4 x 5 = 20 rows) run gate/up in the
+    chunked kernel and the other projections split-K, each sequence alone (5 rows) and plain
+    greedy decoding (1 row) the narrow kernels; every sequence's tokens must be identical."""
+    cfg = WIDE.replace(dtype=dtype)
+    w = synth.make_weights(cfg, seed=8)
+    prompts = _prompts(cfg, [30, 19, 41, 26], seed=15)
+    dec = decoder(cfg, w, max_batch=4, max_ctx=120, max_draft=4)
+    try:
+        out, cnt, _ = dec.generate(prompts, 4, 40, use_graph=True)
+        assert np.all(cnt == 40)
+        for i, p in enumerate(prompts):
+            alone, _, _ = dec.generate([p], 4, 40)
+            greedy, _, _ = dec.generate([p], 0, 40)
+            np.testing.assert_array_equal(out[i], alone[0])
+            np.testing.assert_array_equal(out[i], greedy[0])
+    finally:
+        dec.close()
+
+
 def test_error_paths_leave_state_unchanged(batch_dec):
     cfg, w, dec = batch_dec
     lib = binding.load_library()
