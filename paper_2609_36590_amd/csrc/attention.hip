@@ -84,7 +84,7 @@ struct PV<float> {
 enum AttnMode { ATT_CAUSAL = 0, ATT_SPEC = 1, ATT_TREE = 2 };
 
 template <typename T, int HD, int QT, int TPW, int MODE>
-__global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k_attention(AttnArgs a) {
   constexpr bool SPEC = MODE == ATT_SPEC;
   // packed draft tree: a row sees positions below its rotary position (the committed prefix and
   // its ancestors on the top-1 chain) and its own cache slot
@@ -120,21 +120,28 @@ __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
   int blk[TPW];
 #pragma unroll
   for (int t = 0; t < TPW; ++t) blk[t] = btp[(P0 >> 4) + t];
-  // queries (lane column qv = qt*16 + tl, k-slots d = ds*32 + kg*8 + j) and their positions:
-  // loaded branch-free from a valid row, masked when converted
-  float qraw[QT][DS][8];
+  // positions of the lane's query columns qv = qt*16 + tl (loaded from a valid row, masked later)
   int qpos[QT], qstart[QT], qslot[QT];
   bool qok[QT];
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
     const int qv = qt * 16 + tl;
     qok[qt] = qv < nqv;
-    const int rl = qok[qt] ? qv / a.G : 0, gq = qok[qt] ? qv - rl * a.G : 0;
+    const int rl = qok[qt] ? qv / a.G : 0;
     qpos[qt] = a.row_pos[mrow0 + rl];
     qslot[qt] = TREE ? a.row_slot[mrow0 + rl] : 0;
-    const float* qp = a.q + (size_t)(mrow0 + rl) * qstride + (h * a.G + gq) * HD + kg * 8;
+  }
+  // the queries, shared by the 4 waves: thread i loads the 8 values of B-operand slots
+  // i, i + 256, .. (slot (qt, ds, lane) = query column qt*16 + (lane & 15), dims ds*32 +
+  // (lane >> 4)*8 .. +7), branch-free from a valid row
+  constexpr int QSLOTS = QT * DS * 64, QPT = (QSLOTS + 255) / 256;
+  float qraw[QPT][8];
 #pragma unroll
-    for (int ds = 0; ds < DS; ++ds) load8(qp + ds * 32, qraw[qt][ds]);
+  for (int u = 0; u < QPT; ++u) {
+    const int sl = u * 256 + (int)threadIdx.x, sc = sl < QSLOTS ? sl : 0;
+    const int qv = (sc / (DS * 64)) * 16 + (sc & 15), ds = (sc / 64) % DS, kq = (sc >> 4) & 3;
+    const int rl = qv < nqv ? qv / a.G : 0, gq = qv < nqv ? qv - rl * a.G : 0;
+    load8(a.q + (size_t)(mrow0 + rl) * qstride + (h * a.G + gq) * HD + ds * 32 + kq * 8, qraw[u]);
   }
   __builtin_amdgcn_sched_barrier(0);
   const int n_groups = maxpos / SPAN + 1;
@@ -182,8 +189,23 @@ __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
   // for registers and sinks them into the MFMA sequence, one round trip at a time
   __builtin_amdgcn_sched_barrier(0);
 
-  // ---- queries scaled by log2(e)/sqrt(d), as bf16 hi/lo B operands ----
-  typename ET<T>::B qf[QT][DS];
+  // ---- queries scaled by log2(e)/sqrt(d), as bf16 hi/lo B operands, parked in LDS (in the
+  // space of the run partials, which are written only after the last tile) so that the K/V
+  // fragments of every tile fit the registers of two waves per SIMD ----
+  typedef typename ET<T>::B QB;
+  QB* s_q = reinterpret_cast<QB*>(&s_o[0][0][0]);
+  static_assert(QSLOTS * sizeof(QB) <= sizeof(s_o), "query fragments exceed the partial buffer");
+#pragma unroll
+  for (int u = 0; u < QPT; ++u) {
+    const int sl = u * 256 + (int)threadIdx.x;
+    if (sl < QSLOTS) {
+      const bool ok = (sl / (DS * 64)) * 16 + (sl & 15) < nqv;
+      float x[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) x[j] = ok ? qraw[u][j] * a.scale_log2 : 0.f;
+      s_q[sl] = ET<T>::split(x);
+    }
+  }
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
     if (!qok[qt]) {
@@ -192,14 +214,12 @@ __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
     }
     // block-causal pass: positions below qstart come from the deep cache
     qstart[qt] = SPEC ? (qpos[qt] / a.s_block) * a.s_block : 0;
-#pragma unroll
-    for (int ds = 0; ds < DS; ++ds) {
-      float x[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) x[j] = qok[qt] ? qraw[qt][ds][j] * a.scale_log2 : 0.f;
-      qf[qt][ds] = ET<T>::split(x);
-    }
   }
+  __syncthreads();
+  // read per use: an offset the compiler cannot see through keeps it from hoisting the fragments
+  // of every tile into registers (which would cost the second wave per SIMD again)
+  int q_off = 0;
+  auto qf = [&](int qt, int ds) -> QB { return s_q[q_off + (qt * DS + ds) * 64 + lane]; };
 
   // ---- online softmax over the run's tiles, left to right ----
   float m_c[QT], l_c[QT];
@@ -214,6 +234,7 @@ __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
 #pragma unroll
   for (int t = 0; t < TPW; ++t) {
     if (t >= n_live) break;
+    asm volatile("" : "+v"(q_off));
     f32x4 sacc[QT], ssh[QT];
 #pragma unroll
     for (int qt = 0; qt < QT; ++qt) {
@@ -224,14 +245,14 @@ __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
 #pragma unroll
       for (int ds = 0; ds < DS; ++ds)
 #pragma unroll
-        for (int qt = 0; qt < QT; ++qt) ET<T>::mma(sacc[qt], kf[t][ds], qf[qt][ds]);
+        for (int qt = 0; qt < QT; ++qt) ET<T>::mma(sacc[qt], kf[t][ds], qf(qt, ds));
     }
     if constexpr (SPEC) {
       if (need_sh[t]) {
 #pragma unroll
         for (int ds = 0; ds < DS; ++ds)
 #pragma unroll
-          for (int qt = 0; qt < QT; ++qt) ET<T>::mma(ssh[qt], kfs[t][ds], qf[qt][ds]);
+          for (int qt = 0; qt < QT; ++qt) ET<T>::mma(ssh[qt], kfs[t][ds], qf(qt, ds));
       }
     }
     typename PV<T>::B pf[QT], pfs[QT];
@@ -298,6 +319,7 @@ __global__ void __launch_bounds__(256) k_attention(AttnArgs a) {
   // ---- merge the group's 4 runs left to right: every wave parks its run partial in LDS (lane
   // (qv, kg) holds dims dt*16 + 4kg..+3), then thread e merges query vector e / (HD/4),
   // columns 4*(e mod HD/4).., run 0 first ----
+  __syncthreads();   // every wave is done with the query fragments under s_o
 #pragma unroll
   for (int qt = 0; qt < QT; ++qt) {
     const int qv = qt * 16 + tl;
