@@ -8,6 +8,9 @@
 //   O^T += V^T P^T  16x16x16 MFMAs, the block's transposed V as the A operand (k = positions).
 // After S^T, lane (qv, kg) holds the scores of positions 4kg..4kg+3 of the tile for query vector
 // qv, which is exactly the k-slot layout O^T needs for P^T: no cross-lane shuffle of P.
+// The queries' B-operand fragments (bf16 hi/lo) are built once per workgroup into LDS and read
+// per tile, so that a wave's registers hold only its tiles' K/V fragments and two waves fit per
+// SIMD even with 4 tiles per wave and 32 query vectors.
 // Positions later than a query's own are masked; a wave keeps an online softmax (base 2) over its
 // tiles. The 4 waves' partials are merged left to right in LDS and written as the group partial
 // (o, m, l), or as the final output when the pass sees a single group.
@@ -38,6 +41,7 @@ namespace seedk {
 
 static constexpr int ATT_WAVES = 4;
 static constexpr int CMB_LANES = 8;
+static constexpr int CMB_INFLIGHT = 4;   // group partials in flight per lane (8 measured slower)
 
 // 16-position contraction (k = 16) for O^T: 4 stored elements per lane as the A operand, 4 fp32
 // probabilities per lane as the B operand (bf16 hi/lo pair, or fp32 for fp32 caches).
@@ -381,17 +385,17 @@ __global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
   if (n_groups == 1) return;   // k_attention wrote the final output
   const float* pq = a.part + ((((size_t)(b * a.n_kv + h) * a.n_rb + rb) * a.n_groups_max) * 32 + qv) * PS;
   float m_r = NEG_INF, l_r = 0.f, o_r[4] = {0.f, 0.f, 0.f, 0.f};
-  for (int g0 = j; g0 < n_groups; g0 += 4 * CMB_LANES) {
-    float4 ov[4];
-    float2 ml[4];
+  for (int g0 = j; g0 < n_groups; g0 += CMB_INFLIGHT * CMB_LANES) {
+    float4 ov[CMB_INFLIGHT];
+    float2 ml[CMB_INFLIGHT];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < CMB_INFLIGHT; ++u) {
       const float* pp = pq + (size_t)min(g0 + u * CMB_LANES, n_groups - 1) * 32 * PS;
       ov[u] = *reinterpret_cast<const float4*>(pp + d);
       ml[u] = *reinterpret_cast<const float2*>(pp + HD);
     }
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < CMB_INFLIGHT; ++u) {
       if (g0 + u * CMB_LANES < n_groups) {
         const float oc[4] = {ov[u].x, ov[u].y, ov[u].z, ov[u].w};
         softmax_merge(m_r, l_r, o_r, ml[u].x, ml[u].y, oc, 4);
