@@ -658,8 +658,24 @@ __global__ void __launch_bounds__(256) k_argmax_finalize(const float* val, const
 // ---------------------------------------------------------------------------------------------
 // Launchers.
 // ---------------------------------------------------------------------------------------------
-// waves (n-tiles) per workgroup of the split-K kernel
-static constexpr int SPLITK_NT = 8;
+// Waves (n-tiles) per workgroup of the split-K kernel: 8, or fewer (down to 4) where that gives
+// the busiest CU at least 30% fewer weight tiles with the grid's workgroups spread evenly over the
+// 256 CUs: the 2560-wide projections (down: 160 n-tiles x 16 k-ranges make 320 workgroups of 8,
+// so 64 CUs stream two, against 512 of 5, two on every CU; O: 160 workgroups of 8 leave 96 CUs
+// idle, 256 of 5 fill them). Measured: verify down 17.9 -> 16.0 us at 5 rows, O 16.4 -> 15.4 us at
+// 40 rows; QKV (384 n-tiles, 25% by this count) was slower with 6. Each wave's work and summation
+// order are the same for any choice.
+static int splitk_nt(int n_tiles, int ks) {
+  constexpr int CUS = 256;
+  auto cost = [&](int nt) {   // weight tiles per k-range on the busiest CU
+    const long long wgs = (long long)((n_tiles + nt - 1) / nt) * ks;
+    return (wgs + CUS - 1) / CUS * nt;
+  };
+  int best = 8;
+  for (int nt = 7; nt >= 4; --nt)
+    if (cost(nt) < cost(best)) best = nt;
+  return 10 * cost(best) <= 7 * cost(8) ? best : 8;
+}
 
 size_t linear_lds_bytes(int M, int K, int NT, int KS, int S, int NJ, int kind) {
   (void)S;
@@ -812,9 +828,9 @@ static void launch_linear_pe(const LinArgs& a0, int kind, hipStream_t s, const L
   if (kind == LIN_SPLITK) {
     const int nk_max = ((a.K >> 5) + a.KS - 1) / a.KS;
     LinArgs b = a;
-    b.NT = SPLITK_NT;
+    b.NT = splitk_nt(n_tiles, a.KS);
     b.NJ = 1;
-    const dim3 grid((n_tiles + SPLITK_NT - 1) / SPLITK_NT, a.KS), block(64 * SPLITK_NT);
+    const dim3 grid((n_tiles + b.NT - 1) / b.NT, a.KS), block(64 * b.NT);
     const size_t lds = (size_t)nk_max * 4 * a.M * 32 + 64;   // + zero slot + dummy slot
     const LaunchEvents e0{ev ? ev->start : nullptr, nullptr}, e1{nullptr, ev ? ev->stop : nullptr};
     const int xi = (nk_max * 4 * a.M + (int)block.x - 1) / (int)block.x <= 4 ? 4 : 8;
