@@ -556,6 +556,8 @@ def main():
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--profile-run", action="store_true",
                     help="only prefill + eager rounds (for rocprofv3 counter passes)")
+    ap.add_argument("--profile-drafts", type=int, default=0,
+                    help="with --profile-run: this many eager seed_draft calls (k steps each) after the rounds")
     ap.add_argument("--copy-calib", action="store_true",
                     help="only a plain 1 GiB device-to-device copy (counter calibration)")
     ap.add_argument("--config-sweep", metavar="OUT_MD",
@@ -618,9 +620,13 @@ def main():
         sync()
         t0 = time.perf_counter()
         binding.seed_rounds(ctx, k, args.steps, False)
+        for _ in range(args.profile_drafts):
+            dec.draft(k)
         sync()
-        log(f"[bench] profile run: {args.steps} eager rounds in {(time.perf_counter() - t0) * 1e3:.1f} ms")
-        print(json.dumps({"profile_run": cfg.name, "k": k, "rounds": args.steps}), flush=True)
+        log(f"[bench] profile run: {args.steps} eager rounds and {args.profile_drafts} draft calls in "
+            f"{(time.perf_counter() - t0) * 1e3:.1f} ms")
+        print(json.dumps({"profile_run": cfg.name, "k": k, "rounds": args.steps, "draft_calls": args.profile_drafts,
+                          "t_end": int(len(dec.tokens(0)))}), flush=True)
         return
 
     # ---------------- timed rounds (graph replay) ----------------

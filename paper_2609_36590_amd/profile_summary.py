@@ -12,7 +12,10 @@ kernel and launch shape, the mean value of each collected counter per dispatch.
 
        python3 paper_2609_36590_amd/profile_summary.py --traffic <dir> <kernel> <name-substring> <grid> <lds> <out.md>
 
-writes the HBM-traffic summary that bench.py reads for `roofline.traffic`, from the four runs
+       python3 paper_2609_36590_amd/profile_summary.py --step-traffic <dir> <out.md>
+
+--step-traffic writes the counted HBM bytes per decode round, verification and draft step (see
+step_traffic). --traffic writes the HBM-traffic summary that bench.py reads for `roofline.traffic`, from the four runs
 <dir>/pmc_copy_{FETCH,WRITE}_SIZE and <dir>/pmc_bench_{FETCH,WRITE}_SIZE (see the commands in the
 written file): the dominant kernel's per-dispatch FETCH_SIZE and WRITE_SIZE, each scaled by what
 the counter reads for the plain 1 GiB copy, stamped with the hash of the kernel sources.
@@ -106,8 +109,95 @@ def traffic(argv):
     print(json.dumps(rec))
 
 
+STEP_COMMANDS = """```
+cd /tmp && export TMPDIR=/tmp && cd <repository root>
+for c in FETCH_SIZE WRITE_SIZE; do
+  timeout -s KILL 120 rocprofv3 --pmc $c -d gpurun_out/pmc_copy_$c -o run -- python3 bench.py --copy-calib
+  timeout -s KILL 300 rocprofv3 --pmc $c -d gpurun_out/pmc_r10_$c -o run -- python3 bench.py --profile-run --steps 10 --warmup 5
+  timeout -s KILL 300 rocprofv3 --pmc $c -d gpurun_out/pmc_r30_$c -o run -- python3 bench.py --profile-run --steps 30 --warmup 5
+  timeout -s KILL 300 rocprofv3 --pmc $c -d gpurun_out/pmc_r10d20_$c -o run -- python3 bench.py --profile-run --steps 10 --warmup 5 --profile-drafts 20
+done
+python3 paper_2609_36590_amd/profile_summary.py --step-traffic gpurun_out {out}
+```"""
+
+
+def group_sums(path):
+    """Sum of the counter (KiB) over all dispatches, per kernel and launch shape."""
+    db = sqlite3.connect(path)
+    rows = db.execute("select kernel_name, grid_size, workgroup_size, lds_block_size, sum(value), count(*) "
+                      "from counters_collection group by kernel_name, grid_size, workgroup_size, lds_block_size")
+    return {(n, g, w, l): (v, c) for (n, g, w, l, v, c) in rows}
+
+
+def step_traffic(argv):
+    """HBM bytes per decode step from the counters of three profile runs that differ only in the
+    number of rounds (10 vs 30) or in 20 extra draft calls: the prefill and the warm-up cancel
+    in the differences. Per round = (r30 - r10) / 20, per draft step = (r10d20 - r10) / (20 k),
+    per verification = per round - k draft steps."""
+    d, out = argv[0], argv[1]
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    sys.path.insert(0, root)
+    import bench
+    from paper_2609_36590_amd import synth
+
+    k = 4
+    run = lambda c: os.path.join(d, f"pmc_{c}", "run_results.db")
+    scale = {}
+    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+        v, _ = counter_mean(run(f"copy_{c}"), "copyBuffer")
+        scale[c] = COPY_BYTES / 1024 / v   # bytes of a copy per KiB the counter reads
+    per = {}   # group -> [round bytes, draft-call bytes]
+    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+        a, b, e = group_sums(run(f"r10_{c}")), group_sums(run(f"r30_{c}")), group_sums(run(f"r10d20_{c}"))
+        for key in set(a) | set(b) | set(e):
+            va, vb, ve = (x.get(key, (0.0, 0))[0] for x in (a, b, e))
+            r = (vb - va) / 20 * 1024 * scale[c]
+            dc = (ve - va) / 20 * 1024 * scale[c]
+            acc = per.setdefault(key, [0.0, 0.0])
+            acc[0] += r
+            acc[1] += dc
+    rnd = sum(v[0] for v in per.values())
+    dcall = sum(v[1] for v in per.values())
+    dstep = dcall / k
+    ver = rnd - k * dstep
+    cfg = synth.C3_4B
+    L = cfg.prompt_len + 25
+    alg_v = bench.step_bytes(cfg, k + 1, L, cfg.n_layers)
+    alg_d = bench.step_bytes(cfg, 1, L, cfg.n_dec_layers)
+    lines = ["# HBM traffic per decode step from rocprofv3 counters: 4B-36L-h2560, batch 1, k = 4", "",
+             "FETCH_SIZE and WRITE_SIZE summed over every kernel dispatch of three profile runs (prefill, 5",
+             "warm-up rounds, then 10 rounds; 30 rounds; 10 rounds and 20 eager draft calls of k = 4 steps),",
+             "each scaled by what the counter reads for a plain 1 GiB copy "
+             f"(FETCH x {scale['FETCH_SIZE']:.5f}, WRITE x {scale['WRITE_SIZE']:.5f}). The prefill and the warm-up "
+             "cancel in the differences: per round = (30 rounds - 10 rounds) / 20, per draft step = (extra",
+             "draft calls) / (20 k), per verification = per round - k draft steps. Algorithmic bytes at the",
+             f"runs' mean context (~{L} positions): verification {alg_v / 1e9:.4f} GB, draft step {alg_d / 1e9:.4f} GB.",
+             "", "| | counted HBM bytes | algorithmic bytes | counted / algorithmic |", "|---|---|---|---|",
+             f"| round (k draft steps + verification) | {rnd / 1e9:.4f} GB | {(alg_v + k * alg_d) / 1e9:.4f} GB | "
+             f"{rnd / (alg_v + k * alg_d):.3f} |",
+             f"| verification | {ver / 1e9:.4f} GB | {alg_v / 1e9:.4f} GB | {ver / alg_v:.3f} |",
+             f"| draft step | {dstep / 1e9:.4f} GB | {alg_d / 1e9:.4f} GB | {dstep / alg_d:.3f} |", "",
+             "Per kernel and launch shape (MB per round; MB per draft call of k steps):", "", "```",
+             f"{'kernel':60s} {'grid':>9s} {'wg':>5s} {'lds':>6s} {'MB/round':>10s} {'MB/draft call':>14s}"]
+    for key, (r, dc) in sorted(per.items(), key=lambda kv: -kv[1][0]):
+        if abs(r) < 0.05e6 and abs(dc) < 0.05e6:
+            continue
+        name = key[0].replace("seedk::", "").replace("unsigned short", "bf16").replace("void ", "")
+        name = name.replace("(seedk::LinArgs)", "").replace("(seedk::AttnArgs)", "").split("(")[0]
+        lines.append(f"{name[:60]:60s} {key[1]:9d} {key[2]:5d} {key[3]:6d} {r / 1e6:10.2f} {dc / 1e6:14.2f}")
+    lines += ["```", "", "Commands (one MI355X, library built by `__graft_entry__.build()`):", "",
+              STEP_COMMANDS.format(out=out), ""]
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print(json.dumps({"round_bytes": rnd, "verify_bytes": ver, "draft_step_bytes": dstep,
+                      "alg_verify": alg_v, "alg_draft": alg_d}))
+
+
 def main():
     args = sys.argv[1:]
+    if args and args[0] == "--step-traffic":
+        step_traffic(args[1:])
+        return
     if args and args[0] == "--traffic":
         traffic(args[1:])
         return
