@@ -4,7 +4,7 @@ step-wise calls, and the error paths of the C ABI (state is left unchanged after
 import numpy as np
 import pytest
 
-from gpu_common import compare_kv, decoder, oracle_model, say, top2_gap
+from gpu_common import compare_kv, decoder, first_ambiguous, oracle_model, say, top2_gap
 from oracle import model as om
 from oracle import seed as os_
 from paper_2609_36590_amd import binding, synth
@@ -187,6 +187,38 @@ def test_cache_contents_match_oracle(cfg):
         with pytest.raises(binding.SeedError) as e:
             dec.read_kv(0, cfg.n_layers, 0, 1)
         assert e.value.status == -1
+    finally:
+        dec.close()
+
+
+def test_one_token_prompts_and_one_new_token():
+    """Degenerate lengths: prompts of 1 and 2 tokens (no cache entry exists before the first
+    verification; the first drafts attend only to their own entries) batched with a 17-token one,
+    and a single generated token. Speculative decoding equals plain greedy decoding bit for bit,
+    and each sequence follows the oracle's Algorithm 2 (logits of the first verification within
+    1e-4; tokens up to the first round whose top-2 gap is within twice that)."""
+    cfg, k, n = synth.C1_TINY, 4, 12
+    w = synth.make_weights(cfg, seed=9)
+    m = oracle_model(cfg, w)
+    prompts = _prompts(cfg, [1, 2, 17], seed=16)
+    dec = decoder(cfg, w, max_batch=3, max_ctx=40, max_draft=k)
+    try:
+        out, cnt, _ = dec.generate(prompts, k, n)
+        greedy, _, _ = dec.generate(prompts, 0, n)
+        assert np.all(cnt == n)
+        np.testing.assert_array_equal(out, greedy)
+        for i, p in enumerate(prompts):
+            ref, rounds = os_.generate(m, p, k, n, record=True)
+            n_ok = first_ambiguous(rounds, 1e-4)
+            upto = (rounds[n_ok].p + 1 - len(p)) if n_ok < len(rounds) else n
+            say(f"[gpu] prompt of {len(p)} tokens: {upto} of {n} tokens compared with the oracle")
+            np.testing.assert_array_equal(out[i, :upto], ref[:upto])
+            rd = rounds[0]
+            dec.prefill([p])
+            _, _, vlog = dec.verify(k, drafts=np.asarray(rd.drafts[1:], np.int32)[None], logits=True)
+            assert float(np.abs(vlog[0] - rd.verify_logits).max()) <= 1e-4
+            one, c1, _ = dec.generate([p], k, 1)
+            assert c1[0] == 1 and one[0, 0] == greedy[i, 0]
     finally:
         dec.close()
 
