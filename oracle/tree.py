@@ -13,8 +13,10 @@ Readings (where the paper leaves the procedure open):
   further; the other candidates are leaves.
 * Stop rule: drafting stops after a step whose top-1 probability is below tau (that step's
   candidates are still verified), and after max_depth steps.
-* Node budget (the paper sets none): a tree holds at most max_nodes nodes, root included; a step's
-  fan-out is cut to the nodes left and drafting stops once none are left.
+* Node budget: the paper sets none, so by default a tree is unbounded. A caller comparing with an
+  implementation that verifies at most N rows in one pass passes max_nodes = N: a tree then holds
+  at most N nodes, root included, a step's fan-out is cut to the nodes left and drafting stops
+  once none are left.
 * Packing: node 0 is the pending token X[p] (the root), then the top-1 chain in depth order, then
   the other candidates by depth and rank. Node i sits at rotary position p + depth(i).
 * Verification: one full-model pass over the packed nodes; node i attends to the committed prefix
@@ -69,9 +71,20 @@ def _ranked(logits):
     return np.lexsort((np.arange(len(z)), -z))
 
 
-def draft_tree(st, tau, max_depth, table=FANOUT, rest=FANOUT_REST, max_nodes=64):
+def _confidence(logits):
+    """Top-1 probability p0 of one drafting step's logits (softmax in float64) and the token ids
+    ranked by decreasing logit (ties to the lower id)."""
+    z = np.asarray(logits, dtype=np.float64)
+    pr = np.exp(z - z.max())
+    pr /= pr.sum()
+    order = _ranked(z)
+    return float(pr[order[0]]), order
+
+
+def draft_tree(st, tau, max_depth, table=FANOUT, rest=FANOUT_REST, max_nodes=None):
     """Dynamic drafting: decoder-only steps from the pending token (Eq. 5, as in Algorithm 2),
-    each expanded into top-p candidates; stops by the confidence threshold tau or at max_depth."""
+    each expanded into top-p candidates; stops by the confidence threshold tau or at max_depth
+    (or, when max_nodes is given, once the tree holds max_nodes nodes)."""
     m = st.model
     dec = range(m.first_decoder_layer, m.n_layers)
     chain = [st.tokens[-1]]
@@ -81,18 +94,17 @@ def draft_tree(st, tau, max_depth, table=FANOUT, rest=FANOUT_REST, max_nodes=64)
         h = m.embed([chain[i - 1]])
         h = run_layers(m, st.cache, dec, h, st.p + i - 1)
         q = m.head(h)[0]
-        z = q.astype(np.float64)
-        pr = np.exp(z - z.max())
-        pr /= pr.sum()
-        order = _ranked(q)
-        p0 = float(pr[order[0]])
-        cands = [int(x) for x in order[:min(fanout(p0, table, rest), max_nodes - nodes)]]
+        p0, order = _confidence(q)
+        k = fanout(p0, table, rest)
+        if max_nodes is not None:
+            k = min(k, max_nodes - nodes)
+        cands = [int(x) for x in order[:k]]
         nodes += len(cands)
         steps.append(cands)
         p0s.append(p0)
         logits.append(q)
         chain.append(cands[0])
-        if p0 < tau or nodes >= max_nodes:
+        if p0 < tau or (max_nodes is not None and nodes >= max_nodes):
             break
     tokens, parents, depths, chain_nodes = [chain[0]], [-1], [0], [0]
     for d, cands in enumerate(steps, 1):
@@ -205,10 +217,11 @@ class TreeRound:
 
 
 def generate_tree(model, prompt, tau, max_depth, max_new, table=FANOUT, rest=FANOUT_REST, record=False,
-                  capacity=None, max_nodes=64):
+                  capacity=None, max_nodes=None):
     """Dynamic drafting with tree verification end to end: returns (new tokens, rounds)."""
     t0 = len(prompt)
-    cap = capacity or (t0 + max_new + max_nodes + 2)
+    most = 1 + max_depth * max([k for _, k in table] + [rest])   # nodes of one unbounded tree
+    cap = capacity or (t0 + max_new + (most if max_nodes is None else min(most, max_nodes)) + 2)
     st = prefill(model, [int(x) for x in prompt], cap)
     rounds = []
     while st.t - t0 < max_new:

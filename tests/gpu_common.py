@@ -13,6 +13,11 @@ from oracle import seed as os_
 from paper_2609_36590_amd import binding, synth
 
 
+# rows one GPU pass verifies at most (seed_config: max_batch * (max_draft + 1) <= 64); a draft
+# tree compared with the GPU's is built by the oracle under the same node budget
+GPU_ROWS = 64
+
+
 def say(*a):
     print(*a, flush=True)
     sys.stdout.flush()

@@ -21,7 +21,7 @@ The oracle runs in float32 on the host; its inputs come from ``synth`` only.
 import numpy as np
 import pytest
 
-from gpu_common import compare_kv, decoder, oracle_model, say, top2_gap
+from gpu_common import GPU_ROWS, compare_kv, decoder, oracle_model, say, top2_gap
 from oracle import model as om
 from oracle import seed as os_
 from paper_2609_36590_amd import synth
@@ -213,7 +213,7 @@ def test_tree_round_matches_oracle_at_full_size(weights_4b):
         toks, par, p0, dlog = dec.draft_tree(binding.tree_opts(K), logits=True)
         say(f"[gpu] oracle prefill {cfg.name} over {len(prompt)} tokens")
         st = os_.prefill(m, prompt, len(prompt) + 70)
-        tree = ot.draft_tree(st, 0.7, K)
+        tree = ot.draft_tree(st, 0.7, K, max_nodes=GPU_ROWS)
         derr = float(np.abs(dlog[0] - tree.draft_logits[0]).max())
         say(f"[gpu] step 1: p0 {p0[0]:.4g} vs {tree.p0[0]:.4g}, max |draft - oracle| = {derr:.3g}, "
             f"{len(toks)} vs {len(tree.tokens)} nodes")
@@ -224,7 +224,7 @@ def test_tree_round_matches_oracle_at_full_size(weights_4b):
             assert toks == tree.tokens and par == tree.parents
         # a wide tree through the GPU's verification (drafting again from the committed prefix)
         st.cache.truncate(st.t - 1)
-        wide = ot.draft_tree(st, 0.0, 3)
+        wide = ot.draft_tree(st, 0.0, 3, max_nodes=GPU_ROWS)
         assert len(wide.tokens) == 31
         logits, _ = ot.verify_tree(st, wide)
         path, bonus = ot.accept_tree(wide, logits)

@@ -12,7 +12,7 @@ doubt.
 import numpy as np
 import pytest
 
-from gpu_common import decoder, oracle_model, say, top2_gap
+from gpu_common import GPU_ROWS, decoder, oracle_model, say, top2_gap
 from oracle import model as om
 from oracle import seed as os_
 from oracle import tree as ot
@@ -36,7 +36,7 @@ def _oracle_rounds(m, prompt, depth, n_rounds, schedule):
     st = os_.prefill(m, [int(x) for x in prompt], len(prompt) + n_rounds * (depth + 1) + 70)
     rounds = []
     for r in range(n_rounds):
-        tree = ot.draft_tree(st, 0.0, depth)
+        tree = ot.draft_tree(st, 0.0, depth, max_nodes=GPU_ROWS)
         if schedule[r % len(schedule)]:
             _swap_chain_with_sibling(tree, schedule[r % len(schedule)])
         logits, kv = ot.verify_tree(st, tree)
@@ -170,7 +170,7 @@ def test_drafting_matches_oracle(cfg, tol, tau, depth):
         dec.prefill([prompt])
         same_trees, levels, worst = 0, set(), 0.0
         for r in range(n_rounds):
-            tree = ot.draft_tree(st, tau, depth)
+            tree = ot.draft_tree(st, tau, depth, max_nodes=GPU_ROWS)
             toks, par, p0, lg = dec.draft_tree(opts, logits=True)
             say(f"[gpu] round {r}: oracle {len(tree.tokens)} nodes / {len(tree.p0)} steps, "
                 f"GPU {len(toks)} nodes / {len(p0)} steps")
@@ -229,7 +229,7 @@ def test_generate_tree_is_lossless(cfg, tol, tau, depth, graph):
         np.testing.assert_array_equal(toks[:n_ok], ref[0][:n_ok])
         assert st["accepted"] > 0
         # the oracle's rounds, compared while every draft and verification decision is clear
-        _, rounds = ot.generate_tree(m, prompt, tau, depth, max_new, record=True)
+        _, rounds = ot.generate_tree(m, prompt, tau, depth, max_new, record=True, max_nodes=GPU_ROWS)
         log = st["n_accept_log"]
         compared, t_gpu, t_or = 0, 0, 0
         for i, rd in enumerate(rounds):

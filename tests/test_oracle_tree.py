@@ -88,3 +88,57 @@ def test_siblings_are_leaves_and_packed_after_the_chain():
     for i in range(len(chain), len(tree.tokens)):
         assert tree.parents[i] in chain and all(tree.parents[j] != i for j in range(len(tree.tokens)))
         assert tree.depths[i] == tree.depths[tree.parents[i]] + 1
+
+
+def test_ranking_breaks_ties_to_the_lower_id():
+    z = np.array([1.0, 3.0, 3.0, 2.0, 3.0, -1.0])
+    p0, order = ot._confidence(z)
+    assert list(order) == [1, 2, 4, 3, 0, 5]
+    e = np.exp(z - 3.0)
+    assert abs(p0 - 1.0 / e.sum()) < 1e-15
+
+
+@pytest.mark.parametrize("gain,tau,depth", [(1.0, 0.0, 3), (8.0, 0.0, 4), (20.0, 0.7, 6), (40.0, 0.5, 6),
+                                            (60.0, 0.0, 5)])
+def test_drafting_steps_match_an_independent_softmax_and_sort(gain, tau, depth):
+    """p0, fan-out, candidates and the tau stop of every drafting step against a torch float64
+    softmax and a stable torch sort of the recorded drafter logits; the final-norm gain scales the
+    logits so that p0 moves across the top-p table's levels."""
+    from tree_pins import check_drafting_steps
+    cfg = SMALL.replace(n_dec_layers=2)
+    w = synth.make_weights(cfg, seed=0, std=0.2, enc_out_scale=0.3)
+    w["final_norm"] = w["final_norm"] * gain
+    m = om.Model(cfg, w, np.float64)
+    seen = set()
+    for seed in range(4):
+        st = os_.prefill(m, _prompt(9, seed=20 + seed), 96)
+        tree = ot.draft_tree(st, tau, depth)
+        seen.update(check_drafting_steps(tree, tau, depth, ot.FANOUT, ot.FANOUT_REST))
+    assert seen
+
+
+def test_every_fanout_level_is_exercised():
+    """Across the scaled models of the test above, every level of the table (1, 3, 5, 10) occurs."""
+    from tree_pins import check_drafting_steps
+    cfg = SMALL.replace(n_dec_layers=2)
+    seen = set()
+    for gain in (1.0, 8.0, 20.0, 40.0, 60.0):
+        w = synth.make_weights(cfg, seed=0, std=0.2, enc_out_scale=0.3)
+        w["final_norm"] = w["final_norm"] * gain
+        m = om.Model(cfg, w, np.float64)
+        for seed in range(4):
+            st = os_.prefill(m, _prompt(9, seed=20 + seed), 96)
+            seen.update(check_drafting_steps(ot.draft_tree(st, 0.0, 6), 0.0, 6, ot.FANOUT, ot.FANOUT_REST))
+    assert seen >= {1, 3, 5, 10}, seen
+
+
+def test_unbounded_by_default_and_budget_when_asked():
+    """The paper sets no node budget: a depth-6 tree at fan-out 10 holds 61 nodes by default, and a
+    budget of 20 cuts the fan-out to the nodes left and stops drafting once none are left."""
+    m = _model()
+    st = os_.prefill(m, _prompt(7, seed=6), 96)
+    full = ot.draft_tree(st, 0.0, 6)
+    assert len(full.tokens) == 1 + 6 * 10
+    st.cache.truncate(st.t - 1)     # drop the shallow entries of the first drafting (Alg. 2's truncate)
+    cut = ot.draft_tree(st, 0.0, 6, max_nodes=20)
+    assert len(cut.tokens) == 20 and len(cut.p0) == 2

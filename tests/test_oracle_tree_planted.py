@@ -144,3 +144,64 @@ def test_committing_packed_rows_breaks_lossless_pin(monkeypatch):
             caught = True
             break
     assert leaf_rounds > 0 and caught
+
+
+def _confidence_pin_fails(monkeypatch, bad_confidence):
+    """Plant bad_confidence as the drafting step's (p0, ranking) and report whether the
+    independent softmax/sort pin (tests/tree_pins.py) rejects the drafted trees."""
+    from tree_pins import check_drafting_steps
+    monkeypatch.setattr(ot, "_confidence", bad_confidence)
+    cfg = SMALL.replace(n_dec_layers=2)
+    for gain in (1.0, 20.0, 40.0):
+        w = synth.make_weights(cfg, seed=0, std=0.2, enc_out_scale=0.3)
+        w["final_norm"] = w["final_norm"] * gain
+        m = om.Model(cfg, w, np.float64)
+        for seed in range(4):
+            st = os_.prefill(m, _prompt(9, 20 + seed), 96)
+            tree = ot.draft_tree(st, 0.5, 5)
+            try:
+                check_drafting_steps(tree, 0.5, 5, ot.FANOUT, ot.FANOUT_REST)
+            except AssertionError:
+                return True
+    return False
+
+
+def test_p0_from_the_second_ranked_token_breaks_confidence_pin(monkeypatch):
+    # p0 read at rank 2 (the ranking itself right): every existing losslessness pin still passes,
+    # the independent recomputation of p0 does not
+    good = ot._confidence
+
+    def second(logits):
+        _, order = good(logits)
+        z = np.asarray(logits, dtype=np.float64)
+        pr = np.exp(z - z.max())
+        pr /= pr.sum()
+        return float(pr[order[1]]), order
+
+    assert _confidence_pin_fails(monkeypatch, second)
+
+
+def test_coarse_ranking_with_ties_to_the_higher_id_breaks_confidence_pin(monkeypatch):
+    # the ranking taken over logits coarsened to quarters (so candidates tie) with ties broken
+    # towards the higher token id; the tie rule itself is pinned directly in
+    # test_oracle_tree.py::test_ranking_breaks_ties_to_the_lower_id
+    def higher_first(logits):
+        z = np.asarray(logits, dtype=np.float64)
+        z = np.round(z * 4.0) / 4.0          # coarse logits: many exact ties among candidates
+        pr = np.exp(z - z.max())
+        pr /= pr.sum()
+        order = np.lexsort((-np.arange(len(z)), -z))
+        return float(pr[order[0]]), order
+
+    assert _confidence_pin_fails(monkeypatch, higher_first)
+
+
+def test_candidates_from_the_lowest_logits_break_confidence_pin(monkeypatch):
+    # ranking reversed: the fan-out's candidates taken from the bottom of the distribution
+    good = ot._confidence
+
+    def reversed_rank(logits):
+        p0, order = good(logits)
+        return p0, order[::-1]
+
+    assert _confidence_pin_fails(monkeypatch, reversed_rank)
