@@ -128,6 +128,13 @@ typedef struct seed_stats {
   int32_t* n_accept_log;     /* nullable host [n_accept_log_cap * B]: n_accept per round per
                                 sequence, -1 once a sequence has finished */
   int64_t n_accept_log_cap;  /* rows available in n_accept_log */
+  /* Step latencies, medians over the rounds of the call, from the device's constant-rate clock
+   * stamped by the kernels that open and close each phase inside the (graph-replayed) rounds:
+   * verify_ms = one verification (row setup to acceptance and commit); draft_ms = one drafting
+   * step of seed_generate (the k-step drafting phase / k; 0 when k = 0) or, for
+   * seed_generate_tree, one round's whole drafting phase (its step count varies). */
+  double verify_ms;
+  double draft_ms;
 } seed_stats;
 
 /* Kernel ids for seed_kernel_timing: phase * 16 + op. SEED_OP_ATTN times the attention partial
@@ -296,7 +303,8 @@ seed_status seed_generate_tree(seed_ctx* ctx, const int32_t* tokens, int32_t len
  * s = floor(q / block) * block) attends causally to the rows s..q of its own block and to the
  * deep decoder keys/values of positions < s, and predicts X[q+1]. Forward only.
  * shallow_kv: device, at least seed_spec_kv_bytes bytes, 256-byte aligned, caller-owned: the
- *             decoder layers' keys/values of this pass (its contents are scratch).
+ *             decoder layers' keys/values of this pass (scratch: the call clears it first, so
+ *             its prior contents never matter).
  * logits: device [(n-1) * vocab], the drafter's logits of every row (required).
  * row_nll: nullable device [n-1]: -log softmax(logits[q])[X[q+1]].
  * loss: nullable host: L_spec = the sum of row_nll (accumulated in double on the host).

@@ -58,11 +58,19 @@ class State:
         return self.t - 1
 
 
-def prefill(model, prompt, capacity):
-    """Initialise KV_{1:t} with (f_dec o f_enc)(X_{1:t}), then keep positions [0, t-1) (Alg. 2)."""
+def prefill(model, prompt, capacity, row_block=None):
+    """Initialise KV_{1:t} with (f_dec o f_enc)(X_{1:t}), then keep positions [0, t-1) (Alg. 2).
+
+    With ``row_block`` the prompt's rows go through the layers ``row_block`` rows at a time (each
+    block after the earlier blocks filled the cache): every row still attends to exactly the
+    positions up to its own, so the cache is the same; only the memory of the score matrices is
+    bounded (a 16384-token prompt)."""
     st = State(model, prompt, capacity)
-    h = model.embed(st.tokens)
-    run_layers(model, st.cache, range(model.n_layers), h, 0)
+    n = len(st.tokens)
+    step = n if row_block is None else row_block
+    for s in range(0, n, step):
+        h = model.embed(st.tokens[s:s + step])
+        run_layers(model, st.cache, range(model.n_layers), h, s)
     st.cache.truncate(st.t - 1)
     return st
 

@@ -76,7 +76,8 @@ def tree_opts(max_depth: int, tau: float | None = None, table=None, rest: int | 
 class SeedStats(ctypes.Structure):
     _fields_ = [("rounds", ctypes.c_int64), ("drafted", ctypes.c_int64), ("accepted", ctypes.c_int64),
                 ("prefill_ms", ctypes.c_double), ("decode_ms", ctypes.c_double),
-                ("n_accept_log", ctypes.POINTER(ctypes.c_int32)), ("n_accept_log_cap", ctypes.c_int64)]
+                ("n_accept_log", ctypes.POINTER(ctypes.c_int32)), ("n_accept_log_cap", ctypes.c_int64),
+                ("verify_ms", ctypes.c_double), ("draft_ms", ctypes.c_double)]
 
 
 EXPORTS = ("seed_arena_bytes", "seed_create", "seed_load_weights", "seed_prefill", "seed_draft",
@@ -241,7 +242,8 @@ def seed_generate(ctx: int, prompts, k: int, max_new: int, eos_id: int = -1, sim
     _check(load_library().seed_generate(ctx, B, tp, lp, ctypes.byref(opts), out.ctypes.data_as(_I32P),
                                         counts.ctypes.data_as(_I32P), ctypes.byref(stats)), "seed_generate")
     st = {"rounds": stats.rounds, "drafted": stats.drafted, "accepted": stats.accepted,
-          "prefill_ms": stats.prefill_ms, "decode_ms": stats.decode_ms}
+          "prefill_ms": stats.prefill_ms, "decode_ms": stats.decode_ms, "verify_ms": stats.verify_ms,
+          "draft_ms": stats.draft_ms}
     if log_cap > 0:
         st["n_accept_log"] = log.reshape(-1, B)[:min(stats.rounds, log_cap)]
     return out.reshape(B, max_new), counts, st
@@ -337,7 +339,8 @@ def seed_generate_tree(ctx: int, prompt, opts: SeedTreeOpts, max_new: int, eos_i
                                              out.ctypes.data_as(_I32P), ctypes.byref(count), ctypes.byref(stats)),
            "seed_generate_tree")
     st = {"rounds": stats.rounds, "drafted": stats.drafted, "accepted": stats.accepted,
-          "prefill_ms": stats.prefill_ms, "decode_ms": stats.decode_ms}
+          "prefill_ms": stats.prefill_ms, "decode_ms": stats.decode_ms, "verify_ms": stats.verify_ms,
+          "draft_ms": stats.draft_ms}
     if log_cap > 0:
         st["n_accept_log"] = log[:min(stats.rounds, log_cap)]
     return out[:count.value], st

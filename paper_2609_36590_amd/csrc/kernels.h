@@ -126,6 +126,11 @@ struct SetupArgs {
   float* xg;              // [M][H] h * gain (input of the pass's first RMSNorm consumer)
   const float* gain;      // [H]
   float* ssq;             // [M][H/16]
+  // phase clock (nullable): block 0 writes the constant-rate clock to stamp[round * 3 + stamp_col]
+  // when the kernel starts (round = *rounds, only while round < stamp_cap)
+  long long* stamp;
+  int stamp_col, stamp_cap;
+  const int* rounds;
 };
 
 // Device-resident decoding state.
@@ -146,6 +151,8 @@ struct DevState {
   int log_cap;
   const int* vtok;        // [B*R] verifier argmax per row
   int eos;
+  long long* stamp;       // nullable [stamp_cap][3]: the acceptance kernels write column 2 when done
+  int stamp_cap;
 };
 
 // Kernel choice for a linear launch: weights streamed with the activation rows staged in LDS as

@@ -15,6 +15,11 @@ template <typename T>
 __global__ void __launch_bounds__(256) k_setup(SetupArgs a) {
   const int m = blockIdx.x;
   __shared__ int s_tok, s_pos, s_seq, s_slot;
+  if (a.stamp && m == 0 && threadIdx.x == 0) {
+    const long long now = (long long)__builtin_amdgcn_s_memrealtime();
+    const int r = *a.rounds;
+    if (r >= 0 && r < a.stamp_cap) a.stamp[(size_t)r * 3 + a.stamp_col] = now;
+  }
   if (threadIdx.x == 0) {
     int b, pos, tok, slot = -1;
     if (a.mode == SETUP_PREFILL || a.mode == SETUP_SPEC) {
@@ -132,7 +137,10 @@ __global__ void __launch_bounds__(64) k_accept(DevState st, int B, int k) {
     if (s_round < st.log_cap) st.nacc_log[(size_t)s_round * B + b] = logv;
   }
   __syncthreads();
-  if (threadIdx.x == 0) *st.rounds = s_round + 1;
+  if (threadIdx.x == 0) {
+    *st.rounds = s_round + 1;
+    if (st.stamp && s_round < st.stamp_cap) st.stamp[(size_t)s_round * 3 + 2] = (long long)__builtin_amdgcn_s_memrealtime();
+  }
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -191,6 +199,7 @@ __global__ void __launch_bounds__(64) k_accept_tree(DevState st, int n, const in
   }
   if (s_round < st.log_cap) st.nacc_log[s_round] = logv;
   *st.rounds = s_round + 1;
+  if (st.stamp && s_round < st.stamp_cap) st.stamp[(size_t)s_round * 3 + 2] = (long long)__builtin_amdgcn_s_memrealtime();
   if (hstat) {   // host-visible: the sequence's length and liveness, tagged with the round count
     hstat[5] = st.t[0];
     hstat[6] = st.active[0];

@@ -57,7 +57,7 @@ struct Plan {
   size_t o_h, o_xg, o_ssq, o_q, o_attn, o_act, o_part, o_row_seq, o_row_pos, o_row_slot, o_row_blk, o_row_rope, o_amax_val,
       o_amax_idx, o_vtok;
   size_t o_t, o_len, o_limit, o_active, o_nacc, o_bonus, o_rounds, o_counters, o_drafts, o_tokens,
-      o_trace, o_log, o_bt, o_nll, o_splitk, o_splitk_rs, o_tree, o_tree_out, o_scratch, ws_total;
+      o_trace, o_log, o_bt, o_nll, o_splitk, o_splitk_rs, o_tree, o_tree_out, o_scratch, o_stamp, ws_total;
   // dynamic drafting: top-k partials, the round's drafting state, one step's drafter logits
   size_t o_topk, o_tdraft, o_dlog;
 };
@@ -156,6 +156,7 @@ Plan make_plan(const seed_config& c) {
   p.o_tokens = take(B * (size_t)p.tstride * 4);
   p.o_trace = take(B * (size_t)p.tstride * 4);
   p.o_log = take((size_t)p.log_cap * B * 4);
+  p.o_stamp = take((size_t)p.log_cap * 3 * 8);   // per round: drafting start, verification start, end
   p.o_bt = take(B * (size_t)p.bt_stride * 4);
   p.o_nll = take((size_t)c.max_ctx * 4);
   p.o_tree = take((3 * MAX_ROWS + 1) * 4);
@@ -337,6 +338,8 @@ DevState dev_state(seed_ctx* c) {
   st.log_cap = p.log_cap;
   st.vtok = c->ws<int>(p.o_vtok);
   st.eos = c->eos;
+  st.stamp = c->ws<long long>(p.o_stamp);
+  st.stamp_cap = p.log_cap;
   return st;
 }
 
@@ -514,7 +517,16 @@ SetupArgs setup_base(seed_ctx* c, int l0) {
   s.xg = c->ws<float>(p.o_xg);
   s.gain = c->wf(l0 < p.L ? p.w_attn_norm[l0] : p.w_final_norm);
   s.ssq = c->ws<float>(p.o_ssq);
+  s.rounds = c->ws<int>(p.o_rounds);
+  s.stamp_cap = p.log_cap;
   return s;
+}
+
+// The setup kernel that opens a phase of a round stamps the device clock (column 0: drafting,
+// 1: verification; the acceptance kernel writes column 2 when the round is done).
+void stamp_phase(seed_ctx* c, SetupArgs& s, int col) {
+  s.stamp = c->ws<long long>(c->p.o_stamp);
+  s.stamp_col = col;
 }
 
 // Drafting phase: k decoder-only steps for every sequence.
@@ -525,6 +537,7 @@ void enqueue_draft(seed_ctx* c, int k, float* logits, bool cap) {
   for (int i = 1; i <= k; ++i) {
     SetupArgs s = setup_base(c, p.LD);
     s.mode = SETUP_DRAFT; s.M = B; s.R = 1; s.step = i;
+    if (i == 1) stamp_phase(c, s, 0);
     timed(c, SEED_PHASE_DRAFT, SEED_OP_SETUP, cap, [&](const LaunchEvents*) { launch_setup<T>(s, c->s); });
     run_layers<T>(c, B, B, 1, p.LD, p.L, SEED_PHASE_DRAFT, nullptr, cap);
     run_head<T>(c, B, c->ws<int>(p.o_drafts) + i, p.dstride,
@@ -539,6 +552,7 @@ void enqueue_verify(seed_ctx* c, int k, int sim_accept, float* logits, bool cap)
   const int B = c->B, R = k + 1, M = B * R;
   SetupArgs s = setup_base(c, 0);
   s.mode = SETUP_VERIFY; s.M = M; s.R = R; s.sim_accept = sim_accept;
+  stamp_phase(c, s, 1);
   timed(c, SEED_PHASE_VERIFY, SEED_OP_SETUP, cap, [&](const LaunchEvents*) { launch_setup<T>(s, c->s); });
   run_layers<T>(c, M, B, R, 0, p.L, SEED_PHASE_VERIFY, nullptr, cap);
   run_head<T>(c, M, c->ws<int>(p.o_vtok), 1, logits, (long long)p.V, SEED_PHASE_VERIFY, cap);
@@ -744,6 +758,7 @@ seed_status do_prefill(seed_ctx* c, const std::vector<int>& tokens_packed) {
   HIPCHK(hipMemcpyAsync(c->ws<int>(p.o_active), active.data(), B * 4, hipMemcpyHostToDevice, c->s));
   HIPCHK(hipMemcpyAsync(c->ws<int>(p.o_drafts), drafts.data(), drafts.size() * 4, hipMemcpyHostToDevice, c->s));
   launch_fill_u32(c->ws<int>(p.o_rounds), 0, 1, c->s);
+  launch_fill_u32(c->ws<int>(p.o_stamp), 0, (long long)p.log_cap * 6, c->s);
   launch_fill_u32(c->ws<long long>(p.o_counters), 0, 4, c->s);
   HIPCHK(hipGetLastError());
   // run the full model over X[0..t-2]; X[t-1] stays pending (its cache entry would be dropped
@@ -775,6 +790,10 @@ seed_status do_spec(seed_ctx* c, int n, int block, void* skv, float* logits) {
   const Plan& p = c->p;
   const SpecPass sp{skv, p.blocks_per_seq, block};
   const int rows = n - 1;
+  // the pass's own cache starts as zeros: a 16-position tile of it that holds a visible position
+  // is contracted whole, and the positions this pass has not written yet (probability 0) must be
+  // finite, which the caller's buffer need not be
+  launch_fill_u32(skv, 0, (long long)(spec_kv_bytes(p) / 4), c->s);
   for (int s0 = 0; s0 < rows; s0 += PREFILL_ROWS) {
     const int M = std::min(PREFILL_ROWS, rows - s0);
     SetupArgs s = setup_base(c, p.LD);
@@ -784,6 +803,37 @@ seed_status do_spec(seed_ctx* c, int n, int block, void* skv, float* logits) {
     run_head<T>(c, M, c->ws<int>(p.o_vtok), 1, logits + (size_t)s0 * p.V, (long long)p.V, SEED_PHASE_SPEC, false);
   }
   HIPCHK(hipGetLastError());
+  return SEED_OK;
+}
+
+// Medians over rounds [0, rounds) of the stamped phase times (ms): verification (column 1 to 2)
+// and drafting (column 0 to 1, divided by steps; 0 when the rounds draft nothing). Rounds whose
+// stamps are missing or out of order (a phase not run) are skipped.
+seed_status phase_medians(seed_ctx* c, int64_t rounds, int steps, double* verify_ms, double* draft_ms) {
+  *verify_ms = 0.0;
+  *draft_ms = 0.0;
+  const int64_t n = std::min<int64_t>(rounds, c->p.log_cap);
+  if (n <= 0) return SEED_OK;
+  int dev = 0, khz = 0;
+  HIPCHK(hipGetDevice(&dev));
+  HIPCHK(hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev));
+  if (khz <= 0) return fail(SEED_ERR_HIP, "device reports no constant clock rate");
+  std::vector<long long> t((size_t)n * 3);
+  HIPCHK(hipMemcpy(t.data(), c->ws<long long>(c->p.o_stamp), t.size() * 8, hipMemcpyDeviceToHost));
+  std::vector<double> v, d;
+  for (int64_t r = 0; r < n; ++r) {
+    const long long a = t[r * 3], b = t[r * 3 + 1], e = t[r * 3 + 2];
+    if (e > b && b > 0) v.push_back((double)(e - b) / khz);
+    if (steps > 0 && b > a && a > 0) d.push_back((double)(b - a) / khz / steps);
+  }
+  auto median = [](std::vector<double>& x) {
+    if (x.empty()) return 0.0;
+    std::sort(x.begin(), x.end());
+    const size_t m = x.size() / 2;
+    return x.size() % 2 ? x[m] : 0.5 * (x[m - 1] + x[m]);
+  };
+  *verify_ms = median(v);
+  *draft_ms = median(d);
   return SEED_OK;
 }
 
@@ -871,6 +921,7 @@ void enqueue_verify_tree(seed_ctx* c, int n, float* logits, bool cap) {
   s.mode = SETUP_TREE; s.M = n; s.R = n; s.sim_accept = c->sim_accept;
   s.tree_tok = c->ws<int>(p.o_tree);
   s.tree_depth = c->ws<int>(p.o_tree) + 2 * MAX_ROWS;
+  stamp_phase(c, s, 1);
   timed(c, SEED_PHASE_VERIFY, SEED_OP_SETUP, cap, [&](const LaunchEvents*) { launch_setup<T>(s, c->s); });
   run_layers<T>(c, n, 1, n, 0, p.L, SEED_PHASE_VERIFY, nullptr, cap, nullptr, true);
   run_head<T>(c, n, c->ws<int>(p.o_vtok), 1, logits, (long long)p.V, SEED_PHASE_VERIFY, cap);
@@ -882,7 +933,9 @@ void enqueue_verify_tree(seed_ctx* c, int n, float* logits, bool cap) {
   });
 }
 
-seed_status check_tree_opts(const seed_ctx* c, const seed_tree_opts* o) {
+// B: the number of sequences the call runs (the current state's for seed_draft_tree and
+// seed_verify_tree, 1 for seed_generate_tree, which starts a new state)
+seed_status check_tree_opts(const seed_ctx* c, const seed_tree_opts* o, int B) {
   const Plan& p = c->p;
   if (!o) return fail(SEED_ERR_ARG, "tree options must not be NULL");
   if (o->max_depth < 1 || o->max_depth > p.cfg.max_draft)
@@ -896,7 +949,7 @@ seed_status check_tree_opts(const seed_ctx* c, const seed_tree_opts* o) {
   }
   if (o->k_rest < 1 || o->k_rest > TOPK_MAX) return fail(SEED_ERR_ARG, "k_rest must be in [1, 16]");
   if (!(o->tau >= 0.f && o->tau <= 1.f)) return fail(SEED_ERR_ARG, "tau must be in [0, 1]");
-  if (c->B != 1) return fail(SEED_ERR_UNSUPPORTED, "dynamic drafting runs one sequence (B = 1)");
+  if (B != 1) return fail(SEED_ERR_UNSUPPORTED, "dynamic drafting runs one sequence (B = 1)");
   if (p.V < TOPK_MAX || p.V > TOPK_PARTS * 64 * 16)
     return fail(SEED_ERR_UNSUPPORTED, "dynamic drafting needs 16 <= vocab <= 262144");
   return SEED_OK;
@@ -944,6 +997,7 @@ void enqueue_tree_step(seed_ctx* c, const seed_tree_opts& o, int step, float* lo
   const Plan& p = c->p;
   SetupArgs s = setup_base(c, p.LD);
   s.mode = SETUP_DRAFT; s.M = 1; s.R = 1; s.step = step;
+  if (step == 1) stamp_phase(c, s, 0);
   timed(c, SEED_PHASE_DRAFT, SEED_OP_SETUP, cap, [&](const LaunchEvents*) { launch_setup<T>(s, c->s); });
   run_layers<T>(c, 1, 1, 1, p.LD, p.L, SEED_PHASE_DRAFT, nullptr, cap);
   run_head<T>(c, 1, nullptr, p.dstride, logits, (long long)p.V, SEED_PHASE_DRAFT, cap);
@@ -1280,6 +1334,11 @@ seed_status seed_generate(seed_ctx* c, int32_t B, const int32_t* tokens, const i
   const int extra = opts->max_new + 2 * k + 1;
   st = check_prompts(c, B, tokens, lens, extra, packed);
   if (st != SEED_OK) return st;
+  if (opts->sim_accept >= 0)
+    for (int64_t i = 0; i < (int64_t)B * opts->max_new; ++i)
+      if (opts->forced_trace[i] < 0 || opts->forced_trace[i] >= p.V)
+        return fail(SEED_ERR_ARG, "forced_trace token out of range at " + std::to_string(i));
+  // every argument is checked: from here on the previous decoding state is replaced
   st = start_sequences(c, B, lens, extra);
   if (st != SEED_OK) return st;
   c->eos = opts->eos_id;
@@ -1299,11 +1358,8 @@ seed_status seed_generate(seed_ctx* c, int32_t B, const int32_t* tokens, const i
   if (opts->sim_accept >= 0) {
     std::vector<int> tr((size_t)B * p.tstride, 0);
     for (int b = 0; b < B; ++b)
-      for (int i = 0; i < opts->max_new; ++i) {
-        const int v = opts->forced_trace[(size_t)b * opts->max_new + i];
-        if (v < 0 || v >= p.V) return fail(SEED_ERR_ARG, "forced_trace token out of range");
-        tr[(size_t)b * p.tstride + lens[b] + i] = v;
-      }
+      for (int i = 0; i < opts->max_new; ++i)
+        tr[(size_t)b * p.tstride + lens[b] + i] = opts->forced_trace[(size_t)b * opts->max_new + i];
     HIPCHK(hipMemcpyAsync(c->ws<int>(p.o_trace), tr.data(), tr.size() * 4, hipMemcpyHostToDevice, c->s));
     HIPCHK(hipStreamSynchronize(c->s));
     c->sim_accept = opts->sim_accept;
@@ -1360,6 +1416,8 @@ seed_status seed_generate(seed_ctx* c, int32_t B, const int32_t* tokens, const i
       const int64_t rows = std::min<int64_t>({(int64_t)rounds, stats->n_accept_log_cap, (int64_t)p.log_cap});
       HIPCHK(hipMemcpy(stats->n_accept_log, c->ws<int>(p.o_log), rows * B * 4, hipMemcpyDeviceToHost));
     }
+    st = phase_medians(c, rounds, k, &stats->verify_ms, &stats->draft_ms);
+    if (st != SEED_OK) return st;
   }
   c->sim_accept = -1;
   c->drafts_k = -1;
@@ -1424,7 +1482,7 @@ seed_status seed_draft_tree(seed_ctx* c, const seed_tree_opts* opts, int32_t* to
   seed_status st = check_ready(c);
   if (st != SEED_OK) return st;
   if (!c->prefilled) return fail(SEED_ERR_STATE, "call seed_prefill first");
-  st = check_tree_opts(c, opts);
+  st = check_tree_opts(c, opts, c->B);
   if (st != SEED_OK) return st;
   if (!tokens || !parents || !n_nodes) return fail(SEED_ERR_ARG, "tokens, parents and n_nodes must not be NULL");
   const Plan& p = c->p;
@@ -1478,9 +1536,14 @@ seed_status seed_generate_tree(seed_ctx* c, const int32_t* tokens, int32_t len, 
   const int extra = max_new + 2 * (topts->max_nodes + 1);
   st = check_prompts(c, 1, tokens, &len, extra, packed);
   if (st != SEED_OK) return st;
-  st = start_sequences(c, 1, &len, extra);
+  st = check_tree_opts(c, topts, 1);
   if (st != SEED_OK) return st;
-  st = check_tree_opts(c, topts);
+  if (opts->sim_accept >= 0)
+    for (int i = 0; i < max_new; ++i)
+      if (opts->forced_trace[i] < 0 || opts->forced_trace[i] >= p.V)
+        return fail(SEED_ERR_ARG, "forced_trace token out of range at " + std::to_string(i));
+  // every argument is checked: from here on the previous decoding state is replaced
+  st = start_sequences(c, 1, &len, extra);
   if (st != SEED_OK) return st;
   c->eos = opts->eos_id;
   c->sim_accept = -1;
@@ -1496,11 +1559,7 @@ seed_status seed_generate_tree(seed_ctx* c, const int32_t* tokens, int32_t len, 
   std::vector<int> tr;
   if (opts->sim_accept >= 0) {
     tr.assign(p.tstride, 0);
-    for (int i = 0; i < max_new; ++i) {
-      const int v = opts->forced_trace[i];
-      if (v < 0 || v >= p.V) return fail(SEED_ERR_ARG, "forced_trace token out of range");
-      tr[len + i] = v;
-    }
+    for (int i = 0; i < max_new; ++i) tr[len + i] = opts->forced_trace[i];
     HIPCHK(hipMemcpyAsync(c->ws<int>(p.o_trace), tr.data(), tr.size() * 4, hipMemcpyHostToDevice, c->s));
     c->sim_accept = opts->sim_accept;
   }
@@ -1538,6 +1597,9 @@ seed_status seed_generate_tree(seed_ctx* c, const int32_t* tokens, int32_t len, 
       const int64_t rows = std::min<int64_t>({(int64_t)rounds, stats->n_accept_log_cap, (int64_t)p.log_cap});
       HIPCHK(hipMemcpy(stats->n_accept_log, c->ws<int>(p.o_log), rows * 4, hipMemcpyDeviceToHost));
     }
+    // a round's drafting steps vary here: draft_ms is the whole drafting phase of a round
+    st = phase_medians(c, rounds, 1, &stats->verify_ms, &stats->draft_ms);
+    if (st != SEED_OK) return st;
   }
   c->drafts_k = -1;
   return SEED_OK;

@@ -36,7 +36,7 @@ def test_struct_sizes_match_header_layout():
     assert ctypes.sizeof(binding.SeedConfig) == 15 * 4
     assert ctypes.sizeof(binding.SeedTensor) == 8 + 8 + 4 * 3 + 4 + 16
     assert ctypes.sizeof(binding.SeedGenOpts) == 16 + 8 + 8
-    assert ctypes.sizeof(binding.SeedStats) == 3 * 8 + 2 * 8 + 8 + 8
+    assert ctypes.sizeof(binding.SeedStats) == 3 * 8 + 2 * 8 + 8 + 8 + 2 * 8
 
 
 def _cfg(**kw):
@@ -105,3 +105,25 @@ def test_tree_options_layout_and_paper_defaults(lib):
     o2 = binding.tree_opts(3, tau=0.5, table=((0.9, 2),), rest=4, max_nodes=20)
     assert (o2.tau, o2.n_levels, o2.k[0], o2.k_rest, o2.max_nodes) == (pytest.approx(0.5), 1, 2, 4, 20)
     assert o2.thr[0] == pytest.approx(0.9)
+
+
+def test_struct_offsets_match_the_c_compiler(tmp_path):
+    """Every field offset of the ctypes structures equals the C compiler's for include/seed.h."""
+    import subprocess
+    structs = {"seed_config": binding.SeedConfig, "seed_gen_opts": binding.SeedGenOpts,
+               "seed_stats": binding.SeedStats, "seed_tree_opts": binding.SeedTreeOpts}
+    src = ['#include <stdio.h>', '#include <stddef.h>', '#include "seed.h"', "int main(void) {"]
+    for c_name, cls in structs.items():
+        src.append(f'  printf("{c_name} %zu\\n", sizeof({c_name}));')
+        for f, _ in cls._fields_:
+            src.append(f'  printf("{c_name}.{f} %zu\\n", offsetof({c_name}, {f}));')
+    src.append("  return 0;\n}")
+    (tmp_path / "layout.c").write_text("\n".join(src))
+    subprocess.run(["gcc", "-I", os.path.join(ROOT, "include"), str(tmp_path / "layout.c"), "-o",
+                    str(tmp_path / "layout")], check=True)
+    got = dict(line.split() for line in subprocess.run([str(tmp_path / "layout")], check=True, capture_output=True,
+                                                        text=True).stdout.splitlines())
+    for c_name, cls in structs.items():
+        assert int(got[c_name]) == ctypes.sizeof(cls), c_name
+        for f, _ in cls._fields_:
+            assert int(got[f"{c_name}.{f}"]) == getattr(cls, f).offset, (c_name, f)

@@ -7,8 +7,16 @@
 * 4B at batch 8 with ragged prompt lengths (uniform in [256, 2048]): the shortest sequence's first
   round against the oracle inside the batch, and every sequence's batched decode bit-exact to the
   same sequence decoded alone and to plain greedy decoding.
+* 28L-h2048 and 4B-36L-h2560, three consecutive rounds from one prefill (the second with drafts
+  forced to the oracle's greedy continuation, so it accepts all four and the third round's drafter
+  reads decoder-layer keys/values that a verification wrote): every round's draft and verify
+  logits against the oracle, which commits what the GPU committed (teacher forcing).
+* 4B with a 16384-token prompt, first round against the oracle's stored round
+  (tests/golden/c5_first_round.npz, written by tests/golden/make_c5_first_round.py, which calls
+  only the oracle and the seeded generators): draft logits and verify logits of the oracle's drafts
+  element by element within 2e-2, n_accept and bonus where the top-2 gaps allow.
 * 4B with a 16384-token prompt: the oracle cannot follow a 16k-token prefill through all 36
-  layers within a test. It forms the first two layers' keys/values at sampled positions one
+  layers within a test's time. It forms the first two layers' keys/values at sampled positions one
   position at a time (layer 1's need one row of layer 0 attending to the whole prefix), and
   those are compared with the GPU's cache after prefill and one verification: prefill rows and
   the verification rows at positions 16383..16387, whose layer-1 entries pass through the
@@ -18,6 +26,9 @@
 
 The oracle runs in float32 on the host; its inputs come from ``synth`` only.
 """
+import hashlib
+import os
+
 import numpy as np
 import pytest
 
@@ -110,6 +121,77 @@ def test_first_round_matches_oracle_at_full_size(cfg, request):
         if np.all(top2_gap(rd.verify_logits) > 2 * TOL):
             first = list(rd.drafts[1:rd.n_accept + 1]) + [rd.bonus]
             np.testing.assert_array_equal(out[0, :len(first)], first)
+    finally:
+        dec.close()
+
+
+def greedy_continuation(st, n):
+    """The next n tokens of plain greedy decoding from the oracle state st (each from one more
+    verification pass; the state's committed tokens are left as they are)."""
+    out = []
+    for _ in range(n):
+        plog = os_.verify(st, np.asarray([st.tokens[-1]] + out + [0] * (n - len(out)), dtype=np.int64))
+        out.append(int(np.argmax(plog[len(out)])))
+    st.cache.truncate(st.t - 1)
+    return out
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("cfg", [synth.C2_28L, synth.C3_4B], ids=["28L-h2048", "4B-36L-h2560"])
+def test_three_rounds_match_oracle_at_full_size(cfg, request):
+    w = request.getfixturevalue("weights_4b") if cfg is synth.C3_4B else synth.make_weights(cfg, seed=0)
+    prompt = synth.make_prompts(cfg)[0]
+    dec = decoder(cfg, w, max_batch=1, max_ctx=cfg.prompt_len + 3 * (K + 1) + 2 * K + 2, max_draft=K)
+    m = oracle_model(cfg, w)
+    try:
+        say(f"[gpu] oracle prefill {cfg.name} over {len(prompt)} tokens")
+        st = os_.prefill(m, prompt, len(prompt) + 3 * (K + 1) + K + 2)
+        dec.prefill([prompt])
+        accepted = []
+        for r in range(3):
+            d, qlog = dec.draft(K, logits=True)
+            drafts, qref = os_.draft(st, K)
+            if r == 1:
+                drafts = np.asarray([st.tokens[-1]] + greedy_continuation(st, K), dtype=np.int64)
+            plog = os_.verify(st, drafts)
+            n, bonus = os_.accept(drafts, plog)
+            na, bo, vlog = dec.verify(K, drafts=np.asarray(drafts[1:], dtype=np.int32)[None], logits=True)
+            say(f"[gpu] {cfg.name} round {r} at p={st.p}: drafts {drafts[1:].tolist()} n_accept {int(na[0])} "
+                f"(oracle {n}), bonus {int(bo[0])} (oracle {bonus})")
+            # draft rows compare with the oracle drafter's own drafts; the verify rows, n_accept and
+            # bonus with the verification of the drafts actually verified
+            own = np.asarray([st.tokens[-1]] + [int(x) for x in np.argmax(qref, axis=1)], dtype=np.int64)
+            compare_round(os_.Round(st.p, own, qref, plog, n, bonus), d[0], qlog[0], int(na[0]), int(bo[0]), vlog[0])
+            if r == 1 and np.all(top2_gap(plog) > 2 * TOL):
+                assert int(na[0]) == K     # the greedy continuation is accepted whole
+            os_.commit(st, drafts, int(na[0]), int(bo[0]))   # the oracle commits what the GPU committed
+            accepted.append(int(na[0]))
+        np.testing.assert_array_equal(dec.tokens(0), st.tokens)
+        say(f"[gpu] {cfg.name}: accepted per round {accepted}")
+    finally:
+        dec.close()
+
+
+GOLDEN_C5 = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "c5_first_round.npz")
+
+
+@pytest.mark.timeout(900)
+def test_long_context_first_round_matches_stored_oracle(weights_4b):
+    cfg = synth.C5_4B_LONG
+    g = np.load(GOLDEN_C5)
+    prompt = synth.make_prompts(cfg)[0]
+    assert str(g["config"]) == cfg.name
+    assert hashlib.sha256(np.asarray(prompt, dtype=np.int32).tobytes()).hexdigest() == str(g["prompt_sha256"])
+    rd = os_.Round(int(g["p"]), g["drafts"], g["draft_logits"], g["verify_logits"], int(g["n_accept"]), int(g["bonus"]))
+    assert rd.p == len(prompt) - 1
+    dec = decoder(cfg, weights_4b, max_batch=1, max_ctx=len(prompt) + N_NEW + 2 * K + 2, max_draft=K)
+    try:
+        say("[gpu] 16k prefill, first round against the stored oracle round")
+        dec.prefill([prompt])
+        d, qlog = dec.draft(K, logits=True)
+        dec.prefill([prompt])
+        na, bo, vlog = dec.verify(K, drafts=np.asarray(rd.drafts[1:], dtype=np.int32)[None], logits=True)
+        compare_round(rd, d[0], qlog[0], int(na[0]), int(bo[0]), vlog[0])
     finally:
         dec.close()
 

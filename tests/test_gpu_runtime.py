@@ -293,6 +293,49 @@ def test_error_paths_leave_state_unchanged(batch_dec):
         fresh.close()
 
 
+def test_rejected_generate_calls_leave_the_state_readable(batch_dec):
+    """seed_generate with a forced trace out of range and seed_generate_tree with bad options are
+    rejected before the previous decoding state is touched: its tokens stay readable."""
+    cfg, w, _ = batch_dec
+    dec = decoder(cfg, w, max_batch=2, max_ctx=200, max_draft=4)
+    try:
+        prompts = _prompts(cfg, [9, 14], seed=21)
+        out, _, _ = dec.generate(prompts, 2, 12)
+        before = [dec.tokens(b) for b in range(2)]
+        bad = np.zeros((2, 12), np.int32)
+        bad[1, 5] = cfg.vocab
+        with pytest.raises(binding.SeedError) as e:
+            dec.generate(prompts, 2, 12, sim_accept=1, forced_trace=bad)
+        assert e.value.status == -1
+        with pytest.raises(binding.SeedError) as e:
+            dec.generate_tree(prompts[0], binding.tree_opts(7), 8)            # max_depth > max_draft
+        assert e.value.status == -1
+        with pytest.raises(binding.SeedError) as e:
+            dec.generate_tree(prompts[0], binding.tree_opts(3, table=((0.5, 1), (0.6, 3))), 8)
+        assert e.value.status == -1
+        for b in range(2):
+            np.testing.assert_array_equal(dec.tokens(b), before[b])
+    finally:
+        dec.close()
+
+
+@pytest.mark.parametrize("graph", [False, True], ids=["eager", "graph"])
+def test_stats_report_step_latencies(batch_dec, graph):
+    """seed_stats carries the medians of the verification and drafting-step latencies stamped by
+    the kernels inside the rounds; one round's stamped phases fit inside the call's decode time."""
+    cfg, w, dec = batch_dec
+    prompts = _prompts(cfg, [40, 33], seed=5)
+    _, _, st = dec.generate(prompts, 4, 40, use_graph=graph)
+    say(f"[gpu] k=4: rounds {st['rounds']}, verify {st['verify_ms']:.4f} ms, draft step {st['draft_ms']:.4f} ms, "
+        f"decode {st['decode_ms']:.3f} ms")
+    assert st["verify_ms"] > 0 and st["draft_ms"] > 0
+    assert st["verify_ms"] + 4 * st["draft_ms"] <= st["decode_ms"] / st["rounds"] * 1.05
+    _, _, st0 = dec.generate(prompts, 0, 20, use_graph=graph)
+    assert st0["verify_ms"] > 0 and st0["draft_ms"] == 0
+    _, st_t = dec.generate_tree(prompts[0], binding.tree_opts(3), 16, use_graph=graph)
+    assert st_t["verify_ms"] > 0 and st_t["draft_ms"] > 0
+
+
 def test_missing_weights_are_reported():
     cfg = synth.C1_TINY
     w = synth.make_weights(cfg, seed=0)

@@ -71,3 +71,23 @@ def test_decoder_only_split_is_the_full_model():
             assert float(np.abs(lg - full).max()) <= 1e-4
     finally:
         dec.close()
+
+
+@pytest.mark.parametrize("cfg,tol", [(synth.C1_TINY, 1e-4), (TINY_BF16, 2e-2)], ids=["f32", "bf16"])
+def test_shallow_buffer_contents_do_not_matter(cfg, tol):
+    """The caller's buffer for the pass's own keys/values may hold anything (here every byte
+    0xFF: NaN in fp32 and bf16); the call clears it, so the logits still match the oracle."""
+    w = synth.make_weights(cfg, seed=0)
+    x = synth.make_prompts(cfg.replace(prompt_len=37), seed=17)[0]
+    m = oracle_model(cfg, w)
+    dec = decoder(cfg, w, max_batch=1, max_ctx=len(x) + 8, max_draft=4)
+    try:
+        dec.spec_forward(x, 4)          # allocates the shallow buffer
+        dec._skv.fill_(255)
+        lg, _, _ = dec.spec_forward(x, 4)
+        ref, _ = os_.spec_forward(m, x, 4)
+        err = float(np.abs(lg - ref).max())
+        say(f"[gpu] {cfg.name}: shallow buffer of 0xFF bytes, max |logits - oracle| = {err:.3g}")
+        assert np.all(np.isfinite(lg)) and err <= tol
+    finally:
+        dec.close()

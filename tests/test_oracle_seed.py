@@ -227,3 +227,15 @@ def test_spec_loss_is_the_summed_negative_log_likelihood():
     p /= p.sum(axis=1, keepdims=True)
     ref = -sum(np.log(p[q, x[q + 1]]) for q in range(len(x) - 1))
     assert abs(loss - ref) <= 1e-9 * abs(ref)
+
+
+def test_row_blocked_prefill_is_the_same_cache():
+    """Prefill in row blocks (bounded memory for long prompts) fills the same cache as one pass."""
+    cfg = synth.C1_TINY
+    mm = om.Model(cfg, synth.weights_as_f32(cfg, synth.make_weights(cfg, seed=2)), np.float64)
+    prompt = synth.make_prompts(cfg.replace(prompt_len=45), seed=4)[0]
+    a = os_.prefill(mm, prompt, 64)
+    b = os_.prefill(mm, prompt, 64, row_block=16)
+    np.testing.assert_array_equal(a.cache.valid, b.cache.valid)
+    np.testing.assert_allclose(b.cache.K, a.cache.K, rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(b.cache.V, a.cache.V, rtol=1e-12, atol=1e-14)
