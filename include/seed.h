@@ -315,6 +315,23 @@ seed_status seed_spec_kv_bytes(const seed_config* cfg, size_t* bytes);
 seed_status seed_spec_forward(seed_ctx* ctx, int32_t n, const int32_t* tokens, int32_t block,
                               void* shallow_kv, float* logits, float* row_nll, double* loss);
 
+/*
+ * seed_spec_forward for callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): the same pass, the same kernels and the
+ * same results, with the pass's own keys/values in a fixed array inside the library instead of a
+ * caller buffer. The array holds 16 MiB per GPU (one copy on each GPU the library runs on, kept
+ * until the process ends; its address is taken once per device by seed_create); a sequence needs
+ * 2 * n_kv_heads * head_dim * element-size bytes per position and decoder layer, positions
+ * rounded up to a multiple of 16 (the 4B-scale model: 8 KiB per
+ * position, n <= 2048). The call allocates nothing: no hipMalloc/hipFree, no events (kernel
+ * timing is suspended for its duration). Every call on one GPU shares the array and the pass
+ * clears what it uses first, so calls that overlap on one GPU (several contexts or streams) race:
+ * the caller serialises them. Arguments, outputs and errors as seed_spec_forward, plus
+ * SEED_ERR_CAPACITY when the sequence needs more than the array holds.
+ */
+seed_status seed_spec_forward_noalloc(seed_ctx* ctx, int32_t n, const int32_t* tokens, int32_t block,
+                                      float* logits, float* row_nll, double* loss);
+
 /* Committed tokens of sequence b (prompt included): out host [cap]; *len receives t_b. */
 seed_status seed_get_tokens(seed_ctx* ctx, int32_t b, int32_t* out, int32_t cap, int32_t* len);
 

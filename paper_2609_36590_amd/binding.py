@@ -83,8 +83,8 @@ class SeedStats(ctypes.Structure):
 EXPORTS = ("seed_arena_bytes", "seed_create", "seed_load_weights", "seed_prefill", "seed_draft",
            "seed_verify", "seed_rounds", "seed_generate", "seed_get_tokens", "seed_read_kv", "seed_kernel_timing",
            "seed_kernel_timing_read", "seed_last_error", "seed_destroy", "seed_spec_kv_bytes",
-           "seed_spec_forward", "seed_verify_tree", "seed_tree_defaults", "seed_draft_tree",
-           "seed_generate_tree")
+           "seed_spec_forward", "seed_spec_forward_noalloc", "seed_verify_tree", "seed_tree_defaults",
+           "seed_draft_tree", "seed_generate_tree")
 
 _LIB = None
 _P = ctypes.c_void_p
@@ -130,6 +130,7 @@ def load_library(path: str | None = None):
         "seed_generate_tree": [_P, _I32P, ctypes.c_int32, ctypes.POINTER(SeedTreeOpts), ctypes.POINTER(SeedGenOpts),
                                _I32P, _I32P, ctypes.POINTER(SeedStats)],
         "seed_spec_forward": [_P, ctypes.c_int32, _I32P, ctypes.c_int32, _P, _P, _P, ctypes.POINTER(ctypes.c_double)],
+        "seed_spec_forward_noalloc": [_P, ctypes.c_int32, _I32P, ctypes.c_int32, _P, _P, ctypes.POINTER(ctypes.c_double)],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -292,6 +293,17 @@ def seed_spec_forward(ctx: int, tokens, block: int, shallow_kv: int, logits: int
     loss = ctypes.c_double()
     _check(load_library().seed_spec_forward(ctx, len(t), tp, block, shallow_kv, logits, row_nll,
                                             ctypes.byref(loss) if want_loss else None), "seed_spec_forward")
+    return loss.value if want_loss else None
+
+
+def seed_spec_forward_noalloc(ctx: int, tokens, block: int, logits: int, row_nll: int | None = None,
+                              want_loss: bool = True):
+    """seed_spec_forward with the pass's own keys/values in the library's fixed scratch array."""
+    t, tp = _i32(tokens)
+    loss = ctypes.c_double()
+    _check(load_library().seed_spec_forward_noalloc(ctx, len(t), tp, block, logits, row_nll,
+                                                    ctypes.byref(loss) if want_loss else None),
+           "seed_spec_forward_noalloc")
     return loss.value if want_loss else None
 
 

@@ -14,6 +14,7 @@
 #include <cmath>
 #include <cstring>
 #include <map>
+#include <mutex>
 #include <string>
 #include <tuple>
 #include <vector>
@@ -22,9 +23,19 @@
 
 using namespace seedk;
 
+// Scratch of seed_spec_forward_noalloc (the drafting-objective pass's own keys/values): one copy
+// per GPU, held by the loaded library until the process ends. Every call on a GPU shares it.
+constexpr size_t NOALLOC_SCRATCH_BYTES = (size_t)16 << 20;
+static __device__ __align__(256) char scratch[NOALLOC_SCRATCH_BYTES];
+
 namespace {
 
 thread_local std::string g_err;
+
+// Device address of `scratch` on each GPU (the host-side name is not a device address): taken
+// once per device, with that device current, at context creation.
+std::mutex g_scratch_mu;
+std::map<int, char*> g_scratch_addr;
 
 seed_status fail(seed_status s, const std::string& msg) {
   g_err = msg;
@@ -237,6 +248,7 @@ struct seed_ctx {
   seed_tree_opts tree_key{};
   int* hstat = nullptr;       // host pointer
   int* hstat_dev = nullptr;   // its device address
+  char* scratch_dev = nullptr;   // this device's copy of `scratch` (nullptr if unavailable)
 
   template <typename X>
   X* ws(size_t off) { return reinterpret_cast<X*>(WS + off); }
@@ -779,21 +791,24 @@ seed_status do_prefill(seed_ctx* c, const std::vector<int>& tokens_packed) {
 }
 
 // Bytes of the block-causal pass's own cache: the decoder layers' keys/values by position.
-size_t spec_kv_bytes(const Plan& p) {
-  return align256((size_t)std::max(1, p.L - p.LD) * p.blocks_per_seq * 2 * p.NKV * 16 * p.HD * p.esize);
+// Bytes of the drafting-objective pass's own cache (decoder layers, `blocks` 16-position blocks
+// per layer, indexed by position).
+size_t spec_cache_bytes(const Plan& p, int blocks) {
+  return align256((size_t)std::max(1, p.L - p.LD) * blocks * 2 * p.NKV * 16 * p.HD * p.esize);
 }
+size_t spec_kv_bytes(const Plan& p) { return spec_cache_bytes(p, p.blocks_per_seq); }
 
 // Decoder rows of the speculative drafting objective (Algorithm 1) over positions 0..n-2, in
 // passes of PREFILL_ROWS rows; the deep cache holds the prefill of the same sequence.
 template <typename T>
-seed_status do_spec(seed_ctx* c, int n, int block, void* skv, float* logits) {
+seed_status do_spec(seed_ctx* c, int n, int block, void* skv, int skv_blocks, float* logits) {
   const Plan& p = c->p;
-  const SpecPass sp{skv, p.blocks_per_seq, block};
+  const SpecPass sp{skv, skv_blocks, block};
   const int rows = n - 1;
   // the pass's own cache starts as zeros: a 16-position tile of it that holds a visible position
   // is contracted whole, and the positions this pass has not written yet (probability 0) must be
   // finite, which the caller's buffer need not be
-  launch_fill_u32(skv, 0, (long long)(spec_kv_bytes(p) / 4), c->s);
+  launch_fill_u32(skv, 0, (long long)(spec_cache_bytes(p, skv_blocks) / 4), c->s);
   for (int s0 = 0; s0 < rows; s0 += PREFILL_ROWS) {
     const int M = std::min(PREFILL_ROWS, rows - s0);
     SetupArgs s = setup_base(c, p.LD);
@@ -1177,6 +1192,21 @@ seed_status seed_create(const seed_config* cfg, void* hip_stream, void* weight_a
   if (e == hipSuccess) e = hipStreamSynchronize(c->s);
   if (e == hipSuccess) e = hipHostMalloc((void**)&c->hstat, 256, hipHostMallocCoherent);
   if (e == hipSuccess) e = hipHostGetDevicePointer((void**)&c->hstat_dev, c->hstat, 0);
+  if (e == hipSuccess) {
+    // once per device, with the device current: the address of this GPU's `scratch`
+    int dev = 0;
+    e = hipGetDevice(&dev);
+    if (e == hipSuccess) {
+      std::lock_guard<std::mutex> lock(g_scratch_mu);
+      auto it = g_scratch_addr.find(dev);
+      if (it == g_scratch_addr.end()) {
+        char* ptr = nullptr;
+        e = hipGetSymbolAddress((void**)&ptr, HIP_SYMBOL(scratch));
+        if (e == hipSuccess && ptr) it = g_scratch_addr.emplace(dev, ptr).first;
+      }
+      if (e == hipSuccess && it != g_scratch_addr.end()) c->scratch_dev = it->second;
+    }
+  }
   if (e != hipSuccess) {
     if (c->hstat) hipHostFree(c->hstat);
     delete c;
@@ -1613,16 +1643,15 @@ seed_status seed_spec_kv_bytes(const seed_config* cfg, size_t* bytes) {
   return SEED_OK;
 }
 
-seed_status seed_spec_forward(seed_ctx* c, int32_t n, const int32_t* tokens, int32_t block, void* shallow_kv,
+}  // extern "C"
+
+namespace {
+
+// seed_spec_forward with the pass's own cache at skv (skv_blocks blocks per decoder layer).
+seed_status spec_forward_impl(seed_ctx* c, int32_t n, const int32_t* tokens, int32_t block, void* skv, int skv_blocks,
                               float* logits, float* row_nll, double* loss) {
-  seed_status st = check_ready(c);
-  if (st != SEED_OK) return st;
-  if (n < 2) return fail(SEED_ERR_ARG, "the sequence needs at least two tokens");
-  if (block < 1) return fail(SEED_ERR_ARG, "block must be >= 1");
-  if (!shallow_kv || !logits) return fail(SEED_ERR_ARG, "shallow_kv and logits must not be NULL");
-  if ((uintptr_t)shallow_kv & 255) return fail(SEED_ERR_ARG, "shallow_kv must be 256-byte aligned");
   std::vector<int> packed;
-  st = check_prompts(c, 1, tokens, &n, 1, packed);
+  seed_status st = check_prompts(c, 1, tokens, &n, 1, packed);
   if (st != SEED_OK) return st;
   st = start_sequences(c, 1, &n, 1);
   if (st != SEED_OK) return st;
@@ -1632,7 +1661,7 @@ seed_status seed_spec_forward(seed_ctx* c, int32_t n, const int32_t* tokens, int
   st = bf ? do_prefill<uint16_t>(c, packed) : do_prefill<float>(c, packed);
   if (st != SEED_OK) return st;
   c->prefilled = true;
-  st = bf ? do_spec<uint16_t>(c, n, block, shallow_kv, logits) : do_spec<float>(c, n, block, shallow_kv, logits);
+  st = bf ? do_spec<uint16_t>(c, n, block, skv, skv_blocks, logits) : do_spec<float>(c, n, block, skv, skv_blocks, logits);
   if (st != SEED_OK) return st;
   if (row_nll || loss) {
     float* nll = row_nll ? row_nll : c->ws<float>(c->p.o_nll);
@@ -1649,6 +1678,43 @@ seed_status seed_spec_forward(seed_ctx* c, int32_t n, const int32_t* tokens, int
   }
   HIPCHK(hipStreamSynchronize(c->s));
   return SEED_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+seed_status seed_spec_forward(seed_ctx* c, int32_t n, const int32_t* tokens, int32_t block, void* shallow_kv,
+                              float* logits, float* row_nll, double* loss) {
+  seed_status st = check_ready(c);
+  if (st != SEED_OK) return st;
+  if (n < 2) return fail(SEED_ERR_ARG, "the sequence needs at least two tokens");
+  if (block < 1) return fail(SEED_ERR_ARG, "block must be >= 1");
+  if (!shallow_kv || !logits) return fail(SEED_ERR_ARG, "shallow_kv and logits must not be NULL");
+  if ((uintptr_t)shallow_kv & 255) return fail(SEED_ERR_ARG, "shallow_kv must be 256-byte aligned");
+  return spec_forward_impl(c, n, tokens, block, shallow_kv, c->p.blocks_per_seq, logits, row_nll, loss);
+}
+
+seed_status seed_spec_forward_noalloc(seed_ctx* c, int32_t n, const int32_t* tokens, int32_t block, float* logits,
+                                      float* row_nll, double* loss) {
+  seed_status st = check_ready(c);
+  if (st != SEED_OK) return st;
+  if (n < 2) return fail(SEED_ERR_ARG, "the sequence needs at least two tokens");
+  if (block < 1) return fail(SEED_ERR_ARG, "block must be >= 1");
+  if (!logits) return fail(SEED_ERR_ARG, "logits must not be NULL");
+  if (!c->scratch_dev) return fail(SEED_ERR_HIP, "the library's scratch array has no device address on this GPU");
+  // the pass's cache sized to this sequence (positions 0..n-2) instead of max_ctx
+  const int blocks = cdiv(n, 16);
+  const size_t need = spec_cache_bytes(c->p, blocks);
+  if (need > NOALLOC_SCRATCH_BYTES)
+    return fail(SEED_ERR_CAPACITY, "the pass needs " + std::to_string(need) + " bytes of scratch; the fixed array holds " +
+                                       std::to_string(NOALLOC_SCRATCH_BYTES) + " (use seed_spec_forward with a buffer)");
+  // no timing events here (creating them allocates)
+  const int timed_id = c->timed_id;
+  c->timed_id = -1;
+  st = spec_forward_impl(c, n, tokens, block, c->scratch_dev, blocks, logits, row_nll, loss);
+  c->timed_id = timed_id;
+  return st;
 }
 
 seed_status seed_get_tokens(seed_ctx* c, int32_t b, int32_t* out, int32_t cap, int32_t* len) {
