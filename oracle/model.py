@@ -72,15 +72,19 @@ def attention(q, K, V, q_pos):
     R, nh, d = q.shape
     L, nkv, _ = K.shape
     rep = nh // nkv
-    Kh = np.repeat(K, rep, axis=1).transpose(1, 2, 0)   # [nh, d, L]
-    Vh = np.repeat(V, rep, axis=1).transpose(1, 0, 2)   # [nh, L, d]
-    s = np.matmul(q.transpose(1, 0, 2), Kh) / np.sqrt(d).astype(q.dtype)   # [nh, R, L]
-    allowed = np.arange(L)[None, :] <= np.asarray(q_pos)[:, None]          # [R, L]
-    s = np.where(allowed[None], s, -np.inf)
+    # query head j = kv * rep + g uses KV head kv: group the query heads by KV head and let the
+    # matrix products broadcast over the group (no copy of K/V per query head)
+    qg = q.reshape(R, nkv, rep, d).transpose(1, 2, 0, 3)               # [nkv, rep, R, d]
+    Kt = K.transpose(1, 2, 0)[:, None]                                   # [nkv, 1, d, L]
+    Vt = V.transpose(1, 0, 2)[:, None]                                   # [nkv, 1, L, d]
+    s = np.matmul(qg, Kt) / np.sqrt(d).astype(q.dtype)                   # [nkv, rep, R, L]
+    allowed = np.arange(L)[None, :] <= np.asarray(q_pos)[:, None]      # [R, L]
+    s = np.where(allowed, s, -np.inf)
     s = s - s.max(axis=-1, keepdims=True)
     p = np.exp(s)
     p = p / p.sum(axis=-1, keepdims=True)
-    return np.matmul(p, Vh).transpose(1, 0, 2)                               # [R, nh, d]
+    o = np.matmul(p, Vt)                                                 # [nkv, rep, R, d]
+    return o.transpose(2, 0, 1, 3).reshape(R, nh, d)                     # [R, nh, d]
 
 
 class Model:
