@@ -639,6 +639,106 @@ def cpu_baseline(cfg, weights, prompt, k, rounds):
 REPS = 5   # timed repetitions of the K rounds; value is their median
 
 
+OP_NAMES = {binding.OP_SETUP: "setup", binding.OP_QKV: "qkv", binding.OP_ATTN: "attn", binding.OP_COMBINE: "combine",
+            binding.OP_O: "o", binding.OP_GATEUP: "gateup", binding.OP_DOWN: "down", binding.OP_HEAD: "head",
+            binding.OP_ACCEPT: "accept", binding.OP_HEAD_ARGMAX: "argmax"}
+
+
+def profile_workload(torch, cfg, k, args):
+    """--profile-run (prefill, eager rounds, optional eager draft calls: the runs the rocprofv3
+    counter passes are taken over) and --kernel-breakdown (per-kernel HIP-event times of the
+    verification and draft step against algorithmic bytes) for any workload, batched ones
+    included: every sequence of the workload is decoded."""
+    lens = synth.make_prompt_lengths(cfg)
+    prompts = synth.make_prompts(cfg, lengths=lens)
+    B = len(prompts)
+    rounds = args.warmup + args.steps + 8
+    gen_probe = min(cfg.gen_len, 64)
+    max_ctx = max(lens) + max(rounds, gen_probe) * (k + 1) + 2 * k + 2
+    weights = synth.make_weights(cfg)
+    dec = binding.Decoder(cfg, max_batch=B, max_ctx=max_ctx, max_draft=max(k, 1))
+    dec.load_weights(weights)
+    ctx, stream = dec.ctx, dec.stream
+    if args.profile_run:
+        dec.prefill(prompts)
+        binding.seed_rounds(ctx, k, args.warmup, False)
+        stream.synchronize()
+        t0 = time.perf_counter()
+        binding.seed_rounds(ctx, k, args.steps, False)
+        for _ in range(args.profile_drafts):
+            dec.draft(k)
+        stream.synchronize()
+        log(f"[bench] profile run ({cfg.name}, batch {B}): {args.steps} eager rounds and {args.profile_drafts} "
+            f"draft calls in {(time.perf_counter() - t0) * 1e3:.1f} ms")
+        print(json.dumps({"profile_run": cfg.name, "batch": B, "k": k, "rounds": args.steps,
+                          "draft_calls": args.profile_drafts, "t_end": [int(len(dec.tokens(b))) for b in range(B)]}),
+              flush=True)
+        dec.close()
+        return
+    # --kernel-breakdown: HIP events around every launch of one operation over a few eager rounds
+    probe_rounds = 4
+    M_ver, M_dr = B * (k + 1), B
+    table = []
+    for phase, M in ((binding.PHASE_VERIFY, M_ver), (binding.PHASE_DRAFT, M_dr)):
+        for op in (binding.OP_SETUP, binding.OP_QKV, binding.OP_ATTN, binding.OP_COMBINE, binding.OP_O,
+                   binding.OP_GATEUP, binding.OP_DOWN, binding.OP_HEAD, binding.OP_HEAD_ARGMAX, binding.OP_ACCEPT):
+            dec.prefill(prompts)
+            binding.seed_rounds(ctx, k, 2, False)
+            binding.seed_kernel_timing(ctx, binding.kernel_id(phase, op), True)
+            binding.seed_rounds(ctx, k, probe_rounds, False)
+            n, ms = binding.seed_kernel_timing_read(ctx)
+            binding.seed_kernel_timing(ctx, 0, False)
+            if n == 0:
+                continue
+            Ls = [len(dec.tokens(b)) - probe_rounds // 2 for b in range(B)]
+            if op == binding.OP_ATTN:   # every sequence's keys/values at its own context
+                b_op = sum(kernel_bytes(cfg, op, 0, L) for L in Ls) + M * cfg.q_dim * 4
+            elif op == binding.OP_COMBINE:
+                b_op = sum(combine_bytes(cfg, M // B, L, attention_span(max_ctx)) for L in Ls)
+            else:
+                b_op = kernel_bytes(cfg, op, M, int(np.mean(Ls)))
+            name = ("verify_" if phase == binding.PHASE_VERIFY else "draft_") + OP_NAMES[op]
+            avg_us = ms / n * 1e3
+            table.append({"kernel": name, "rows": M, "launches_per_round": n / probe_rounds, "avg_us": avg_us,
+                          "us_per_round": avg_us * n / probe_rounds, "alg_bytes": b_op,
+                          "gbps": b_op / (avg_us * 1e-6) / 1e9 if b_op else None})
+    # step latencies inside graph-replayed rounds (kernel-stamped clock), for the sum check
+    _, _, st = dec.generate(prompts, k, gen_probe, use_graph=True)
+    dec.close()
+    Lm = int(np.mean(lens)) + gen_probe // 2
+    vb = step_bytes(cfg, M_ver, Lm, cfg.n_layers) + (B - 1) * cfg.n_layers * kernel_bytes(cfg, binding.OP_ATTN, 0, Lm)
+    db = step_bytes(cfg, M_dr, Lm, cfg.n_dec_layers) + (B - 1) * cfg.n_dec_layers * kernel_bytes(cfg, binding.OP_ATTN, 0, Lm)
+    out = args.kernel_breakdown
+    lines = [f"# Per-kernel breakdown: {cfg.name}, batch {B}, k = {k}", "",
+             f"Prompt lengths {lens}; verification passes of {M_ver} rows (every sequence's pending token and "
+             f"{k} drafts), draft steps of {M_dr} rows. Eager rounds, HIP events around every launch of one "
+             "operation at a time (the events add about 1-3 us per launch against the graph-replayed rounds); "
+             "algorithmic bytes per launch as in bench.py (weights once, activations in and out, every "
+             "sequence's keys/values at its own context). `frac` is against the 8 TB/s HBM peak.", "",
+             "| kernel | rows | launches / round | mean us | us / round | alg. MB / launch | GB/s | frac |",
+             "|---|---|---|---|---|---|---|---|"]
+    for r in sorted(table, key=lambda x: (not x["kernel"].startswith("verify"), -x["us_per_round"])):
+        g = f"{r['gbps']:.0f}" if r["gbps"] else "-"
+        fr = f"{r['gbps'] * 1e9 / PEAK_HBM:.3f}" if r["gbps"] else "-"
+        lines.append(f"| {r['kernel']} | {r['rows']} | {r['launches_per_round']:.2f} | {r['avg_us']:.2f} | "
+                     f"{r['us_per_round']:.1f} | {r['alg_bytes'] / 1e6:.2f} | {g} | {fr} |")
+    ver_sum = sum(r["us_per_round"] for r in table if r["kernel"].startswith("verify"))
+    dr_sum = sum(r["us_per_round"] for r in table if r["kernel"].startswith("draft")) / max(k, 1)
+    lines += ["", f"Sum of the event-timed kernels: verification {ver_sum / 1e3:.3f} ms, draft step "
+                  f"{dr_sum / 1e3:.4f} ms. Graph-replayed rounds (kernel-stamped device clock, medians over "
+                  f"{st['rounds']} rounds of a {gen_probe}-token generate): verification "
+                  f"{st['verify_ms']:.3f} ms ({vb / (st['verify_ms'] * 1e-3) / 1e9:.0f} GB/s, "
+                  f"{vb / (st['verify_ms'] * 1e-3) / PEAK_HBM:.3f} of 8 TB/s for {vb / 1e9:.3f} GB), draft step "
+                  f"{st['draft_ms']:.4f} ms ({db / (st['draft_ms'] * 1e-3) / 1e9:.0f} GB/s, "
+                  f"{db / (st['draft_ms'] * 1e-3) / PEAK_HBM:.3f} for {db / 1e9:.3f} GB).", "",
+              "Command (one MI355X, library built by `__graft_entry__.build()`):", "", "```",
+              f"python3 bench.py --config {cfg.name} --k {k} --kernel-breakdown {out}", "```", ""]
+    with open(out, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print(json.dumps({"kernel_breakdown": cfg.name, "verify_ms": st["verify_ms"], "draft_ms": st["draft_ms"],
+                      "verify_event_sum_ms": ver_sum / 1e3, "draft_event_sum_ms": dr_sum / 1e3}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -651,6 +751,9 @@ def main():
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--profile-run", action="store_true",
                     help="only prefill + eager rounds (for rocprofv3 counter passes)")
+    ap.add_argument("--kernel-breakdown", metavar="OUT_MD",
+                    help="per-kernel HIP-event times, algorithmic bytes and rates of the verification and "
+                         "draft step of --config (every sequence of a batched workload), written to OUT_MD")
     ap.add_argument("--profile-drafts", type=int, default=0,
                     help="with --profile-run: this many eager seed_draft calls (k steps each) after the rounds")
     ap.add_argument("--copy-calib", action="store_true",
@@ -692,6 +795,9 @@ def main():
 
     cfg = synth.CONFIGS[args.config]
     k = args.k
+    if args.profile_run or args.kernel_breakdown:
+        profile_workload(torch, cfg, k, args)
+        return
     t_start = time.perf_counter()
     log(f"[bench] generating weights for {cfg.name}")
     weights = synth.make_weights(cfg)
@@ -708,21 +814,6 @@ def main():
 
     def sync():
         stream.synchronize()
-
-    if args.profile_run:
-        dec.prefill([prompt])
-        binding.seed_rounds(ctx, k, args.warmup, False)
-        sync()
-        t0 = time.perf_counter()
-        binding.seed_rounds(ctx, k, args.steps, False)
-        for _ in range(args.profile_drafts):
-            dec.draft(k)
-        sync()
-        log(f"[bench] profile run: {args.steps} eager rounds and {args.profile_drafts} draft calls in "
-            f"{(time.perf_counter() - t0) * 1e3:.1f} ms")
-        print(json.dumps({"profile_run": cfg.name, "k": k, "rounds": args.steps, "draft_calls": args.profile_drafts,
-                          "t_end": int(len(dec.tokens(0)))}), flush=True)
-        return
 
     # ---------------- timed rounds (graph replay): 5 repetitions, median ----------------
     # each repetition starts from the prompt (so the context stays at the workload's length), runs

@@ -112,12 +112,12 @@ def traffic(argv):
 STEP_COMMANDS = """```
 cd /tmp && export TMPDIR=/tmp && cd <repository root>
 for c in FETCH_SIZE WRITE_SIZE; do
-  timeout -s KILL 120 rocprofv3 --pmc $c -d gpurun_out/pmc_copy_$c -o run -- python3 bench.py --copy-calib
-  timeout -s KILL 300 rocprofv3 --pmc $c -d gpurun_out/pmc_r10_$c -o run -- python3 bench.py --profile-run --steps 10 --warmup 5
-  timeout -s KILL 300 rocprofv3 --pmc $c -d gpurun_out/pmc_r30_$c -o run -- python3 bench.py --profile-run --steps 30 --warmup 5
-  timeout -s KILL 300 rocprofv3 --pmc $c -d gpurun_out/pmc_r10d20_$c -o run -- python3 bench.py --profile-run --steps 10 --warmup 5 --profile-drafts 20
+  timeout -s KILL 120 rocprofv3 --pmc $c -d {d}/pmc_copy_$c -o run -- python3 bench.py --copy-calib
+  timeout -s KILL 300 rocprofv3 --pmc $c -d {d}/pmc_r10_$c -o run -- python3 bench.py --config {cfg} --k {k} --profile-run --steps 10 --warmup 5
+  timeout -s KILL 300 rocprofv3 --pmc $c -d {d}/pmc_r30_$c -o run -- python3 bench.py --config {cfg} --k {k} --profile-run --steps 30 --warmup 5
+  timeout -s KILL 300 rocprofv3 --pmc $c -d {d}/pmc_r10d20_$c -o run -- python3 bench.py --config {cfg} --k {k} --profile-run --steps 10 --warmup 5 --profile-drafts 20
 done
-python3 paper_2609_36590_amd/profile_summary.py --step-traffic gpurun_out {out}
+python3 paper_2609_36590_amd/profile_summary.py --step-traffic {d} {out} {cfg} {k}
 ```"""
 
 
@@ -140,7 +140,8 @@ def step_traffic(argv):
     import bench
     from paper_2609_36590_amd import synth
 
-    k = 4
+    cfg = synth.CONFIGS[argv[2]] if len(argv) > 2 else synth.C3_4B
+    k = int(argv[3]) if len(argv) > 3 else 4
     run = lambda c: os.path.join(d, f"pmc_{c}", "run_results.db")
     scale = {}
     for c in ("FETCH_SIZE", "WRITE_SIZE"):
@@ -160,11 +161,15 @@ def step_traffic(argv):
     dcall = sum(v[1] for v in per.values())
     dstep = dcall / k
     ver = rnd - k * dstep
-    cfg = synth.C3_4B
-    L = cfg.prompt_len + 25
-    alg_v = bench.step_bytes(cfg, k + 1, L, cfg.n_layers)
-    alg_d = bench.step_bytes(cfg, 1, L, cfg.n_dec_layers)
-    lines = ["# HBM traffic per decode step from rocprofv3 counters: 4B-36L-h2560, batch 1, k = 4", "",
+    lens = synth.make_prompt_lengths(cfg)
+    B = len(lens)
+    # the runs' mean context: prompt + ~25 positions (5 warm-up and 10-30 rounds at a ~ 0)
+    Ls = [n + 25 for n in lens]
+    att = lambda L, layers: layers * bench.kernel_bytes(cfg, bench.binding.OP_ATTN, 0, L)
+    alg_v = bench.step_bytes(cfg, B * (k + 1), Ls[0], cfg.n_layers) + sum(att(L, cfg.n_layers) for L in Ls[1:])
+    alg_d = bench.step_bytes(cfg, B, Ls[0], cfg.n_dec_layers) + sum(att(L, cfg.n_dec_layers) for L in Ls[1:])
+    L = int(sum(Ls) / B)
+    lines = [f"# HBM traffic per decode step from rocprofv3 counters: {cfg.name}, batch {B}, k = {k}", "",
              "FETCH_SIZE and WRITE_SIZE summed over every kernel dispatch of three profile runs (prefill, 5",
              "warm-up rounds, then 10 rounds; 30 rounds; 10 rounds and 20 eager draft calls of k = 4 steps),",
              "each scaled by what the counter reads for a plain 1 GiB copy "
@@ -186,7 +191,7 @@ def step_traffic(argv):
         name = name.replace("(seedk::LinArgs)", "").replace("(seedk::AttnArgs)", "").split("(")[0]
         lines.append(f"{name[:60]:60s} {key[1]:9d} {key[2]:5d} {key[3]:6d} {r / 1e6:10.2f} {dc / 1e6:14.2f}")
     lines += ["```", "", "Commands (one MI355X, library built by `__graft_entry__.build()`):", "",
-              STEP_COMMANDS.format(out=out), ""]
+              STEP_COMMANDS.format(out=out, d=d, cfg=cfg.name, k=k), ""]
     with open(out, "w") as fh:
         fh.write("\n".join(lines) + "\n")
     print(json.dumps({"round_bytes": rnd, "verify_bytes": ver, "draft_step_bytes": dstep,
