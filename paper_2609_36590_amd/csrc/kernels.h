@@ -156,8 +156,9 @@ struct DevState {
 };
 
 // Kernel choice for a linear launch: weights streamed with the activation rows staged in LDS as
-// MFMA fragments (M <= 16 and the rows fit), else the activation fragments come from global memory.
-enum LinearKind { LIN_LDS = 0, LIN_GLOBAL = 1, LIN_SPLITK = 2 };
+// MFMA fragments (M <= 16 and the rows fit), split-K across workgroups for up to 64 rows, the
+// compute-bound tiled GEMM (LIN_WIDE) for wider passes, else activation fragments from global memory.
+enum LinearKind { LIN_LDS = 0, LIN_GLOBAL = 1, LIN_SPLITK = 2, LIN_WIDE = 3 };
 constexpr int LDS_MAX_PASSES = 8;   // n-tile passes (NJ) of one k_linear_lds workgroup
 
 // Optional timing events stamped by the launches themselves (hipExtLaunchKernel): `start` at the

@@ -628,6 +628,199 @@ __global__ void __launch_bounds__(1024) k_splitk_reduce(LinArgs a, const float* 
   linear_epilogue<T, EPI>(a, gr, Y, per, epre);
 }
 
+// ---------------------------------------------------------------------------------------------
+// Wide passes (more than 64 rows: the prompt's prefill and the drafting objective's decoder
+// pass): a compute-bound MFMA GEMM, Y[M, N] = X[M, K] W^T. A workgroup owns WIDE_WN n-tiles
+// (16 output features each) x WIDE_WM token tiles (16 rows each); its 8 waves form a 4 x 2 grid,
+// wave (wn, wm) accumulating n-tiles 2wn, 2wn+1 for token tiles 4wm..4wm+3 (8 MFMA outputs), so
+// each weight fragment feeds 4 token tiles and each activation fragment 2 n-tiles. K runs in
+// chunks of WIDE_CK k-tiles: a chunk's activation rows are staged in LDS as bf16 hi/lo B-operand
+// slots, double-buffered (chunk c+1's global loads are issued before chunk c is consumed and
+// written to the other buffer after it), and the weight fragments of chunk c+1 are loaded into
+// registers while chunk c is consumed. K is cut into the same KS k-ranges as in the narrow
+// kernels (a function of the weight shape): each range is one MFMA chain in k order from zero, and
+// the range sums are added in range order from zero, so every row's output is bit-identical to
+// what the narrow and split-K kernels compute for it.
+// Workgroup order: the token tiles of one n-group are consecutive workgroups of one XCD (workgroup
+// w runs on XCD w mod 8), so that n-group's weights come from HBM once and from that XCD's L2 for
+// its other token tiles. The finished tile goes through the same epilogues as the narrow kernels.
+// ---------------------------------------------------------------------------------------------
+constexpr int WIDE_WN = 8;    // n-tiles per workgroup
+constexpr int WIDE_WM = 8;    // token tiles per workgroup (128 rows)
+constexpr int WIDE_CK = 2;    // k-tiles per staged chunk
+constexpr int WIDE_ROWS_TILE = WIDE_WM * 16;
+constexpr size_t WIDE_CHUNK_BYTES = (size_t)WIDE_CK * 4 * WIDE_ROWS_TILE * 32;   // one staging buffer
+constexpr size_t WIDE_LDS = 2 * WIDE_CHUNK_BYTES;   // = WIDE_WN x 128 rows x 16 fp32 outputs
+
+// row-indexed arguments of rows m0.. of a pass
+__device__ __forceinline__ LinArgs wide_rows(const LinArgs& a0, int m0, int Mt) {
+  LinArgs a = a0;
+  const int n_tiles = a0.N >> 4;
+  a.M = Mt;
+  a.X = a0.X + (size_t)m0 * a0.ldx;
+  if (a0.ssq) a.ssq = a0.ssq + (size_t)m0 * a0.nssq;
+  if (a0.h) a.h = a0.h + (size_t)m0 * a0.N;
+  if (a0.xg) a.xg = a0.xg + (size_t)m0 * a0.N;
+  if (a0.ssq_out) a.ssq_out = a0.ssq_out + (size_t)m0 * n_tiles;
+  if (a0.act) a.act = a0.act + (size_t)m0 * (a0.N >> 1);
+  if (a0.q) a.q = a0.q + (size_t)m0 * a0.n_heads * a0.head_dim;
+  if (a0.row_pos) a.row_pos = a0.row_pos + m0;
+  if (a0.row_slot) a.row_slot = a0.row_slot + m0;
+  if (a0.row_blk) a.row_blk = a0.row_blk + m0;
+  if (a0.row_rope) a.row_rope = a0.row_rope + (size_t)m0 * a0.head_dim;
+  if (a0.logits) a.logits = a0.logits + (long long)m0 * a0.ld_logits;
+  if (a0.amax_val) a.amax_val = a0.amax_val + (size_t)m0 * a0.amax_stride;
+  if (a0.amax_idx) a.amax_idx = a0.amax_idx + (size_t)m0 * a0.amax_stride;
+  a.NT = WIDE_WN;
+  a.KS = 1;
+  a.S = 1;
+  a.NJ = 1;
+  return a;
+}
+
+template <typename T, int PRO, int EPI>
+__global__ void __launch_bounds__(512) k_linear_wide(LinArgs a0) {
+  extern __shared__ __attribute__((aligned(16))) char lds[];
+  __shared__ float s_rs[WIDE_ROWS_TILE];
+  constexpr int XI = (int)(WIDE_CHUNK_BYTES / 32 / 512);   // staged slots per thread and chunk
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tl = lane & 15, kg = lane >> 4;
+  const int KT = a0.K >> 5, n_tiles = a0.N >> 4;
+  const int NG = (n_tiles + WIDE_WN - 1) / WIDE_WN;
+  const int MT = (a0.M + WIDE_ROWS_TILE - 1) / WIDE_ROWS_TILE;
+  // workgroup -> (n-group, token tile): the MT token tiles of n-group g share the XCD g mod 8
+  const int b = blockIdx.x, xcd = b & 7, r = b >> 3;
+  const int mt = r % MT, g = (r / MT) * 8 + xcd;
+  if (g >= NG) return;   // padding of the grid to whole XCD rounds; the workgroup leaves together
+  const int m0 = mt * WIDE_ROWS_TILE;
+  const int Mt = min(WIDE_ROWS_TILE, a0.M - m0);
+  const LinArgs a = wide_rows(a0, m0, Mt);
+  const Grp gr{g, NG};
+  const int wn = wave & 3, wm = wave >> 2;
+
+  EpiPre epre{};
+  epi_load<EPI>(a, gr, tid, epre);
+
+  // weight fragments of n-tiles g*WN + 2wn + i (past the last n-tile: the last one, never stored)
+  const T* wp[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int nt = min(g * WIDE_WN + 2 * wn + i, n_tiles - 1);
+    wp[i] = reinterpret_cast<const T*>(a.W) + (size_t)nt * KT * 512 + lane * 8;
+  }
+  // staged slot q = (ktl*4 + kg') * 128 + row holds x[row][32 (c*CK + ktl) + 8 kg' .. +7]; rows past
+  // the tile's last row read its last row (their outputs are never stored)
+  const int NC = (KT + WIDE_CK - 1) / WIDE_CK;
+  float xv[XI][8];
+  auto stage_load = [&](int c) {
+#pragma unroll
+    for (int u = 0; u < XI; ++u) {
+      const int q = u * 512 + tid;
+      const int s = q / WIDE_ROWS_TILE, rr = min(q % WIDE_ROWS_TILE, Mt - 1);
+      const int kt = min(c * WIDE_CK + (s >> 2), KT - 1);
+      load8(a.X + (size_t)rr * a.ldx + kt * 32 + (s & 3) * 8, xv[u]);
+    }
+  };
+  auto stage_store = [&](int c) {
+    char* buf = lds + (size_t)(c & 1) * WIDE_CHUNK_BYTES;
+#pragma unroll
+    for (int u = 0; u < XI; ++u) ET<T>::to_lds(buf + (size_t)(u * 512 + tid) * 32, xv[u]);
+  };
+  typename ET<T>::A wa[2][WIDE_CK], wb[2][WIDE_CK];
+  auto wload = [&](typename ET<T>::A (&w)[2][WIDE_CK], int c) {
+#pragma unroll
+    for (int kk = 0; kk < WIDE_CK; ++kk) {
+      const int kt = min(c * WIDE_CK + kk, KT - 1);
+#pragma unroll
+      for (int i = 0; i < 2; ++i) w[i][kk] = ET<T>::load(wp[i] + (size_t)kt * 512);
+    }
+  };
+  // acc: the current k-range's chain; tot: the finished ranges, added in range order from zero
+  f32x4 acc[2][4], tot[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      tot[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  const int KS = a0.KS;
+  int ks = 0, range_end = KT / KS;   // last k-tile + 1 of k-range ks: ((ks + 1) * KT) / KS
+  auto consume = [&](const typename ET<T>::A (&w)[2][WIDE_CK], int c) {
+    const char* buf = lds + (size_t)(c & 1) * WIDE_CHUNK_BYTES;
+    const int nk = min(WIDE_CK, KT - c * WIDE_CK);
+#pragma unroll
+    for (int kk = 0; kk < WIDE_CK; ++kk) {
+      if (kk < nk) {
+        typename ET<T>::B xb[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          xb[j] = ET<T>::from_lds(buf + ((size_t)(kk * 4 + kg) * WIDE_ROWS_TILE + (wm * 4 + j) * 16 + tl) * 32);
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) ET<T>::mma(acc[i][j], w[i][kk], xb[j]);
+        if (c * WIDE_CK + kk + 1 == range_end) {
+#pragma unroll
+          for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              tot[i][j] += acc[i][j];
+              acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+            }
+          ++ks;
+          range_end = ((ks + 1) * KT) / KS;
+        }
+      }
+    }
+  };
+
+  stage_load(0);
+  wload(wa, 0);
+  stage_store(0);
+  __syncthreads();
+  for (int c = 0; c < NC; c += 2) {
+    // chunk c (weights in wa, activations in buffer 0), then chunk c+1 (wb, buffer 1)
+    if (c + 1 < NC) { stage_load(c + 1); wload(wb, c + 1); }
+    consume(wa, c);
+    if (c + 1 < NC) stage_store(c + 1);
+    __syncthreads();
+    if (c + 1 < NC) {
+      if (c + 2 < NC) { stage_load(c + 2); wload(wa, c + 2); }
+      consume(wb, c + 1);
+      if (c + 2 < NC) stage_store(c + 2);
+      __syncthreads();
+    }
+  }
+
+  // the tile's outputs Y[lt][row][16] over the staging buffers: lane (tl, kg) holds features
+  // 4kg..4kg+3 of n-tile 2wn+i for row (4wm+j)*16 + tl
+  float* Y = reinterpret_cast<float*>(lds);
+  constexpr int YS = WIDE_ROWS_TILE * 16;   // floats per local n-tile
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      *reinterpret_cast<float4*>(Y + (size_t)(2 * wn + i) * YS + ((wm * 4 + j) * 16 + tl) * 16 + 4 * kg) =
+          make_float4(tot[i][j][0], tot[i][j][1], tot[i][j][2], tot[i][j][3]);
+  if constexpr (PRO == PRO_NORM) {
+    const float ssv[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int m = wave; m < Mt; m += 8) {
+      const float rs = wave_row_scale(a, m, ssv, false);
+      if (lane == 0) s_rs[m] = rs;
+    }
+  }
+  __syncthreads();
+  if constexpr (PRO == PRO_NORM) {
+    for (int e = tid; e < WIDE_WN * Mt * 16; e += 512) {
+      const int lt = e / (Mt * 16), rem = e - lt * Mt * 16;
+      Y[(size_t)lt * YS + rem] *= s_rs[rem >> 4];
+    }
+    __syncthreads();
+  }
+  linear_epilogue<T, EPI>(a, gr, Y, YS, epre);
+}
+
 // Reduce per-n-group argmax partials of one row; lowest token id wins among equal maxima.
 __global__ void __launch_bounds__(256) k_argmax_finalize(const float* val, const int* idx, int stride, int n_parts,
                                                          int* tok_out, int tok_stride) {
@@ -687,6 +880,7 @@ size_t linear_lds_bytes(int M, int K, int NT, int KS, int S, int NJ, int kind) {
     const int nk_max = ((K >> 5) + KS - 1) / KS;
     return (size_t)nk_max * 4 * M * 32 + 64;
   }
+  if (kind == LIN_WIDE) return WIDE_LDS;
   return (size_t)(NT * KS * M * 16) * sizeof(float);
 }
 
@@ -825,6 +1019,13 @@ static void launch_linear_pe(const LinArgs& a0, int kind, hipStream_t s, const L
     else launch(k_linear_lds<T, PRO, EPI, false>, grid, block, lds, s, ev, a);
     return;
   }
+  if (kind == LIN_WIDE) {
+    const int NG = (n_tiles + WIDE_WN - 1) / WIDE_WN;
+    const int MT = (a.M + WIDE_ROWS_TILE - 1) / WIDE_ROWS_TILE;
+    const dim3 grid((unsigned)((NG + 7) / 8 * 8 * MT)), block(512);
+    launch(k_linear_wide<T, PRO, EPI>, grid, block, WIDE_LDS, s, ev, a);
+    return;
+  }
   if (kind == LIN_SPLITK) {
     const int nk_max = ((a.K >> 5) + a.KS - 1) / a.KS;
     LinArgs b = a;
@@ -913,7 +1114,8 @@ static bool allow_big_lds(int bytes) {
                        reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 1>),
                        reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 2>),
                        reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 3>),
-                       reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 4>)};
+                       reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 4>),
+                       reinterpret_cast<const void*>(&k_linear_wide<T, PRO, EPI>)};
   bool ok = true;
   for (const void* f : fns) ok &= hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes) == hipSuccess;
   return ok;

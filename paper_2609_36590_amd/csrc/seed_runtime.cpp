@@ -48,8 +48,9 @@ seed_status fail(seed_status s, const std::string& msg) {
     if (e_ != hipSuccess) return fail(SEED_ERR_HIP, std::string(#expr) + ": " + hipGetErrorString(e_)); \
   } while (0)
 
-constexpr int PREFILL_ROWS = 48;   // rows per prefill pass (3 MFMA token tiles)
+constexpr int PREFILL_ROWS = 1024; // rows per prefill / drafting-objective pass (tiled MFMA GEMMs)
 constexpr int MAX_ROWS = 64;       // rows per decode pass: max_batch * (max_draft + 1)
+constexpr int ATT_ROWS = 256;      // rows per attention launch of a wider single-sequence pass
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 int cdiv(int a, int b) { return (a + b - 1) / b; }
@@ -107,8 +108,11 @@ Plan make_plan(const seed_config& c) {
   p.L = c.n_layers; p.LD = c.n_layers - c.n_dec_layers;
   p.QD = p.NQ * p.HD; p.KVD = p.NKV * p.HD; p.G = p.NQ / p.NKV;
   p.RB = std::max(1, 32 / p.G);
+  // attention row-blocks of one launch: a decode pass (<= MAX_ROWS rows over max_batch sequences)
+  // or ATT_ROWS rows of one sequence's prefill / drafting-objective pass
   p.n_rb_max = cdiv(MAX_ROWS, p.RB);
-  p.max_rows = MAX_ROWS;   // decode passes (B (d+1) <= 64), 48-row passes, draft trees of <= 64 nodes
+  p.max_rows = std::max(MAX_ROWS, PREFILL_ROWS);   // decode passes (B (d+1) <= 64), draft trees of <= 64
+                                                  // nodes, prefill and drafting-objective passes
   p.blocks_per_seq = cdiv(c.max_ctx, 16);
   p.span = seedk::attention_span(c.max_ctx);
   p.bt_stride = cdiv(p.blocks_per_seq, p.span / 16) * (p.span / 16);   // whole groups, padded with block 0
@@ -146,7 +150,8 @@ Plan make_plan(const seed_config& c) {
   p.o_q = take(R * p.QD * 4);
   p.o_attn = take(R * p.QD * 4);
   p.o_act = take(R * p.F * 4);
-  p.o_part = take(B * p.NKV * p.n_rb_max * (size_t)p.n_groups_max * 32 * (p.HD + 4) * 4);
+  p.o_part = take(std::max(B * p.n_rb_max, (size_t)cdiv(ATT_ROWS, p.RB)) * p.NKV * (size_t)p.n_groups_max * 32 *
+                  (p.HD + 4) * 4);
   p.o_row_seq = take(R * 4);
   p.o_row_pos = take(R * 4);
   p.o_row_slot = take(R * 4);
@@ -181,8 +186,8 @@ Plan make_plan(const seed_config& c) {
       tile_policy(sh[0], sh[1], false, NT, KS, S, NJ);
       ksn = std::max(ksn, (size_t)KS * sh[0]);
     }
-    p.o_splitk = take(ksn * R * 4);
-    p.o_splitk_rs = take(R * 4);
+    p.o_splitk = take(ksn * MAX_ROWS * 4);   // only passes of at most MAX_ROWS rows split K
+    p.o_splitk_rs = take((size_t)MAX_ROWS * 4);
   }
   p.o_topk = take((size_t)TOPK_PARTS * (2 * TOPK_MAX + 2) * 4);
   p.o_tdraft = take((size_t)TREE_MAX_STEPS * (TOPK_MAX + 2) * 4 + 16);
@@ -392,6 +397,7 @@ LinArgs lin_base(seed_ctx* c, int M) {
 // stages at most 9 x 4096 activations; beyond that the split-K kernel (each workgroup stages one
 // k-range) is faster than both the LDS kernel and the global-fragment kernel.
 int linear_kind(const LinArgs& a, bool head) {
+  if (a.M > MAX_ROWS) return LIN_WIDE;   // prefill / drafting-objective passes: compute-bound tiles
   if (a.M <= 16 && (head || (long long)a.M * a.K <= 9 * 4096) &&
       linear_lds_bytes(a.M, a.K, a.NT, a.KS, a.S, a.NJ, LIN_LDS) <= linear_lds_limit())
     return LIN_LDS;
@@ -459,9 +465,21 @@ void run_layers(seed_ctx* c, int M, int B, int R, int l0, int l1, int phase,
     at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)p.HD));
     at.part = c->ws<float>(p.o_part);
     at.out = c->ws<float>(p.o_attn);
-    timed(c, phase, SEED_OP_ATTN, cap, [&](const LaunchEvents* ev) { launch_attention<T>(at, c->s, ev); });
-    if (attention_needs_combine(at))
-      timed(c, phase, SEED_OP_COMBINE, cap, [&](const LaunchEvents* ev) { launch_attn_combine(at, c->s, ev); });
+    // a pass wider than the attention partial buffer (one sequence: prefill, the drafting
+    // objective) runs its rows ATT_ROWS at a time; every row attends to its own positions either way
+    const int r_step = (B == 1 && R > MAX_ROWS) ? ATT_ROWS : R;
+    for (int r0 = 0; r0 < R; r0 += r_step) {
+      AttnArgs as = at;
+      as.R = std::min(r_step, R - r0);
+      as.n_rb = cdiv(as.R, p.RB);
+      as.q = at.q + (size_t)r0 * p.QD;
+      as.out = at.out + (size_t)r0 * p.QD;
+      as.row_pos = at.row_pos + r0;
+      as.row_slot = at.row_slot + r0;
+      timed(c, phase, SEED_OP_ATTN, cap, [&](const LaunchEvents* ev) { launch_attention<T>(as, c->s, ev); });
+      if (attention_needs_combine(as))
+        timed(c, phase, SEED_OP_COMBINE, cap, [&](const LaunchEvents* ev) { launch_attn_combine(as, c->s, ev); });
+    }
     // O + residual
     a = lin_base(c, M);
     a.W = c->W + p.w_o[li]; a.N = p.H; a.K = p.QD;
