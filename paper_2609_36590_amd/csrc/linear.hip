@@ -890,17 +890,21 @@ size_t linear_lds_bytes(int M, int K, int NT, int KS, int S, int NJ, int kind) {
 // they are staged in chunks of HEAD_CK k-tiles, double-buffered: the loads of chunk c+1 are issued
 // before chunk c is consumed and written to the other buffer after it. Each of the 8 waves
 // streams one n-tile over all of K in k order (KS = 1, as the narrow kernel does for any M), for TT
-// token tiles of 16 rows, so every row's logits are bit-identical to a pass of fewer rows.
+// token tiles of 16 rows, so every row's logits are bit-identical to a pass of fewer rows. A
+// workgroup has HEAD_WIDE_NT = 16 waves (n-tiles), so the 40 staged rows of a batch-8 verification
+// are read by 594 workgroups instead of 1187 (the argmax partials are per 16-n-tile group; the
+// maximum over them is the same).
 // ---------------------------------------------------------------------------------------------
 constexpr int HEAD_CK = 8;   // k-tiles per staged chunk (= the weight ring depth)
 static size_t g_lds_limit = 65536;   // dynamic LDS one workgroup may use (set by configure_kernels)
 
-template <typename T, int TT>
-__global__ void __launch_bounds__(512) k_linear_head_chunked(LinArgs a) {
+template <typename T, int TT, int NW>
+__global__ void __launch_bounds__(NW * 64) k_linear_head_chunked(LinArgs a) {
   extern __shared__ __attribute__((aligned(16))) char lds[];
   __shared__ float s_rs[64];
   constexpr int P = HEAD_CK;
-  constexpr int XI = (HEAD_CK * 4 * 16 * TT + 511) / 512;   // staged items per thread and chunk
+  constexpr int NTH = NW * 64;
+  constexpr int XI = (HEAD_CK * 4 * 16 * TT + NTH - 1) / NTH;   // staged items per thread and chunk
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int KT = a.K >> 5, n_tiles = a.N >> 4, M = a.M;
   const int tl = lane & 15, kg = lane >> 4;
@@ -923,7 +927,7 @@ __global__ void __launch_bounds__(512) k_linear_head_chunked(LinArgs a) {
     const int nkc = min(HEAD_CK, KT - c * HEAD_CK), items = nkc * 4 * M;
 #pragma unroll
     for (int u = 0; u < XI; ++u) {
-      const int q = u * 512 + tid, qc = q < items ? q : 0;
+      const int q = u * NTH + tid, qc = q < items ? q : 0;
       const int r = qc % M, rest = qc / M;
       load8(a.X + (size_t)r * a.ldx + (size_t)c * HEAD_CK * 32 + rest * 8, xv[u]);
     }
@@ -933,7 +937,7 @@ __global__ void __launch_bounds__(512) k_linear_head_chunked(LinArgs a) {
     char* buf = lds + (c & 1) * chunk_bytes;
 #pragma unroll
     for (int u = 0; u < XI; ++u) {
-      const int q = u * 512 + tid;
+      const int q = u * NTH + tid;
       if (q < items) ET<T>::to_lds(buf + (size_t)q * 32, xv[u]);
     }
   };
@@ -1059,12 +1063,12 @@ static void launch_linear_pe(const LinArgs& a0, int kind, hipStream_t s, const L
   const dim3 grid(n_groups), block(64 * a.NT * a.KS);
   const int TT = (a.M + 15) / 16;
   if constexpr (EPI == EPI_HEAD) {
-    if (a.M > 16 && a.KS == 1 && a.NT == 8 && a.S == 1 && head_chunked_lds(a.M) <= g_lds_limit) {
+    if (a.M > 16 && a.KS == 1 && a.NT == HEAD_WIDE_NT && a.S == 1 && head_chunked_lds(a.M) <= g_lds_limit) {
       const size_t lds_h = head_chunked_lds(a.M);
       switch (TT) {
-        case 2: launch(k_linear_head_chunked<T, 2>, grid, block, lds_h, s, ev, a); break;
-        case 3: launch(k_linear_head_chunked<T, 3>, grid, block, lds_h, s, ev, a); break;
-        default: launch(k_linear_head_chunked<T, 4>, grid, block, lds_h, s, ev, a); break;
+        case 2: launch(k_linear_head_chunked<T, 2, HEAD_WIDE_NT>, grid, block, lds_h, s, ev, a); break;
+        case 3: launch(k_linear_head_chunked<T, 3, HEAD_WIDE_NT>, grid, block, lds_h, s, ev, a); break;
+        default: launch(k_linear_head_chunked<T, 4, HEAD_WIDE_NT>, grid, block, lds_h, s, ev, a); break;
       }
       return;
     }
@@ -1108,9 +1112,9 @@ static bool allow_big_lds(int bytes) {
                        reinterpret_cast<const void*>(&k_linear_splitk<T, 3, 8, PRO>),
                        reinterpret_cast<const void*>(&k_linear_splitk<T, 4, 4, PRO>),
                        reinterpret_cast<const void*>(&k_linear_splitk<T, 4, 8, PRO>),
-                       reinterpret_cast<const void*>(&k_linear_head_chunked<T, 2>),
-                       reinterpret_cast<const void*>(&k_linear_head_chunked<T, 3>),
-                       reinterpret_cast<const void*>(&k_linear_head_chunked<T, 4>),
+                       reinterpret_cast<const void*>(&k_linear_head_chunked<T, 2, HEAD_WIDE_NT>),
+                       reinterpret_cast<const void*>(&k_linear_head_chunked<T, 3, HEAD_WIDE_NT>),
+                       reinterpret_cast<const void*>(&k_linear_head_chunked<T, 4, HEAD_WIDE_NT>),
                        reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 1>),
                        reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 2>),
                        reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 3>),

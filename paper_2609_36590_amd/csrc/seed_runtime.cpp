@@ -406,9 +406,14 @@ int linear_kind(const LinArgs& a, bool head) {
   return LIN_GLOBAL;
 }
 
+// n-tiles per workgroup of the LM head: 8, or HEAD_WIDE_NT for the 17..64-row passes (the chunked
+// kernel), where each workgroup stages every row; the argmax partials are per such group
+int head_nt(int M) { return (M > 16 && M <= MAX_ROWS) ? HEAD_WIDE_NT : 8; }
+
 template <typename T>
 void linear(seed_ctx* c, LinArgs a, int pro, int epi, int phase, int op, bool cap) {
   tile_policy(a.N, a.K, epi == EPI_HEAD, a.NT, a.KS, a.S, a.NJ);
+  if (epi == EPI_HEAD) a.NT = head_nt(a.M);
   const int kind = linear_kind(a, epi == EPI_HEAD);
   timed(c, phase, op, cap, [&](const LaunchEvents* ev) { launch_linear<T>(a, pro, epi, kind, c->s, ev); });
 }
@@ -508,9 +513,7 @@ void run_head(seed_ctx* c, int M, int* tok_out, int tok_stride, float* logits, l
   a.X = c->ws<float>(p.o_xg); a.ldx = p.H;
   a.logits = logits; a.ld_logits = ld;
   linear<T>(c, a, PRO_NORM, EPI_HEAD, phase, SEED_OP_HEAD, cap);
-  int NT, KS, S, NJ;
-  tile_policy(a.N, a.K, true, NT, KS, S, NJ);
-  const int parts = cdiv(p.V / 16, NT);   // one argmax partial per n-group
+  const int parts = cdiv(p.V / 16, head_nt(M));   // one argmax partial per n-group
   if (!tok_out) return;   // the caller ranks the logits itself (dynamic drafting)
   timed(c, phase, SEED_OP_HEAD_ARGMAX, cap, [&](const LaunchEvents*) {
     launch_argmax_finalize(a.amax_val, a.amax_idx, a.amax_stride, parts, M, tok_out, tok_stride, c->s);
