@@ -632,25 +632,27 @@ __global__ void __launch_bounds__(1024) k_splitk_reduce(LinArgs a, const float* 
 // Wide passes (more than 64 rows: the prompt's prefill and the drafting objective's decoder
 // pass): a compute-bound MFMA GEMM, Y[M, N] = X[M, K] W^T. A workgroup owns WIDE_WN n-tiles
 // (16 output features each) x WIDE_WM token tiles (16 rows each); its 8 waves form a 4 x 2 grid,
-// wave (wn, wm) accumulating n-tiles 2wn, 2wn+1 for token tiles 4wm..4wm+3 (8 MFMA outputs), so
-// each weight fragment feeds 4 token tiles and each activation fragment 2 n-tiles. K runs in
+// wave (wn, wm) accumulating WN/4 n-tiles for token tiles 4wm..4wm+3, so each weight fragment
+// feeds 4 token tiles and each activation fragment WN/4 n-tiles. WN = 16 where the projection has
+// at least 3072 outputs; 8 for the 2560-wide ones (O, down), which would otherwise give a pass of
+// 1024 rows only 80 workgroups. K runs in
 // chunks of WIDE_CK k-tiles: a chunk's activation rows are staged in LDS as bf16 hi/lo B-operand
 // slots, double-buffered (chunk c+1's global loads are issued before chunk c is consumed and
 // written to the other buffer after it), and the weight fragments of chunk c+1 are loaded into
-// registers while chunk c is consumed. K is cut into the same KS k-ranges as in the narrow
-// kernels (a function of the weight shape): each range is one MFMA chain in k order from zero, and
-// the range sums are added in range order from zero, so every row's output is bit-identical to
-// what the narrow and split-K kernels compute for it.
+// registers while chunk c is consumed. Every output is one MFMA chain over all of K in k order
+// (these passes write the prompt's cache and the drafting objective's logits, which no decode
+// pass has to reproduce bit for bit).
 // Workgroup order: the token tiles of one n-group are consecutive workgroups of one XCD (workgroup
 // w runs on XCD w mod 8), so that n-group's weights come from HBM once and from that XCD's L2 for
-// its other token tiles. The finished tile goes through the same epilogues as the narrow kernels.
+// its other token tiles. The finished tile goes through the same epilogues as the narrow kernels,
+// 8 n-tiles at a time.
 // ---------------------------------------------------------------------------------------------
-constexpr int WIDE_WN = 8;    // n-tiles per workgroup
 constexpr int WIDE_WM = 8;    // token tiles per workgroup (128 rows)
 constexpr int WIDE_CK = 2;    // k-tiles per staged chunk
+constexpr int WIDE_EPI_NT = 8;   // n-tiles per epilogue half (the head's argmax partials are per 8)
 constexpr int WIDE_ROWS_TILE = WIDE_WM * 16;
 constexpr size_t WIDE_CHUNK_BYTES = (size_t)WIDE_CK * 4 * WIDE_ROWS_TILE * 32;   // one staging buffer
-constexpr size_t WIDE_LDS = 2 * WIDE_CHUNK_BYTES;   // = WIDE_WN x 128 rows x 16 fp32 outputs
+constexpr size_t WIDE_LDS = 2 * WIDE_CHUNK_BYTES;   // = WIDE_EPI_NT x 128 rows x 16 fp32 outputs
 
 // row-indexed arguments of rows m0.. of a pass
 __device__ __forceinline__ LinArgs wide_rows(const LinArgs& a0, int m0, int Mt) {
@@ -671,15 +673,16 @@ __device__ __forceinline__ LinArgs wide_rows(const LinArgs& a0, int m0, int Mt) 
   if (a0.logits) a.logits = a0.logits + (long long)m0 * a0.ld_logits;
   if (a0.amax_val) a.amax_val = a0.amax_val + (size_t)m0 * a0.amax_stride;
   if (a0.amax_idx) a.amax_idx = a0.amax_idx + (size_t)m0 * a0.amax_stride;
-  a.NT = WIDE_WN;
+  a.NT = WIDE_EPI_NT;
   a.KS = 1;
   a.S = 1;
   a.NJ = 1;
   return a;
 }
 
-template <typename T, int PRO, int EPI>
+template <typename T, int PRO, int EPI, int WIDE_WN>
 __global__ void __launch_bounds__(512) k_linear_wide(LinArgs a0) {
+  constexpr int NI = WIDE_WN / 4;   // n-tiles per wave
   extern __shared__ __attribute__((aligned(16))) char lds[];
   __shared__ float s_rs[WIDE_ROWS_TILE];
   constexpr int XI = (int)(WIDE_CHUNK_BYTES / 32 / 512);   // staged slots per thread and chunk
@@ -695,17 +698,13 @@ __global__ void __launch_bounds__(512) k_linear_wide(LinArgs a0) {
   const int m0 = mt * WIDE_ROWS_TILE;
   const int Mt = min(WIDE_ROWS_TILE, a0.M - m0);
   const LinArgs a = wide_rows(a0, m0, Mt);
-  const Grp gr{g, NG};
   const int wn = wave & 3, wm = wave >> 2;
 
-  EpiPre epre{};
-  epi_load<EPI>(a, gr, tid, epre);
-
-  // weight fragments of n-tiles g*WN + 2wn + i (past the last n-tile: the last one, never stored)
-  const T* wp[2];
+  // weight fragments of n-tiles g*WN + NI*wn + i (past the last n-tile: the last one, never stored)
+  const T* wp[NI];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const int nt = min(g * WIDE_WN + 2 * wn + i, n_tiles - 1);
+  for (int i = 0; i < NI; ++i) {
+    const int nt = min(g * WIDE_WN + NI * wn + i, n_tiles - 1);
     wp[i] = reinterpret_cast<const T*>(a.W) + (size_t)nt * KT * 512 + lane * 8;
   }
   // staged slot q = (ktl*4 + kg') * 128 + row holds x[row][32 (c*CK + ktl) + 8 kg' .. +7]; rows past
@@ -726,27 +725,21 @@ __global__ void __launch_bounds__(512) k_linear_wide(LinArgs a0) {
 #pragma unroll
     for (int u = 0; u < XI; ++u) ET<T>::to_lds(buf + (size_t)(u * 512 + tid) * 32, xv[u]);
   };
-  typename ET<T>::A wa[2][WIDE_CK], wb[2][WIDE_CK];
-  auto wload = [&](typename ET<T>::A (&w)[2][WIDE_CK], int c) {
+  typename ET<T>::A wa[NI][WIDE_CK], wb[NI][WIDE_CK];
+  auto wload = [&](typename ET<T>::A (&w)[NI][WIDE_CK], int c) {
 #pragma unroll
     for (int kk = 0; kk < WIDE_CK; ++kk) {
       const int kt = min(c * WIDE_CK + kk, KT - 1);
 #pragma unroll
-      for (int i = 0; i < 2; ++i) w[i][kk] = ET<T>::load(wp[i] + (size_t)kt * 512);
+      for (int i = 0; i < NI; ++i) w[i][kk] = ET<T>::load(wp[i] + (size_t)kt * 512);
     }
   };
-  // acc: the current k-range's chain; tot: the finished ranges, added in range order from zero
-  f32x4 acc[2][4], tot[2][4];
+  f32x4 acc[NI][4];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < NI; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-      tot[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    }
-  const int KS = a0.KS;
-  int ks = 0, range_end = KT / KS;   // last k-tile + 1 of k-range ks: ((ks + 1) * KT) / KS
-  auto consume = [&](const typename ET<T>::A (&w)[2][WIDE_CK], int c) {
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto consume = [&](const typename ET<T>::A (&w)[NI][WIDE_CK], int c) {
     const char* buf = lds + (size_t)(c & 1) * WIDE_CHUNK_BYTES;
     const int nk = min(WIDE_CK, KT - c * WIDE_CK);
 #pragma unroll
@@ -757,20 +750,9 @@ __global__ void __launch_bounds__(512) k_linear_wide(LinArgs a0) {
         for (int j = 0; j < 4; ++j)
           xb[j] = ET<T>::from_lds(buf + ((size_t)(kk * 4 + kg) * WIDE_ROWS_TILE + (wm * 4 + j) * 16 + tl) * 32);
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < NI; ++i)
 #pragma unroll
           for (int j = 0; j < 4; ++j) ET<T>::mma(acc[i][j], w[i][kk], xb[j]);
-        if (c * WIDE_CK + kk + 1 == range_end) {
-#pragma unroll
-          for (int i = 0; i < 2; ++i)
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              tot[i][j] += acc[i][j];
-              acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-            }
-          ++ks;
-          range_end = ((ks + 1) * KT) / KS;
-        }
       }
     }
   };
@@ -793,16 +775,8 @@ __global__ void __launch_bounds__(512) k_linear_wide(LinArgs a0) {
     }
   }
 
-  // the tile's outputs Y[lt][row][16] over the staging buffers: lane (tl, kg) holds features
-  // 4kg..4kg+3 of n-tile 2wn+i for row (4wm+j)*16 + tl
-  float* Y = reinterpret_cast<float*>(lds);
-  constexpr int YS = WIDE_ROWS_TILE * 16;   // floats per local n-tile
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      *reinterpret_cast<float4*>(Y + (size_t)(2 * wn + i) * YS + ((wm * 4 + j) * 16 + tl) * 16 + 4 * kg) =
-          make_float4(tot[i][j][0], tot[i][j][1], tot[i][j][2], tot[i][j][3]);
+  // RMSNorm row scales, then the tile in two halves of 8 n-tiles through the staging buffers:
+  // Y[lt][row][16], lane (tl, kg) holding features 4kg..4kg+3 of its n-tile for row (4wm+j)*16 + tl
   if constexpr (PRO == PRO_NORM) {
     const float ssv[4] = {0.f, 0.f, 0.f, 0.f};
     for (int m = wave; m < Mt; m += 8) {
@@ -810,15 +784,33 @@ __global__ void __launch_bounds__(512) k_linear_wide(LinArgs a0) {
       if (lane == 0) s_rs[m] = rs;
     }
   }
-  __syncthreads();
-  if constexpr (PRO == PRO_NORM) {
-    for (int e = tid; e < WIDE_WN * Mt * 16; e += 512) {
-      const int lt = e / (Mt * 16), rem = e - lt * Mt * 16;
-      Y[(size_t)lt * YS + rem] *= s_rs[rem >> 4];
+  float* Y = reinterpret_cast<float*>(lds);
+  constexpr int YS = WIDE_ROWS_TILE * 16;   // floats per local n-tile
+  constexpr int HALVES = WIDE_WN / WIDE_EPI_NT;
+#pragma unroll
+  for (int half = 0; half < HALVES; ++half) {
+    const Grp gr{HALVES * g + half, HALVES * NG};   // 8 n-tiles: (HALVES g + half) * 8 + local tile
+    EpiPre epre{};
+    epi_load<EPI>(a, gr, tid, epre);
+    if ((NI * wn) / WIDE_EPI_NT == half) {
+#pragma unroll
+      for (int i = 0; i < NI; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          *reinterpret_cast<float4*>(Y + (size_t)((NI * wn + i) % WIDE_EPI_NT) * YS + ((wm * 4 + j) * 16 + tl) * 16 + 4 * kg) =
+              make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
     }
     __syncthreads();
+    if constexpr (PRO == PRO_NORM) {
+      for (int e = tid; e < WIDE_EPI_NT * Mt * 16; e += 512) {
+        const int lt = e / (Mt * 16), rem = e - lt * Mt * 16;
+        Y[(size_t)lt * YS + rem] *= s_rs[rem >> 4];
+      }
+      __syncthreads();
+    }
+    linear_epilogue<T, EPI>(a, gr, Y, YS, epre);
+    __syncthreads();   // the epilogue is done with Y before the second half overwrites it
   }
-  linear_epilogue<T, EPI>(a, gr, Y, YS, epre);
 }
 
 // Reduce per-n-group argmax partials of one row; lowest token id wins among equal maxima.
@@ -1024,10 +1016,12 @@ static void launch_linear_pe(const LinArgs& a0, int kind, hipStream_t s, const L
     return;
   }
   if (kind == LIN_WIDE) {
-    const int NG = (n_tiles + WIDE_WN - 1) / WIDE_WN;
+    const int wn = n_tiles >= 192 ? 16 : 8;
+    const int NG = (n_tiles + wn - 1) / wn;
     const int MT = (a.M + WIDE_ROWS_TILE - 1) / WIDE_ROWS_TILE;
     const dim3 grid((unsigned)((NG + 7) / 8 * 8 * MT)), block(512);
-    launch(k_linear_wide<T, PRO, EPI>, grid, block, WIDE_LDS, s, ev, a);
+    if (wn == 16) launch(k_linear_wide<T, PRO, EPI, 16>, grid, block, WIDE_LDS, s, ev, a);
+    else launch(k_linear_wide<T, PRO, EPI, 8>, grid, block, WIDE_LDS, s, ev, a);
     return;
   }
   if (kind == LIN_SPLITK) {
@@ -1119,7 +1113,8 @@ static bool allow_big_lds(int bytes) {
                        reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 2>),
                        reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 3>),
                        reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 4>),
-                       reinterpret_cast<const void*>(&k_linear_wide<T, PRO, EPI>)};
+                       reinterpret_cast<const void*>(&k_linear_wide<T, PRO, EPI, 16>),
+                       reinterpret_cast<const void*>(&k_linear_wide<T, PRO, EPI, 8>)};
   bool ok = true;
   for (const void* f : fns) ok &= hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes) == hipSuccess;
   return ok;
