@@ -384,7 +384,7 @@ def split_sweep(torch, out_md):
 # ------------------------------------------------------------------------------------------
 # forward pass of the speculative drafting objective (Algorithm 1) on the 4B model
 # ------------------------------------------------------------------------------------------
-SPEC_ROWS = 48   # rows per pass of the GPU path (its prefill chunk)
+SPEC_ROWS = 1024   # rows per pass of the GPU path (its prefill chunk, tiled MFMA GEMMs)
 
 
 def spec_sweep(torch, out_md, reps=5):
@@ -400,7 +400,7 @@ def spec_sweep(torch, out_md, reps=5):
                                                            binding.OP_DOWN))
     head = cfg.vocab * cfg.hidden * es
     passes = (n - 1 + SPEC_ROWS - 1) // SPEC_ROWS
-    # weights are streamed once per pass of 48 rows; keys/values: each row reads the deep cache
+    # weights are streamed once per pass of SPEC_ROWS rows; keys/values: each row reads the deep cache
     # below its block start and the pass's own cache of its block (decoder layers)
     kv_row = 2 * cfg.kv_dim * es
     rows = []
@@ -424,7 +424,7 @@ def spec_sweep(torch, out_md, reps=5):
         # far past the bf16 ridge (2.5 PFLOP/s / 8 TB/s = 312), so the bound is the matrix cores
         kv_bytes = sum((q // b * b + (q - q // b * b + 1)) for q in range(n - 1)) * kv_row * cfg.n_dec_layers
         wbytes_once = cfg.n_dec_layers * dec_layer + head
-        streamed = passes * wbytes_once + kv_bytes   # what the 48-row passes actually read
+        streamed = passes * wbytes_once + kv_bytes   # what the passes read at least once
         attn = sum(4 * (q + 1) * cfg.n_heads * cfg.head_dim for q in range(n - 1)) * cfg.n_dec_layers
         flops = 2 * (n - 1) * (cfg.n_dec_layers * dec_layer / es + head / es) + attn
         pf_flops = 2 * n * cfg.n_layers * dec_layer / es + sum(
@@ -451,9 +451,10 @@ def spec_sweep(torch, out_md, reps=5):
              "visible positions x heads x head_dim per row and layer); at 1023 rows it is ~1000 FLOP per",
              "weight byte, past the bf16 ridge (2.5 PFLOP/s / 8 TB/s = 312 FLOP/B), so its roofline is",
              "the dense bf16 MFMA peak (2.5 PFLOP/s). The prefill (36 layers over 1024 rows, same rule)",
-             f"likewise. The GPU path takes {SPEC_ROWS} rows per pass and streams the decoder layers and",
-             "the head once per pass (`streamed` bytes below): an implementation cost, not the method's",
-             "bytes (the weights once: 1.18 GB, plus the keys/values each row reads).", "",
+             f"likewise. The GPU path takes {SPEC_ROWS} rows per pass (tiled MFMA GEMMs; each n-group's",
+             "weights come from HBM once per pass and are shared by its row tiles through the XCD's L2),",
+             "so the decoder layers and the head are streamed once per pass (`streamed` bytes below: the",
+             "weights once, 1.18 GB per pass, plus the keys/values each row reads).", "",
              "| block | rows | pass ms | rows/s | TFLOP/s (frac of 2.5 PFLOP/s bf16) | streamed GB (GB/s) | "
              "prefill ms | prefill TFLOP/s (frac) | L_spec |",
              "|---|---|---|---|---|---|---|---|---|"]
@@ -638,10 +639,6 @@ def cpu_baseline(cfg, weights, prompt, k, rounds):
 # ------------------------------------------------------------------------------------------
 REPS = 5   # timed repetitions of the K rounds; value is their median
 
-
-OP_NAMES = {binding.OP_SETUP: "setup", binding.OP_QKV: "qkv", binding.OP_ATTN: "attn", binding.OP_COMBINE: "combine",
-            binding.OP_O: "o", binding.OP_GATEUP: "gateup", binding.OP_DOWN: "down", binding.OP_HEAD: "head",
-            binding.OP_ACCEPT: "accept", binding.OP_HEAD_ARGMAX: "argmax"}
 
 
 def profile_workload(torch, cfg, k, args):

@@ -99,8 +99,15 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
   constexpr int SPAN = ATT_WAVES * TPW * 16;
   // run partials for the in-group merge; rows padded by 4 floats so that the 16 query lanes
   // reading one column fall in different banks
-  __shared__ float s_o[ATT_WAVES][32][HD + 4];
-  __shared__ float s_ml[ATT_WAVES][32][2];
+  // run partials for the in-group merge, [wave][query vector][HD + 4] (+ m, l), sized by the
+  // launcher for the launch's query vectors per row-block; rows padded by 4 floats so that the 16
+  // query lanes reading one column fall in different banks
+  extern __shared__ __attribute__((aligned(16))) float att_lds[];
+  const int NQ = a.nq_alloc;
+  float* s_o = att_lds;                               // [ATT_WAVES][NQ][HD + 4]
+  float* s_ml = att_lds + ATT_WAVES * NQ * (HD + 4);  // [ATT_WAVES][NQ][2]
+#define S_O(w_, q_, d_) s_o[((w_) * NQ + (q_)) * (HD + 4) + (d_)]
+#define S_ML(w_, q_, i_) s_ml[((w_) * NQ + (q_)) * 2 + (i_)]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, tl = lane & 15, kg = lane >> 4;
   const int g = blockIdx.x;
   const int h = blockIdx.y % a.n_kv, rb = blockIdx.y / a.n_kv;
@@ -197,8 +204,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
   // space of the run partials, which are written only after the last tile) so that the K/V
   // fragments of every tile fit the registers of two waves per SIMD ----
   typedef typename ET<T>::B QB;
-  QB* s_q = reinterpret_cast<QB*>(&s_o[0][0][0]);
-  static_assert(QSLOTS * sizeof(QB) <= sizeof(s_o), "query fragments exceed the partial buffer");
+  QB* s_q = reinterpret_cast<QB*>(att_lds);   // the launcher sizes the buffer for these too
 #pragma unroll
   for (int u = 0; u < QPT; ++u) {
     const int sl = u * 256 + (int)threadIdx.x;
@@ -330,11 +336,11 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
     if (qv >= nqv) continue;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
-      *reinterpret_cast<float4*>(&s_o[wave][qv][dt * 16 + 4 * kg]) =
+      *reinterpret_cast<float4*>(&S_O(wave, qv, dt * 16 + 4 * kg)) =
           make_float4(o_c[qt][dt][0], o_c[qt][dt][1], o_c[qt][dt][2], o_c[qt][dt][3]);
     if (kg == 0) {
-      s_ml[wave][qv][0] = m_c[qt];
-      s_ml[wave][qv][1] = l_c[qt];
+      S_ML(wave, qv, 0) = m_c[qt];
+      S_ML(wave, qv, 1) = l_c[qt];
     }
   }
   __syncthreads();
@@ -342,13 +348,13 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
   constexpr int HD4 = HD / 4;
   for (int e = threadIdx.x; e < nqv * HD4; e += blockDim.x) {
     const int qv = e / HD4, d = (e - qv * HD4) * 4;
-    const float4 v0 = *reinterpret_cast<const float4*>(&s_o[0][qv][d]);
-    float m_r = s_ml[0][qv][0], l_r = s_ml[0][qv][1], o_r[4] = {v0.x, v0.y, v0.z, v0.w};
+    const float4 v0 = *reinterpret_cast<const float4*>(&S_O(0, qv, d));
+    float m_r = S_ML(0, qv, 0), l_r = S_ML(0, qv, 1), o_r[4] = {v0.x, v0.y, v0.z, v0.w};
 #pragma unroll
     for (int w = 1; w < ATT_WAVES; ++w) {
-      const float4 v = *reinterpret_cast<const float4*>(&s_o[w][qv][d]);
+      const float4 v = *reinterpret_cast<const float4*>(&S_O(w, qv, d));
       const float oc[4] = {v.x, v.y, v.z, v.w};
-      softmax_merge(m_r, l_r, o_r, s_ml[w][qv][0], s_ml[w][qv][1], oc, 4);
+      softmax_merge(m_r, l_r, o_r, S_ML(w, qv, 0), S_ML(w, qv, 1), oc, 4);
     }
     if (n_groups == 1) {
       // the only group: the merge of groups reduces to o / l for it (weight 1), so finish here
@@ -362,6 +368,9 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
     }
   }
 }
+
+#undef S_O
+#undef S_ML
 
 // Merge of the group partials: an 8-lane team per (query vector, 4 columns). Lane j merges groups
 // j, j+8, .. left to right from the identity (4 groups' loads in flight at a time), then the team
@@ -429,18 +438,31 @@ __global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
 }
 
 template <typename Kern>
-static void launch_kernel(Kern k, dim3 grid, hipStream_t s, const LaunchEvents* ev, const AttnArgs& a) {
-  if (ev) hipExtLaunchKernelGGL(k, grid, dim3(256), 0, s, ev->start, ev->stop, 0, a);
-  else hipLaunchKernelGGL(k, grid, dim3(256), 0, s, a);
+static void launch_kernel(Kern k, dim3 grid, hipStream_t s, const LaunchEvents* ev, const AttnArgs& a,
+                          size_t lds = 0) {
+  if (ev) hipExtLaunchKernelGGL(k, grid, dim3(256), (uint32_t)lds, s, ev->start, ev->stop, 0, a);
+  else hipLaunchKernelGGL(k, grid, dim3(256), lds, s, a);
+}
+
+// LDS of one attention workgroup: the 4 waves' run partials for the launch's query vectors per
+// row-block (at most 32), and at least the queries' B-operand fragments parked there first
+template <typename T, int HD, int QT>
+static size_t attention_lds(int nq) {
+  const size_t parts = (size_t)ATT_WAVES * nq * (HD + 4) * 4 + (size_t)ATT_WAVES * nq * 2 * 4;
+  const size_t qfrag = (size_t)QT * (HD / 32) * 64 * sizeof(typename ET<T>::B);
+  return std::max(parts, qfrag);
 }
 
 template <typename T, int HD, int QT, int MODE>
-static void launch_attention_qt(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev) {
+static void launch_attention_qt(const AttnArgs& a0, hipStream_t s, const LaunchEvents* ev) {
+  AttnArgs a = a0;
+  a.nq_alloc = std::min(a.RB, a.R) * a.G;   // query vectors of the widest row-block
+  const size_t lds = attention_lds<T, HD, QT>(a.nq_alloc);
   const dim3 grid(a.n_groups_max, a.n_kv * a.n_rb, a.B);
   switch (a.span) {
-    case 64: launch_kernel(k_attention<T, HD, QT, 1, MODE>, grid, s, ev, a); break;
-    case 128: launch_kernel(k_attention<T, HD, QT, 2, MODE>, grid, s, ev, a); break;
-    default: launch_kernel(k_attention<T, HD, QT, 4, MODE>, grid, s, ev, a); break;
+    case 64: launch_kernel(k_attention<T, HD, QT, 1, MODE>, grid, s, ev, a, lds); break;
+    case 128: launch_kernel(k_attention<T, HD, QT, 2, MODE>, grid, s, ev, a, lds); break;
+    default: launch_kernel(k_attention<T, HD, QT, 4, MODE>, grid, s, ev, a, lds); break;
   }
 }
 

@@ -85,6 +85,7 @@ struct AttnArgs {
   int s_layer, s_n_blocks, s_block;
   int tree;               // 1: packed draft tree rows (mask by row_pos and row_slot)
   int span;               // positions per workgroup group: 64, 128 or 256 (attention_span)
+  int nq_alloc;           // set by the launcher: query vectors per row-block the LDS is sized for
   int n_groups_max;       // grid extent over groups; n_groups_max * span == bt_stride * 16
   float scale_log2;       // log2(e) / sqrt(head_dim)
   float* part;            // group partials [B][n_kv][n_rb][n_groups_max][32][head_dim + 4]
