@@ -17,6 +17,7 @@
 namespace seedk {
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
 typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
 
@@ -80,6 +81,19 @@ struct ET<uint16_t> {
   __device__ static B from_lds(const char* p) {
     return B{*reinterpret_cast<const bf16x8*>(p), *reinterpret_cast<const bf16x8*>(p + 16)};
   }
+  // half `hf` (values 4hf..4hf+3) of a slot: the same bytes to_lds writes for them
+  __device__ static void to_lds_half(char* p, int hf, const float4 x) {
+    const float v[4] = {x.x, x.y, x.z, x.w};
+    bf16x4 h, l;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      __bf16 t = (__bf16)v[j];
+      h[j] = t;
+      l[j] = (__bf16)(v[j] - (float)t);
+    }
+    *reinterpret_cast<bf16x4*>(p + hf * 8) = h;
+    *reinterpret_cast<bf16x4*>(p + 16 + hf * 8) = l;
+  }
 };
 
 template <>
@@ -119,6 +133,7 @@ struct ET<float> {
     const float4 u = reinterpret_cast<const float4*>(p)[0], v = reinterpret_cast<const float4*>(p)[1];
     return B{{u.x, u.y, u.z, u.w, v.x, v.y, v.z, v.w}};
   }
+  __device__ static void to_lds_half(char* p, int hf, const float4 x) { reinterpret_cast<float4*>(p)[hf] = x; }
 };
 
 __device__ __forceinline__ void load8(const float* p, float x[8]) {

@@ -685,7 +685,6 @@ __global__ void __launch_bounds__(512) k_linear_wide(LinArgs a0) {
   constexpr int NI = WIDE_WN / 4;   // n-tiles per wave
   extern __shared__ __attribute__((aligned(16))) char lds[];
   __shared__ float s_rs[WIDE_ROWS_TILE];
-  constexpr int XI = (int)(WIDE_CHUNK_BYTES / 32 / 512);   // staged slots per thread and chunk
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int tl = lane & 15, kg = lane >> 4;
   const int KT = a0.K >> 5, n_tiles = a0.N >> 4;
@@ -708,22 +707,31 @@ __global__ void __launch_bounds__(512) k_linear_wide(LinArgs a0) {
     wp[i] = reinterpret_cast<const T*>(a.W) + (size_t)nt * KT * 512 + lane * 8;
   }
   // staged slot q = (ktl*4 + kg') * 128 + row holds x[row][32 (c*CK + ktl) + 8 kg' .. +7]; rows past
-  // the tile's last row read its last row (their outputs are never stored)
+  // the tile's last row read its last row (their outputs are never stored). A chunk is read as
+  // (8 rows x one k-tile) blocks, one per wave and load: lane (r, e) takes floats 4e..4e+3 of the
+  // k-tile in row r, so a load touches 8 cache lines (not 64 rows' pieces), and its LDS stores
+  // (half e&1 of slot kg' = e/2) fall on 16 distinct 8-byte bank positions.
   const int NC = (KT + WIDE_CK - 1) / WIDE_CK;
-  float xv[XI][8];
+  constexpr int XP = 2 * WIDE_CK;   // 16-byte pieces per thread and chunk (16 x CK blocks / 8 waves)
+  static_assert(XP * 512 * 16 == WIDE_ROWS_TILE * WIDE_CK * 32 * 4, "chunk pieces");
+  float4 xv[XP];
   auto stage_load = [&](int c) {
 #pragma unroll
-    for (int u = 0; u < XI; ++u) {
-      const int q = u * 512 + tid;
-      const int s = q / WIDE_ROWS_TILE, rr = min(q % WIDE_ROWS_TILE, Mt - 1);
-      const int kt = min(c * WIDE_CK + (s >> 2), KT - 1);
-      load8(a.X + (size_t)rr * a.ldx + kt * 32 + (s & 3) * 8, xv[u]);
+    for (int u = 0; u < XP; ++u) {
+      const int blk = u * 8 + wave, ktl = blk % WIDE_CK;
+      const int rr = min((blk / WIDE_CK) * 8 + (lane >> 3), Mt - 1);
+      const int kt = min(c * WIDE_CK + ktl, KT - 1);
+      xv[u] = *reinterpret_cast<const float4*>(a.X + (size_t)rr * a.ldx + kt * 32 + (lane & 7) * 4);
     }
   };
   auto stage_store = [&](int c) {
     char* buf = lds + (size_t)(c & 1) * WIDE_CHUNK_BYTES;
 #pragma unroll
-    for (int u = 0; u < XI; ++u) ET<T>::to_lds(buf + (size_t)(u * 512 + tid) * 32, xv[u]);
+    for (int u = 0; u < XP; ++u) {
+      const int blk = u * 8 + wave, ktl = blk % WIDE_CK, row = (blk / WIDE_CK) * 8 + (lane >> 3);
+      const int q = (ktl * 4 + ((lane & 7) >> 1)) * WIDE_ROWS_TILE + row;
+      ET<T>::to_lds_half(buf + (size_t)q * 32, lane & 1, xv[u]);
+    }
   };
   typename ET<T>::A wa[NI][WIDE_CK], wb[NI][WIDE_CK];
   auto wload = [&](typename ET<T>::A (&w)[NI][WIDE_CK], int c) {
@@ -761,18 +769,22 @@ __global__ void __launch_bounds__(512) k_linear_wide(LinArgs a0) {
   wload(wa, 0);
   stage_store(0);
   __syncthreads();
+  // chunk c (weights in wa, activations in buffer 0), then chunk c+1 (wb, buffer 1). The next
+  // chunk's loads are issued unconditionally (indices clamped to the last k-tile; a chunk past the
+  // end is staged but never consumed): under a data-dependent branch the compiler's wait counts
+  // merge the path without the loads, and every chunk then waits for all loads in flight,
+  // including the prefetch just issued.
   for (int c = 0; c < NC; c += 2) {
-    // chunk c (weights in wa, activations in buffer 0), then chunk c+1 (wb, buffer 1)
-    if (c + 1 < NC) { stage_load(c + 1); wload(wb, c + 1); }
+    stage_load(c + 1);
+    wload(wb, c + 1);
     consume(wa, c);
-    if (c + 1 < NC) stage_store(c + 1);
+    stage_store(c + 1);
     __syncthreads();
-    if (c + 1 < NC) {
-      if (c + 2 < NC) { stage_load(c + 2); wload(wa, c + 2); }
-      consume(wb, c + 1);
-      if (c + 2 < NC) stage_store(c + 2);
-      __syncthreads();
-    }
+    stage_load(c + 2);
+    wload(wa, c + 2);
+    consume(wb, c + 1);
+    stage_store(c + 2);
+    __syncthreads();
   }
 
   // RMSNorm row scales, then the tile in two halves of 8 n-tiles through the staging buffers:
