@@ -957,8 +957,12 @@ __global__ void __launch_bounds__(NW * 64) k_linear_head_chunked(LinArgs a) {
   f32x4 acc[TT];
 #pragma unroll
   for (int tt = 0; tt < TT; ++tt) acc[tt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // every load below is issued unconditionally (the last chunk is reloaded past the end, weight
+  // tiles past K re-read the last one, neither is consumed): a load under a data-dependent branch
+  // makes the compiler's wait counts assume the path without it, and every refill would then wait
+  // for the whole ring
   for (int c = 0; c < NC; ++c) {
-    if (c + 1 < NC) stage_load(c + 1);
+    stage_load(min(c + 1, NC - 1));
     const char* buf = lds + (c & 1) * chunk_bytes;
     const int nkc = min(HEAD_CK, KT - c * HEAD_CK);
 #pragma unroll
@@ -970,9 +974,9 @@ __global__ void __launch_bounds__(NW * 64) k_linear_head_chunked(LinArgs a) {
           const char* xb = m < M ? buf + ((size_t)(p * 4 + kg) * M + m) * 32 : lds + zero_off;
           ET<T>::mma(acc[tt], wb[p], ET<T>::from_lds(xb));
         }
-        const int nxt = c * HEAD_CK + p + P;
-        wb[p] = ET<T>::load_nt(w0 + (size_t)min(nxt, KT - 1) * 512);   // past the end: never consumed
       }
+      const int nxt = c * HEAD_CK + p + P;
+      wb[p] = ET<T>::load_nt(w0 + (size_t)min(nxt, KT - 1) * 512);
       __builtin_amdgcn_sched_barrier(0);
     }
     if (c + 1 < NC) stage_store(c + 1);
