@@ -264,24 +264,57 @@ __global__ void __launch_bounds__(1024) k_linear_lds(LinArgs a) {
   float* part = reinterpret_cast<float*>(alias ? lds : lds + lds_x_bytes(M, KT));
   float* s_rs = part + (size_t)a.NJ * NW * M * 16;
   {
-    const int row_items = KT * 4, items = M * row_items;
-    for (int q0 = 0; q0 < items; q0 += 2 * (int)blockDim.x) {
-      float xv[2][8];
+    // two batches of 2 items per thread per round trip: both batches' loads are issued before
+    // either is written, so a workgroup whose rows take several batches (O at 5 rows, the LM head
+    // at more than 3) pays half the round trips. Loads are branch-free (items past the end reload
+    // the last one and are not written) and none is issued after a wait: a load under a branch
+    // makes the compiler wait for every load in flight before each write, and a surplus load
+    // issued after the first wait would add a round trip to the one-batch case.
+    const int row_items = KT * 4, items = M * row_items, bs = 2 * (int)blockDim.x;
+    float xa[2][8], xb[2][8];
+    auto ld = [&](float (&xv)[2][8], int q0) {
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
-        const int q = q0 + u * blockDim.x + tid;
-        if (q < items) {
-          const int r = q / row_items, rem = q - r * row_items;
-          load8(a.X + (size_t)r * a.ldx + (size_t)rem * 8, xv[u]);
-        }
+        const int q = min(q0 + u * (int)blockDim.x + tid, items - 1);
+        const int r = q / row_items, rem = q - r * row_items;
+        load8(a.X + (size_t)r * a.ldx + (size_t)rem * 8, xv[u]);
       }
+    };
+    auto st = [&](const float (&xv)[2][8], int q0) {
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
-        const int q = q0 + u * blockDim.x + tid;
+        const int q = q0 + u * (int)blockDim.x + tid;
         if (q < items) {
           const int r = q / row_items, rem = q - r * row_items;
           ET<T>::to_lds(lds + ((size_t)rem * M + r) * 32, xv[u]);
         }
+      }
+    };
+    if constexpr (!ALIAS) {
+      if (items <= bs) {   // one batch (both paths finish their loads before they merge)
+        ld(xa, 0);
+        st(xa, 0);
+      } else {
+        for (int q0 = 0; q0 < items; q0 += 2 * bs) {
+          ld(xa, q0);
+          ld(xb, q0 + bs);
+          st(xa, q0);
+          st(xb, q0 + bs);
+        }
+      }
+    } else {
+      // one batch per round trip, loads under the item bound: with this variant's pass registers
+      // the forms above make the compiler wait for every weight tile of the ring below
+      for (int q0 = 0; q0 < items; q0 += bs) {
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const int q = q0 + u * (int)blockDim.x + tid;
+          if (q < items) {
+            const int r = q / row_items, rem = q - r * row_items;
+            load8(a.X + (size_t)r * a.ldx + (size_t)rem * 8, xa[u]);
+          }
+        }
+        st(xa, q0);
       }
     }
     if (tid < 2) *reinterpret_cast<float4*>(lds + zero_off + tid * 16) = make_float4(0.f, 0.f, 0.f, 0.f);
