@@ -687,6 +687,38 @@ constexpr int WIDE_ROWS_TILE = WIDE_WM * 16;
 constexpr size_t WIDE_CHUNK_BYTES = (size_t)WIDE_CK * 4 * WIDE_ROWS_TILE * 32;   // one staging buffer
 constexpr size_t WIDE_LDS = 2 * WIDE_CHUNK_BYTES;   // = WIDE_EPI_NT x 128 rows x 16 fp32 outputs
 
+// A staging buffer's B-operand slots. bf16: two planes, the 16-byte hi halves of all slots, then
+// the lo halves, so that the 16 lanes of a fragment read (consecutive slots) cover 256 contiguous
+// bytes (interleaved 32-byte slots would put lanes tl and tl + 8 on the same banks); fp32: 32-byte
+// slots of 8 values.
+template <typename T>
+__device__ __forceinline__ void wide_store_half(char* buf, int q, int hf, const float4 x) {
+  if constexpr (sizeof(T) == 2) {
+    const float v[4] = {x.x, x.y, x.z, x.w};
+    bf16x4 h, l;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      __bf16 t = (__bf16)v[j];
+      h[j] = t;
+      l[j] = (__bf16)(v[j] - (float)t);
+    }
+    *reinterpret_cast<bf16x4*>(buf + (size_t)q * 16 + hf * 8) = h;
+    *reinterpret_cast<bf16x4*>(buf + WIDE_CHUNK_BYTES / 2 + (size_t)q * 16 + hf * 8) = l;
+  } else {
+    ET<T>::to_lds_half(buf + (size_t)q * 32, hf, x);
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ typename ET<T>::B wide_load_slot(const char* buf, int q) {
+  if constexpr (sizeof(T) == 2) {
+    return typename ET<T>::B{*reinterpret_cast<const bf16x8*>(buf + (size_t)q * 16),
+                             *reinterpret_cast<const bf16x8*>(buf + WIDE_CHUNK_BYTES / 2 + (size_t)q * 16)};
+  } else {
+    return ET<T>::from_lds(buf + (size_t)q * 32);
+  }
+}
+
 // row-indexed arguments of rows m0.. of a pass
 __device__ __forceinline__ LinArgs wide_rows(const LinArgs& a0, int m0, int Mt) {
   LinArgs a = a0;
@@ -763,7 +795,7 @@ __global__ void __launch_bounds__(512) k_linear_wide(LinArgs a0) {
     for (int u = 0; u < XP; ++u) {
       const int blk = u * 8 + wave, ktl = blk % WIDE_CK, row = (blk / WIDE_CK) * 8 + (lane >> 3);
       const int q = (ktl * 4 + ((lane & 7) >> 1)) * WIDE_ROWS_TILE + row;
-      ET<T>::to_lds_half(buf + (size_t)q * 32, lane & 1, xv[u]);
+      wide_store_half<T>(buf, q, lane & 1, xv[u]);
     }
   };
   typename ET<T>::A wa[NI][WIDE_CK], wb[NI][WIDE_CK];
@@ -789,7 +821,7 @@ __global__ void __launch_bounds__(512) k_linear_wide(LinArgs a0) {
         typename ET<T>::B xb[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          xb[j] = ET<T>::from_lds(buf + ((size_t)(kk * 4 + kg) * WIDE_ROWS_TILE + (wm * 4 + j) * 16 + tl) * 32);
+          xb[j] = wide_load_slot<T>(buf, (kk * 4 + kg) * WIDE_ROWS_TILE + (wm * 4 + j) * 16 + tl);
 #pragma unroll
         for (int i = 0; i < NI; ++i)
 #pragma unroll
