@@ -4,9 +4,10 @@
   oracle, every draft and verify logit row within 2e-2 max-abs (bf16 weights and KV cache), the
   drafted tokens, n_accept and the bonus token where the oracle's top-2 gap exceeds twice that;
   then the speculative decode (k=4) is bit-exact to the GPU's own plain greedy decode (k=0).
-* 4B at batch 8 with ragged prompt lengths (uniform in [256, 2048]): the shortest sequence's first
-  round against the oracle inside the batch, and every sequence's batched decode bit-exact to the
-  same sequence decoded alone and to plain greedy decoding.
+* 4B at batch 8 with ragged prompt lengths (uniform in [256, 2048]): every sequence's first round
+  against the oracle inside the batch (one batched draft and one batched verification of the
+  oracle's drafts, 40 rows), and every sequence's batched decode bit-exact to the same sequence
+  decoded alone and to plain greedy decoding.
 * 28L-h2048 and 4B-36L-h2560, three consecutive rounds from one prefill (the second with drafts
   forced to the oracle's greedy continuation, so it accepts all four and the third round's drafter
   reads decoder-layer keys/values that a verification wrote): every round's draft and verify
@@ -51,9 +52,9 @@ def weights_4b():
     yield w
 
 
-def oracle_first_round(cfg, w, prompt):
+def oracle_first_round(cfg, w, prompt, m=None):
     say(f"[gpu] oracle prefill {cfg.name} over {len(prompt)} tokens")
-    m = oracle_model(cfg, w)
+    m = m if m is not None else oracle_model(cfg, w)
     st = os_.prefill(m, prompt, capacity=len(prompt) + K + 2)
     drafts, qlog = os_.draft(st, K)
     plog = os_.verify(st, drafts)
@@ -205,20 +206,23 @@ def test_batch8_ragged_matches_alone_greedy_and_oracle(weights_4b):
     ctx = max(lens) + N_NEW + 2 * K + 2
     dec = decoder(cfg, weights_4b, max_batch=cfg.batch, max_ctx=ctx, max_draft=K)
     try:
-        # the shortest sequence's first round, inside the batch, against the oracle
-        b = int(np.argmin(lens))
+        # every sequence's first round, inside the batch, against the oracle: one batched draft,
+        # then (after a fresh prefill) one batched verification of the oracle's drafts
         dec.prefill(prompts)
         d, qlog = dec.draft(K, logits=True)
-        rd = oracle_first_round(cfg, weights_4b, prompts[b])
+        m = oracle_model(cfg, weights_4b)
+        rds = [oracle_first_round(cfg, weights_4b, p, m) for p in prompts]
         dec.prefill(prompts)
-        drafts = d.copy()
-        drafts[b] = rd.drafts[1:]
-        na, bo, vlog = dec.verify(K, drafts=drafts.astype(np.int32), logits=True)
-        compare_round(rd, d[b], qlog[b], int(na[b]), int(bo[b]), vlog[b])
+        drafts = np.stack([rd.drafts[1:] for rd in rds]).astype(np.int32)
+        na, bo, vlog = dec.verify(K, drafts=drafts, logits=True)
+        for b, rd in enumerate(rds):
+            say(f"[gpu] sequence {b} (len {lens[b]}) first round against the oracle")
+            compare_round(rd, d[b], qlog[b], int(na[b]), int(bo[b]), vlog[b])
         bl = int(np.argmax(lens))
         pl = lens[bl] - 1
         check_sampled_kv(cfg, weights_4b, dec, bl, np.concatenate([prompts[bl], drafts[bl]]),
-                         [0, 17, pl // 2, pl - 1] + list(range(pl, pl + K + 1)))
+                         [0, 17, pl // 2, pl - 1] + list(range(pl, pl + K + 1)), m=m)
+        del m
         say(f"[gpu] batch generate {N_NEW} tokens each, k={K}")
         out_b, cnt, _ = dec.generate(prompts, K, N_NEW, use_graph=True)
         assert np.all(cnt == N_NEW)
