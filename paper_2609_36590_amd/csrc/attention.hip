@@ -437,6 +437,138 @@ __global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
   }
 }
 
+// Causal attention of a wide single-sequence pass (the prompt's prefill, more than 64 rows at a
+// time). The decode kernel above spreads a row-block's positions over groups of workgroups and
+// merges their partials in a second launch, which suits a few rows over a long cache; across a
+// whole prompt it re-reads every key/value once per 32-query-vector row-block and writes a partial
+// per group. Here a workgroup owns 64 query vectors (64 / G rows of the G query heads of one KV
+// head, one 16-vector tile per wave) and each wave streams every visible 16-position tile in
+// order with an online softmax (the same per-tile contractions, masking and base-2 softmax as the
+// decode kernel), so the output is written directly: no partials, no merge launch, and each tile
+// is fetched from memory once per workgroup (the four waves read it from the CU's cache).
+// Tiles are loaded two ahead into registers; every load is issued unconditionally (a tile past the
+// last visible one reloads that tile and is fully masked), and the block table is staged in LDS so
+// that no key/value address waits on a global load.
+template <typename T, int HD>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k_attention_prefill(AttnArgs a) {
+  constexpr int DS = HD / 32, DT = HD / 16;
+  extern __shared__ int s_bt[];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, tl = lane & 15, kg = lane >> 4;
+  const int rows_wg = 64 / a.G;
+  const int n_rbp = (a.R + rows_wg - 1) / rows_wg;
+  // the row-blocks with the most tiles first, so that the short ones fill the tail
+  const int rbp = n_rbp - 1 - (int)blockIdx.x / a.n_kv, h = (int)blockIdx.x % a.n_kv;
+  const int r0 = rbp * rows_wg, nr = min(rows_wg, a.R - r0);
+  const int maxpos = a.row_pos[r0 + nr - 1];
+  const int t_last = maxpos >> 4;
+  for (int i0 = 0; i0 <= t_last; i0 += 4 * (int)blockDim.x) {   // 4 entries per thread in flight
+    int e[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) e[u] = a.bt[min(i0 + u * (int)blockDim.x + (int)threadIdx.x, t_last)];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u * (int)blockDim.x + (int)threadIdx.x;
+      if (i <= t_last) s_bt[i] = e[u];
+    }
+  }
+
+  // this lane's query vector qv = wave*16 + tl: row qv / G, head qv % G of the KV head's group
+  const int qv = wave * 16 + tl;
+  const bool qok = qv < nr * a.G;
+  const int rl = qok ? qv / a.G : 0, gq = qok ? qv - (qv / a.G) * a.G : 0;
+  const int qpos = qok ? a.row_pos[r0 + rl] : -1;
+  const int qstride = a.n_heads * HD;
+  const float* qp = a.q + (size_t)(r0 + rl) * qstride + (h * a.G + gq) * HD;
+  typename ET<T>::B qf[DS];
+#pragma unroll
+  for (int ds = 0; ds < DS; ++ds) {
+    float x[8];
+    load8(qp + ds * 32 + kg * 8, x);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) x[j] = qok ? x[j] * a.scale_log2 : 0.f;
+    qf[ds] = ET<T>::split(x);
+  }
+  __syncthreads();   // the block table is in LDS
+
+  const T* kvp = reinterpret_cast<const T*>(a.kv);
+  const size_t layer_base = (size_t)a.layer * a.n_blocks;
+  typedef typename ET<T>::A KA;
+  typedef typename PV<T>::A VA;
+  auto load_tile = [&](KA (&kf)[DS], VA (&vf)[DT], int t) {
+    const int blk = s_bt[min(t, t_last)];
+    const T* kp = kvp + (((layer_base + blk) * 2 + 0) * a.n_kv + h) * 16 * HD + tl * HD + kg * 8;
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds) kf[ds] = ET<T>::load(kp + ds * 32);
+    const T* vp = kvp + (((layer_base + blk) * 2 + 1) * a.n_kv + h) * HD * 16 + tl * 16 + 4 * kg;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) vf[dt] = PV<T>::load(vp + dt * 16 * 16);
+  };
+  float m_c = NEG_INF, l_c = 0.f;
+  f32x4 o_c[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) o_c[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto consume = [&](const KA (&kf)[DS], const VA (&vf)[DT], int t) {
+    f32x4 sacc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ds = 0; ds < DS; ++ds) ET<T>::mma(sacc, kf[ds], qf[ds]);
+    float sv[4], mx = NEG_INF;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int pos = 16 * t + 4 * kg + i;
+      sv[i] = pos <= qpos ? sacc[i] : NEG_INF;
+      mx = fmaxf(mx, sv[i]);
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float m_n = fmaxf(m_c, mx);
+    const float alpha = (m_c == NEG_INF) ? 0.f : exp2f(m_c - m_n);
+    float pr[4], sum = 0.f;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      pr[i] = (m_n == NEG_INF) ? 0.f : exp2f(sv[i] - m_n);
+      sum += pr[i];
+    }
+    sum += __shfl_xor(sum, 16);
+    sum += __shfl_xor(sum, 32);
+    l_c = l_c * alpha + sum;
+    m_c = m_n;
+    const typename PV<T>::B pf = PV<T>::split(pr);
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) o_c[dt][i] *= alpha;
+      PV<T>::mma(o_c[dt], vf[dt], pf);
+    }
+  };
+
+  KA ka[DS], kb[DS];
+  VA va[DT], vb[DT];
+  // tile 0's loads strictly before tile 1's, here as in the loop: if the scheduler issued them in
+  // the other order, the first use of tile 0 would have to wait for both tiles on every iteration
+  load_tile(ka, va, 0);
+  __builtin_amdgcn_sched_barrier(0);
+  load_tile(kb, vb, 1);
+  __builtin_amdgcn_sched_barrier(0);
+  for (int t = 0; t <= t_last; t += 2) {
+    consume(ka, va, t);
+    load_tile(ka, va, t + 2);
+    __builtin_amdgcn_sched_barrier(0);
+    consume(kb, vb, t + 1);   // past t_last: the last tile again, every position masked
+    load_tile(kb, vb, t + 3);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+
+  // lane (qv, kg) holds dims dt*16 + 4kg .. +3 of query vector qv
+  if (qok) {
+    float* op = a.out + (size_t)(r0 + rl) * qstride + (h * a.G + gq) * HD;
+    const float inv = 1.f / l_c;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+      *reinterpret_cast<float4*>(op + dt * 16 + 4 * kg) =
+          make_float4(o_c[dt][0] * inv, o_c[dt][1] * inv, o_c[dt][2] * inv, o_c[dt][3] * inv);
+  }
+}
+
 template <typename Kern>
 static void launch_kernel(Kern k, dim3 grid, hipStream_t s, const LaunchEvents* ev, const AttnArgs& a,
                           size_t lds = 0) {
@@ -489,6 +621,20 @@ void launch_attention(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev) 
   else launch_attention_hd<T, 64>(a, s, ev);
 }
 
+bool attention_prefill_supported(const AttnArgs& a) {
+  return a.B == 1 && a.G >= 1 && 64 % a.G == 0 && (a.head_dim == 128 || a.head_dim == 64) && a.s_block == 0 &&
+         !a.tree;
+}
+
+template <typename T>
+void launch_attention_prefill(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev) {
+  const int rows_wg = 64 / a.G;
+  const dim3 grid((unsigned)(((a.R + rows_wg - 1) / rows_wg) * a.n_kv));
+  const size_t lds = (size_t)a.bt_stride * sizeof(int);
+  if (a.head_dim == 128) launch_kernel(k_attention_prefill<T, 128>, grid, s, ev, a, lds);
+  else launch_kernel(k_attention_prefill<T, 64>, grid, s, ev, a, lds);
+}
+
 bool attention_needs_combine(const AttnArgs& a) { return a.n_groups_max > 1; }
 
 void launch_attn_combine(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev) {
@@ -500,5 +646,7 @@ void launch_attn_combine(const AttnArgs& a, hipStream_t s, const LaunchEvents* e
 
 template void launch_attention<uint16_t>(const AttnArgs&, hipStream_t, const LaunchEvents*);
 template void launch_attention<float>(const AttnArgs&, hipStream_t, const LaunchEvents*);
+template void launch_attention_prefill<uint16_t>(const AttnArgs&, hipStream_t, const LaunchEvents*);
+template void launch_attention_prefill<float>(const AttnArgs&, hipStream_t, const LaunchEvents*);
 
 }  // namespace seedk

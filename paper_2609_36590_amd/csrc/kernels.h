@@ -175,6 +175,11 @@ void launch_linear(const LinArgs& a, int prologue, int epilogue, int kind, hipSt
 // Attention partials per group of span positions (the final output when the rows see one group).
 template <typename T>
 void launch_attention(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev = nullptr);
+// Causal attention of a single-sequence pass of more than 64 rows (the prompt's prefill), written
+// directly (no partials): 64 query vectors per workgroup, every visible tile streamed in order.
+bool attention_prefill_supported(const AttnArgs& a);
+template <typename T>
+void launch_attention_prefill(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev = nullptr);
 // Merge of the group partials; needed when the context capacity spans more than one group.
 bool attention_needs_combine(const AttnArgs& a);
 // Positions per attention group for a context capacity (fixed per decoder, so that a query's

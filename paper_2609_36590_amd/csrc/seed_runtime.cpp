@@ -470,10 +470,15 @@ void run_layers(seed_ctx* c, int M, int B, int R, int l0, int l1, int phase,
     at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)p.HD));
     at.part = c->ws<float>(p.o_part);
     at.out = c->ws<float>(p.o_attn);
-    // a pass wider than the attention partial buffer (one sequence: prefill, the drafting
-    // objective) runs its rows ATT_ROWS at a time; every row attends to its own positions either way
+    // the prompt's prefill (one sequence, more than 64 rows): one launch over all of the pass's
+    // rows, written directly. Otherwise group partials and their merge; a pass wider than the
+    // partial buffer (the drafting objective's) runs its rows ATT_ROWS at a time, every row
+    // attending to its own positions either way
+    const bool whole_pass = B == 1 && R > MAX_ROWS && attention_prefill_supported(at);
+    if (whole_pass)
+      timed(c, phase, SEED_OP_ATTN, cap, [&](const LaunchEvents* ev) { launch_attention_prefill<T>(at, c->s, ev); });
     const int r_step = (B == 1 && R > MAX_ROWS) ? ATT_ROWS : R;
-    for (int r0 = 0; r0 < R; r0 += r_step) {
+    for (int r0 = 0; r0 < R && !whole_pass; r0 += r_step) {
       AttnArgs as = at;
       as.R = std::min(r_step, R - r0);
       as.n_rb = cdiv(as.R, p.RB);
