@@ -666,9 +666,10 @@ __global__ void __launch_bounds__(1024) k_splitk_reduce(LinArgs a, const float* 
 // pass): a compute-bound MFMA GEMM, Y[M, N] = X[M, K] W^T. A workgroup owns WIDE_WN n-tiles
 // (16 output features each) x WIDE_WM token tiles (16 rows each); its 8 waves form a 4 x 2 grid,
 // wave (wn, wm) accumulating WN/4 n-tiles for token tiles 4wm..4wm+3, so each weight fragment
-// feeds 4 token tiles and each activation fragment WN/4 n-tiles. WN = 16 where the projection has
-// at least 3072 outputs; 8 for the 2560-wide ones (O, down), which would otherwise give a pass of
-// 1024 rows only 80 workgroups. K runs in
+// feeds 4 token tiles and each activation fragment WN/4 n-tiles. WN (8, 12, 16 or 20) is chosen
+// per projection so that the grid fills whole rounds of one workgroup per CU: the cost is rounds x
+// WN (gate/up's 1216 n-tiles: 20 gives 2 rounds of 488 workgroups where 16 gives 3 of 608; QKV's
+// 384: 12 gives one round of 256; the 2560-wide O and down stay at 8, 160 workgroups). K runs in
 // chunks of WIDE_CK k-tiles: a chunk's activation rows are staged in LDS as bf16 hi/lo B-operand
 // slots, double-buffered (chunk c+1's global loads are issued before chunk c is consumed and
 // written to the other buffer after it), and the weight fragments of chunk c+1 are loaded into
@@ -678,14 +679,16 @@ __global__ void __launch_bounds__(1024) k_splitk_reduce(LinArgs a, const float* 
 // Workgroup order: the token tiles of one n-group are consecutive workgroups of one XCD (workgroup
 // w runs on XCD w mod 8), so that n-group's weights come from HBM once and from that XCD's L2 for
 // its other token tiles. The finished tile goes through the same epilogues as the narrow kernels,
-// 8 n-tiles at a time.
+// 8 (or 4) n-tiles at a time.
 // ---------------------------------------------------------------------------------------------
 constexpr int WIDE_WM = 8;    // token tiles per workgroup (128 rows)
 constexpr int WIDE_CK = 2;    // k-tiles per staged chunk
-constexpr int WIDE_EPI_NT = 8;   // n-tiles per epilogue half (the head's argmax partials are per 8)
+// n-tiles per epilogue group: 8 (the head's argmax partials are per 8 n-tiles), or 4 for workgroup
+// widths that are not a multiple of 8 (their epilogues are all tile-local)
+constexpr int wide_epi_nt(int wn) { return wn % 8 == 0 ? 8 : 4; }
 constexpr int WIDE_ROWS_TILE = WIDE_WM * 16;
 constexpr size_t WIDE_CHUNK_BYTES = (size_t)WIDE_CK * 4 * WIDE_ROWS_TILE * 32;   // one staging buffer
-constexpr size_t WIDE_LDS = 2 * WIDE_CHUNK_BYTES;   // = WIDE_EPI_NT x 128 rows x 16 fp32 outputs
+constexpr size_t WIDE_LDS = 2 * WIDE_CHUNK_BYTES;   // = 8 n-tiles x 128 rows x 16 fp32 outputs (the epilogue)
 
 // A staging buffer's B-operand slots. bf16: two planes, the 16-byte hi halves of all slots, then
 // the lo halves, so that the 16 lanes of a fragment read (consecutive slots) cover 256 contiguous
@@ -720,7 +723,7 @@ __device__ __forceinline__ typename ET<T>::B wide_load_slot(const char* buf, int
 }
 
 // row-indexed arguments of rows m0.. of a pass
-__device__ __forceinline__ LinArgs wide_rows(const LinArgs& a0, int m0, int Mt) {
+__device__ __forceinline__ LinArgs wide_rows(const LinArgs& a0, int m0, int Mt, int epi_nt) {
   LinArgs a = a0;
   const int n_tiles = a0.N >> 4;
   a.M = Mt;
@@ -738,7 +741,7 @@ __device__ __forceinline__ LinArgs wide_rows(const LinArgs& a0, int m0, int Mt) 
   if (a0.logits) a.logits = a0.logits + (long long)m0 * a0.ld_logits;
   if (a0.amax_val) a.amax_val = a0.amax_val + (size_t)m0 * a0.amax_stride;
   if (a0.amax_idx) a.amax_idx = a0.amax_idx + (size_t)m0 * a0.amax_stride;
-  a.NT = WIDE_EPI_NT;
+  a.NT = epi_nt;
   a.KS = 1;
   a.S = 1;
   a.NJ = 1;
@@ -761,7 +764,8 @@ __global__ void __launch_bounds__(512) k_linear_wide(LinArgs a0) {
   if (g >= NG) return;   // padding of the grid to whole XCD rounds; the workgroup leaves together
   const int m0 = mt * WIDE_ROWS_TILE;
   const int Mt = min(WIDE_ROWS_TILE, a0.M - m0);
-  const LinArgs a = wide_rows(a0, m0, Mt);
+  constexpr int EPI_NT = wide_epi_nt(WIDE_WN);
+  const LinArgs a = wide_rows(a0, m0, Mt, EPI_NT);
   const int wn = wave & 3, wm = wave >> 2;
 
   // weight fragments of n-tiles g*WN + NI*wn + i (past the last n-tile: the last one, never stored)
@@ -852,7 +856,7 @@ __global__ void __launch_bounds__(512) k_linear_wide(LinArgs a0) {
     __syncthreads();
   }
 
-  // RMSNorm row scales, then the tile in two halves of 8 n-tiles through the staging buffers:
+  // RMSNorm row scales, then the tile in groups of EPI_NT n-tiles through the staging buffers:
   // Y[lt][row][16], lane (tl, kg) holding features 4kg..4kg+3 of its n-tile for row (4wm+j)*16 + tl
   if constexpr (PRO == PRO_NORM) {
     const float ssv[4] = {0.f, 0.f, 0.f, 0.f};
@@ -863,30 +867,32 @@ __global__ void __launch_bounds__(512) k_linear_wide(LinArgs a0) {
   }
   float* Y = reinterpret_cast<float*>(lds);
   constexpr int YS = WIDE_ROWS_TILE * 16;   // floats per local n-tile
-  constexpr int HALVES = WIDE_WN / WIDE_EPI_NT;
+  constexpr int HALVES = WIDE_WN / EPI_NT;
 #pragma unroll
   for (int half = 0; half < HALVES; ++half) {
-    const Grp gr{HALVES * g + half, HALVES * NG};   // 8 n-tiles: (HALVES g + half) * 8 + local tile
+    const Grp gr{HALVES * g + half, HALVES * NG};   // n-tiles (HALVES g + half) * EPI_NT + local tile
     EpiPre epre{};
     epi_load<EPI>(a, gr, tid, epre);
-    if ((NI * wn) / WIDE_EPI_NT == half) {
 #pragma unroll
-      for (int i = 0; i < NI; ++i)
+    for (int i = 0; i < NI; ++i) {
+      const int lt = NI * wn + i;   // a wave's n-tiles may straddle two groups
+      if (lt / EPI_NT == half) {
 #pragma unroll
         for (int j = 0; j < 4; ++j)
-          *reinterpret_cast<float4*>(Y + (size_t)((NI * wn + i) % WIDE_EPI_NT) * YS + ((wm * 4 + j) * 16 + tl) * 16 + 4 * kg) =
+          *reinterpret_cast<float4*>(Y + (size_t)(lt % EPI_NT) * YS + ((wm * 4 + j) * 16 + tl) * 16 + 4 * kg) =
               make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+      }
     }
     __syncthreads();
     if constexpr (PRO == PRO_NORM) {
-      for (int e = tid; e < WIDE_EPI_NT * Mt * 16; e += 512) {
+      for (int e = tid; e < EPI_NT * Mt * 16; e += 512) {
         const int lt = e / (Mt * 16), rem = e - lt * Mt * 16;
         Y[(size_t)lt * YS + rem] *= s_rs[rem >> 4];
       }
       __syncthreads();
     }
     linear_epilogue<T, EPI>(a, gr, Y, YS, epre);
-    __syncthreads();   // the epilogue is done with Y before the second half overwrites it
+    __syncthreads();   // the epilogue is done with Y before the next group overwrites it
   }
 }
 
@@ -1082,6 +1088,29 @@ static void launch(K kernel, dim3 grid, dim3 block, size_t lds, hipStream_t s, c
   else hipLaunchKernelGGL(kernel, grid, block, lds, s, args...);
 }
 
+// Workgroup width (n-tiles) of a wide pass: the candidate with the lowest rounds x width x
+// per-tile cost, one workgroup per CU (the kernel holds ~200-240 registers per lane). The per-tile
+// cost falls with width, since an activation fragment feeds WN/4 n-tiles (128-feature tiles were
+// measured about 1.35x slower per tile than 256-feature ones). The LM head keeps 16 (its argmax
+// partials are per 8 n-tiles); only the tile-local epilogues take 12 (QKV) or 20 (gate/up).
+template <int EPI>
+static int wide_width(int n_tiles, int MT) {
+  const int cands[] = {16, 8, EPI == EPI_SWIGLU ? 20 : 0, EPI == EPI_QKV ? 12 : 0};
+  int best = n_tiles >= 192 ? 16 : 8;
+  long long best_cost = -1;
+  for (int wn : cands) {
+    if (wn == 0 || (EPI == EPI_HEAD && wn != 16 && n_tiles >= 192)) continue;
+    const int per_tile = wn == 8 ? 135 : wn == 12 ? 112 : wn == 16 ? 100 : 95;
+    const long long wgs = (long long)((n_tiles + wn - 1) / wn) * MT;
+    const long long cost = (wgs + 255) / 256 * wn * per_tile;
+    if (best_cost < 0 || cost < best_cost || (cost == best_cost && wn > best)) {
+      best = wn;
+      best_cost = cost;
+    }
+  }
+  return best;
+}
+
 template <typename T, int PRO, int EPI>
 static void launch_linear_pe(const LinArgs& a0, int kind, hipStream_t s, const LaunchEvents* ev) {
   LinArgs a = a0;
@@ -1097,12 +1126,16 @@ static void launch_linear_pe(const LinArgs& a0, int kind, hipStream_t s, const L
     return;
   }
   if (kind == LIN_WIDE) {
-    const int wn = n_tiles >= 192 ? 16 : 8;
-    const int NG = (n_tiles + wn - 1) / wn;
     const int MT = (a.M + WIDE_ROWS_TILE - 1) / WIDE_ROWS_TILE;
+    const int wn = wide_width<EPI>(n_tiles, MT);
+    const int NG = (n_tiles + wn - 1) / wn;
     const dim3 grid((unsigned)((NG + 7) / 8 * 8 * MT)), block(512);
-    if (wn == 16) launch(k_linear_wide<T, PRO, EPI, 16>, grid, block, WIDE_LDS, s, ev, a);
-    else launch(k_linear_wide<T, PRO, EPI, 8>, grid, block, WIDE_LDS, s, ev, a);
+    switch (wn) {
+      case 20: if constexpr (EPI == EPI_SWIGLU) launch(k_linear_wide<T, PRO, EPI, 20>, grid, block, WIDE_LDS, s, ev, a); break;
+      case 12: if constexpr (EPI == EPI_QKV) launch(k_linear_wide<T, PRO, EPI, 12>, grid, block, WIDE_LDS, s, ev, a); break;
+      case 16: launch(k_linear_wide<T, PRO, EPI, 16>, grid, block, WIDE_LDS, s, ev, a); break;
+      default: launch(k_linear_wide<T, PRO, EPI, 8>, grid, block, WIDE_LDS, s, ev, a); break;
+    }
     return;
   }
   if (kind == LIN_SPLITK) {
@@ -1198,6 +1231,12 @@ static bool allow_big_lds(int bytes) {
                        reinterpret_cast<const void*>(&k_linear_wide<T, PRO, EPI, 8>)};
   bool ok = true;
   for (const void* f : fns) ok &= hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes) == hipSuccess;
+  if constexpr (EPI == EPI_SWIGLU)
+    ok &= hipFuncSetAttribute(reinterpret_cast<const void*>(&k_linear_wide<T, PRO, EPI, 20>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, bytes) == hipSuccess;
+  if constexpr (EPI == EPI_QKV)
+    ok &= hipFuncSetAttribute(reinterpret_cast<const void*>(&k_linear_wide<T, PRO, EPI, 12>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, bytes) == hipSuccess;
   return ok;
 }
 
