@@ -449,9 +449,12 @@ __global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
 // Tiles are loaded two ahead into registers; every load is issued unconditionally (a tile past the
 // last visible one reloads that tile and is fully masked), and the block table is staged in LDS so
 // that no key/value address waits on a global load.
-template <typename T, int HD>
+// The block-causal variant (SPEC: the drafting objective's decoder pass) contracts every tile with
+// both caches, the deep one below each query's block start and the pass's own one from there to
+// the query, and selects per (query, position) as the decode kernel's SPEC variant does.
+template <typename T, int HD, bool SPEC>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k_attention_prefill(AttnArgs a) {
-  constexpr int DS = HD / 32, DT = HD / 16;
+  constexpr int DS = HD / 32, DT = HD / 16, NC = SPEC ? 2 : 1;
   extern __shared__ int s_bt[];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, tl = lane & 15, kg = lane >> 4;
   const int rows_wg = 64 / a.G;
@@ -477,6 +480,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
   const bool qok = qv < nr * a.G;
   const int rl = qok ? qv / a.G : 0, gq = qok ? qv - (qv / a.G) * a.G : 0;
   const int qpos = qok ? a.row_pos[r0 + rl] : -1;
+  const int qstart = SPEC ? (qpos < 0 ? 0 : (qpos / a.s_block) * a.s_block) : 0;
   const int qstride = a.n_heads * HD;
   const float* qp = a.q + (size_t)(r0 + rl) * qstride + (h * a.G + gq) * HD;
   typename ET<T>::B qf[DS];
@@ -494,28 +498,39 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
   const size_t layer_base = (size_t)a.layer * a.n_blocks;
   typedef typename ET<T>::A KA;
   typedef typename PV<T>::A VA;
-  auto load_tile = [&](KA (&kf)[DS], VA (&vf)[DT], int t) {
-    const int blk = s_bt[min(t, t_last)];
-    const T* kp = kvp + (((layer_base + blk) * 2 + 0) * a.n_kv + h) * 16 * HD + tl * HD + kg * 8;
+  // cache 0: the deep cache through the block table; cache 1 (SPEC): the pass's own, by position
+  auto load_tile = [&](KA (&kf)[NC][DS], VA (&vf)[NC][DT], int t) {
+    const int tc = min(t, t_last);
 #pragma unroll
-    for (int ds = 0; ds < DS; ++ds) kf[ds] = ET<T>::load(kp + ds * 32);
-    const T* vp = kvp + (((layer_base + blk) * 2 + 1) * a.n_kv + h) * HD * 16 + tl * 16 + 4 * kg;
+    for (int cc = 0; cc < NC; ++cc) {
+      const T* base = cc == 0 ? kvp : reinterpret_cast<const T*>(a.skv);
+      const size_t blk = cc == 0 ? layer_base + s_bt[tc] : (size_t)a.s_layer * a.s_n_blocks + tc;
+      const T* kp = base + ((blk * 2 + 0) * a.n_kv + h) * 16 * HD + tl * HD + kg * 8;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) vf[dt] = PV<T>::load(vp + dt * 16 * 16);
+      for (int ds = 0; ds < DS; ++ds) kf[cc][ds] = ET<T>::load(kp + ds * 32);
+      const T* vp = base + ((blk * 2 + 1) * a.n_kv + h) * HD * 16 + tl * 16 + 4 * kg;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) vf[cc][dt] = PV<T>::load(vp + dt * 16 * 16);
+    }
   };
   float m_c = NEG_INF, l_c = 0.f;
   f32x4 o_c[DT];
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) o_c[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  auto consume = [&](const KA (&kf)[DS], const VA (&vf)[DT], int t) {
-    f32x4 sacc = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto consume = [&](const KA (&kf)[NC][DS], const VA (&vf)[NC][DT], int t) {
+    f32x4 sacc[NC];
 #pragma unroll
-    for (int ds = 0; ds < DS; ++ds) ET<T>::mma(sacc, kf[ds], qf[ds]);
+    for (int cc = 0; cc < NC; ++cc) {
+      sacc[cc] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ds = 0; ds < DS; ++ds) ET<T>::mma(sacc[cc], kf[cc][ds], qf[ds]);
+    }
     float sv[4], mx = NEG_INF;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int pos = 16 * t + 4 * kg + i;
-      sv[i] = pos <= qpos ? sacc[i] : NEG_INF;
+      if constexpr (SPEC) sv[i] = pos > qpos ? NEG_INF : (pos < qstart ? sacc[0][i] : sacc[1][i]);
+      else sv[i] = pos <= qpos ? sacc[0][i] : NEG_INF;
       mx = fmaxf(mx, sv[i]);
     }
     mx = fmaxf(mx, __shfl_xor(mx, 16));
@@ -532,17 +547,31 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
     sum += __shfl_xor(sum, 32);
     l_c = l_c * alpha + sum;
     m_c = m_n;
-    const typename PV<T>::B pf = PV<T>::split(pr);
+    typename PV<T>::B pf[NC];
+    if constexpr (SPEC) {
+      float pd[4], ps[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const bool deep = 16 * t + 4 * kg + i < qstart;
+        pd[i] = deep ? pr[i] : 0.f;
+        ps[i] = deep ? 0.f : pr[i];
+      }
+      pf[0] = PV<T>::split(pd);
+      pf[NC - 1] = PV<T>::split(ps);
+    } else {
+      pf[0] = PV<T>::split(pr);
+    }
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) o_c[dt][i] *= alpha;
-      PV<T>::mma(o_c[dt], vf[dt], pf);
+#pragma unroll
+      for (int cc = 0; cc < NC; ++cc) PV<T>::mma(o_c[dt], vf[cc][dt], pf[cc]);
     }
   };
 
-  KA ka[DS], kb[DS];
-  VA va[DT], vb[DT];
+  KA ka[NC][DS], kb[NC][DS];
+  VA va[NC][DT], vb[NC][DT];
   // tile 0's loads strictly before tile 1's, here as in the loop: if the scheduler issued them in
   // the other order, the first use of tile 0 would have to wait for both tiles on every iteration
   load_tile(ka, va, 0);
@@ -622,8 +651,7 @@ void launch_attention(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev) 
 }
 
 bool attention_prefill_supported(const AttnArgs& a) {
-  return a.B == 1 && a.G >= 1 && 64 % a.G == 0 && (a.head_dim == 128 || a.head_dim == 64) && a.s_block == 0 &&
-         !a.tree;
+  return a.B == 1 && a.G >= 1 && 64 % a.G == 0 && (a.head_dim == 128 || a.head_dim == 64) && !a.tree;
 }
 
 template <typename T>
@@ -631,8 +659,13 @@ void launch_attention_prefill(const AttnArgs& a, hipStream_t s, const LaunchEven
   const int rows_wg = 64 / a.G;
   const dim3 grid((unsigned)(((a.R + rows_wg - 1) / rows_wg) * a.n_kv));
   const size_t lds = (size_t)a.bt_stride * sizeof(int);
-  if (a.head_dim == 128) launch_kernel(k_attention_prefill<T, 128>, grid, s, ev, a, lds);
-  else launch_kernel(k_attention_prefill<T, 64>, grid, s, ev, a, lds);
+  if (a.s_block > 0) {
+    if (a.head_dim == 128) launch_kernel(k_attention_prefill<T, 128, true>, grid, s, ev, a, lds);
+    else launch_kernel(k_attention_prefill<T, 64, true>, grid, s, ev, a, lds);
+  } else {
+    if (a.head_dim == 128) launch_kernel(k_attention_prefill<T, 128, false>, grid, s, ev, a, lds);
+    else launch_kernel(k_attention_prefill<T, 64, false>, grid, s, ev, a, lds);
+  }
 }
 
 bool attention_needs_combine(const AttnArgs& a) { return a.n_groups_max > 1; }
