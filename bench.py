@@ -60,9 +60,10 @@ def kernel_bytes(cfg, op, M, L):
     return 0
 
 
-def attention_span(max_ctx):
-    """Positions per attention group for a context capacity (the runtime's rule)."""
-    return 64 if max_ctx <= 4096 else (128 if max_ctx <= 8192 else 256)
+def attention_span(max_ctx, max_batch):
+    """Positions per attention group for a context and batch capacity (the runtime's rule)."""
+    small = 4096 if max_batch == 1 else 2048
+    return 64 if max_ctx <= small else (128 if max_ctx <= 8192 else 256)
 
 
 def combine_bytes(cfg, M, L, group):
@@ -691,7 +692,7 @@ def profile_workload(torch, cfg, k, args):
             if op == binding.OP_ATTN:   # every sequence's keys/values at its own context
                 b_op = sum(kernel_bytes(cfg, op, 0, L) for L in Ls) + M * cfg.q_dim * 4
             elif op == binding.OP_COMBINE:
-                b_op = sum(combine_bytes(cfg, M // B, L, attention_span(max_ctx)) for L in Ls)
+                b_op = sum(combine_bytes(cfg, M // B, L, attention_span(max_ctx, B)) for L in Ls)
             else:
                 b_op = kernel_bytes(cfg, op, M, int(np.mean(Ls)))
             name = ("verify_" if phase == binding.PHASE_VERIFY else "draft_") + OP_NAMES[op]
@@ -866,7 +867,7 @@ def main():
         L_here = len(dec.tokens(0)) - probe_rounds // 2
         name = ("verify_" if phase == binding.PHASE_VERIFY else "draft_") + names[op]
         avg = ms / n
-        b = (combine_bytes(cfg, M, L_here, attention_span(max_ctx)) if op == binding.OP_COMBINE
+        b = (combine_bytes(cfg, M, L_here, attention_span(max_ctx, 1)) if op == binding.OP_COMBINE
              else kernel_bytes(cfg, op, M, L_here))
         per_kernel[name] = {"launches_per_round": n / probe_rounds, "avg_us": avg * 1e3,
                             "us_per_round": avg * 1e3 * n / probe_rounds,

@@ -642,10 +642,15 @@ static void launch_attention_hd(const AttnArgs& a, hipStream_t s, const LaunchEv
   }
 }
 
-// 64 positions per group up to 2048 (the 1k-context workloads), 128 up to 8192 (the batch-8
-// workload's ~2300: verification attention 19.7 -> 17.4 us per layer and its merge 9.3 -> 7.6 us
-// against 64; 256 gave 19.3), 256 beyond (16k)
-int attention_span(int max_ctx) { return max_ctx <= 2048 ? 64 : (max_ctx <= 8192 ? 128 : 256); }
+// One sequence: 64 positions per group up to 4096 (at its ~1.2k-position context, 1024-token
+// prompt, 128-position groups leave half the 160 workgroups of a launch out: verification
+// attention 7.9 -> 9.6 us per layer). Several sequences fill the chip sooner: 64 up to 2048, then
+// 128 (batch 8 at ~2300 positions: verification attention 19.7 -> 17.4 us per layer and its merge
+// 9.3 -> 7.6 us against 64; 256 gave 19.3). 256 beyond 8192 positions (16k contexts).
+int attention_span(int max_ctx, int max_batch) {
+  const int small = max_batch == 1 ? 4096 : 2048;
+  return max_ctx <= small ? 64 : (max_ctx <= 8192 ? 128 : 256);
+}
 
 template <typename T>
 void launch_attention(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev) {

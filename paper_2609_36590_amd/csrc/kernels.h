@@ -182,9 +182,9 @@ template <typename T>
 void launch_attention_prefill(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev = nullptr);
 // Merge of the group partials; needed when the context capacity spans more than one group.
 bool attention_needs_combine(const AttnArgs& a);
-// Positions per attention group for a context capacity (fixed per decoder, so that a query's
-// merge tree depends only on absolute positions).
-int attention_span(int max_ctx);
+// Positions per attention group for a context capacity and batch capacity (fixed per decoder, so
+// that a query's merge tree depends only on absolute positions).
+int attention_span(int max_ctx, int max_batch);
 void launch_attn_combine(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev = nullptr);
 template <typename T>
 void launch_setup(const SetupArgs& a, hipStream_t s);

@@ -114,7 +114,7 @@ Plan make_plan(const seed_config& c) {
   p.max_rows = std::max(MAX_ROWS, PREFILL_ROWS);   // decode passes (B (d+1) <= 64), draft trees of <= 64
                                                   // nodes, prefill and drafting-objective passes
   p.blocks_per_seq = cdiv(c.max_ctx, 16);
-  p.span = seedk::attention_span(c.max_ctx);
+  p.span = seedk::attention_span(c.max_ctx, c.max_batch);
   p.bt_stride = cdiv(p.blocks_per_seq, p.span / 16) * (p.span / 16);   // whole groups, padded with block 0
   p.n_blocks = c.max_batch * p.blocks_per_seq + 1;                  // block 0 = permanent zero block
 

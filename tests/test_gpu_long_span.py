@@ -1,7 +1,8 @@
 """GPU parity of the wider attention groups against the oracle.
 
-A decoder's context capacity fixes how many positions one attention workgroup covers: 64 up to
-4096, 128 up to 8192 and 256 beyond (so a query's merge tree depends only on absolute positions).
+A decoder's context and batch capacities fix how many positions one attention workgroup covers:
+for one sequence 64 up to 4096, 128 up to 8192 and 256 beyond (several sequences take 128 from 2049
+on), so that a query's merge tree depends only on absolute positions.
 The other GPU tests run small capacities (64-position groups); these cases build the tiny models
 with capacities 6000 and 9000 and a 600-token prompt, so the 128- and 256-position groups run
 several groups per query and merge them in the combine kernel, for each attention variant:
