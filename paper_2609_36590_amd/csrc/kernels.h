@@ -162,6 +162,7 @@ struct DevState {
 enum LinearKind { LIN_LDS = 0, LIN_GLOBAL = 1, LIN_SPLITK = 2, LIN_WIDE = 3 };
 constexpr int LDS_MAX_PASSES = 8;   // n-tile passes (NJ) of one k_linear_lds workgroup
 constexpr int HEAD_WIDE_NT = 16;    // n-tiles (waves) per workgroup of the LM head for 17..64 rows
+constexpr int WIDE_SPLIT_MAX = 4;   // k-ranges of a split wide pass (its partials: WIDE_SPLIT_MAX x rows x N floats)
 
 // Optional timing events stamped by the launches themselves (hipExtLaunchKernel): `start` at the
 // start of the first kernel of the operation, `stop` at the end of its last kernel.

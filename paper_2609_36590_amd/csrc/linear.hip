@@ -748,20 +748,25 @@ __device__ __forceinline__ LinArgs wide_rows(const LinArgs& a0, int m0, int Mt, 
   return a;
 }
 
-template <typename T, int PRO, int EPI, int WIDE_WN>
+template <typename T, int PRO, int EPI, int WIDE_WN, bool SPLIT>
 __global__ void __launch_bounds__(512) k_linear_wide(LinArgs a0) {
   constexpr int NI = WIDE_WN / 4;   // n-tiles per wave
   extern __shared__ __attribute__((aligned(16))) char lds[];
   __shared__ float s_rs[WIDE_ROWS_TILE];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int tl = lane & 15, kg = lane >> 4;
-  const int KT = a0.K >> 5, n_tiles = a0.N >> 4;
+  const int KTF = a0.K >> 5, n_tiles = a0.N >> 4;
   const int NG = (n_tiles + WIDE_WN - 1) / WIDE_WN;
   const int MT = (a0.M + WIDE_ROWS_TILE - 1) / WIDE_ROWS_TILE;
-  // workgroup -> (n-group, token tile): the MT token tiles of n-group g share the XCD g mod 8
+  // SPLIT: K in a0.KS k-ranges, each (n-group, k-range) pair a virtual n-group of its own
+  const int S = SPLIT ? a0.KS : 1;
+  // workgroup -> (virtual n-group, token tile): the MT token tiles of virtual n-group gv share the
+  // XCD gv mod 8
   const int b = blockIdx.x, xcd = b & 7, r = b >> 3;
-  const int mt = r % MT, g = (r / MT) * 8 + xcd;
-  if (g >= NG) return;   // padding of the grid to whole XCD rounds; the workgroup leaves together
+  const int mt = r % MT, gv = (r / MT) * 8 + xcd;
+  if (gv >= NG * S) return;   // padding of the grid to whole XCD rounds; the workgroup leaves together
+  const int g = gv / S, ks = gv - g * S;
+  const int kt0 = (ks * KTF) / S, KT = ((ks + 1) * KTF) / S - kt0;   // this workgroup's k-tiles
   const int m0 = mt * WIDE_ROWS_TILE;
   const int Mt = min(WIDE_ROWS_TILE, a0.M - m0);
   constexpr int EPI_NT = wide_epi_nt(WIDE_WN);
@@ -773,8 +778,9 @@ __global__ void __launch_bounds__(512) k_linear_wide(LinArgs a0) {
 #pragma unroll
   for (int i = 0; i < NI; ++i) {
     const int nt = min(g * WIDE_WN + NI * wn + i, n_tiles - 1);
-    wp[i] = reinterpret_cast<const T*>(a.W) + (size_t)nt * KT * 512 + lane * 8;
+    wp[i] = reinterpret_cast<const T*>(a.W) + ((size_t)nt * KTF + kt0) * 512 + lane * 8;
   }
+  const float* X = a.X + (size_t)kt0 * 32;
   // staged slot q = (ktl*4 + kg') * 128 + row holds x[row][32 (c*CK + ktl) + 8 kg' .. +7]; rows past
   // the tile's last row read its last row (their outputs are never stored). A chunk is read as
   // (8 rows x one k-tile) blocks, one per wave and load: lane (r, e) takes floats 4e..4e+3 of the
@@ -790,7 +796,7 @@ __global__ void __launch_bounds__(512) k_linear_wide(LinArgs a0) {
       const int blk = u * 8 + wave, ktl = blk % WIDE_CK;
       const int rr = min((blk / WIDE_CK) * 8 + (lane >> 3), Mt - 1);
       const int kt = min(c * WIDE_CK + ktl, KT - 1);
-      xv[u] = *reinterpret_cast<const float4*>(a.X + (size_t)rr * a.ldx + kt * 32 + (lane & 7) * 4);
+      xv[u] = *reinterpret_cast<const float4*>(X + (size_t)rr * a.ldx + kt * 32 + (lane & 7) * 4);
     }
   };
   auto stage_store = [&](int c) {
@@ -856,6 +862,24 @@ __global__ void __launch_bounds__(512) k_linear_wide(LinArgs a0) {
     __syncthreads();
   }
 
+  if constexpr (SPLIT) {
+    // the k-range's partial tile: part[ks][row][feature] over the pass's rows, added in k-range
+    // order by k_wide_splitk_reduce, which runs the epilogue
+    float* pp = a0.part + ((size_t)ks * a0.M + m0) * a0.N;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int nt = g * WIDE_WN + NI * wn + i;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int row = (wm * 4 + j) * 16 + tl;
+        if (nt < n_tiles && row < Mt)
+          *reinterpret_cast<float4*>(pp + (size_t)row * a0.N + nt * 16 + 4 * kg) =
+              make_float4(acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]);
+      }
+    }
+    return;
+  }
+
   // RMSNorm row scales, then the tile in groups of EPI_NT n-tiles through the staging buffers:
   // Y[lt][row][16], lane (tl, kg) holding features 4kg..4kg+3 of its n-tile for row (4wm+j)*16 + tl
   if constexpr (PRO == PRO_NORM) {
@@ -893,6 +917,53 @@ __global__ void __launch_bounds__(512) k_linear_wide(LinArgs a0) {
     }
     linear_epilogue<T, EPI>(a, gr, Y, YS, epre);
     __syncthreads();   // the epilogue is done with Y before the next group overwrites it
+  }
+}
+
+// k-range partials of a split wide pass (the residual projections) added in k-range order from 0,
+// then the residual epilogue of linear_epilogue (h += y, xg = h * gain of the next norm, and the
+// per-16-feature sums of squares in the same xor order): a workgroup per 128 features x
+// WIDE_RED_ROWS rows, 4 rows per thread with all their loads issued before the first store, each
+// row's 128 features read and written as one contiguous 512-byte run.
+constexpr int WIDE_RED_ROWS = 16;
+__global__ void __launch_bounds__(512) k_wide_splitk_resid(LinArgs a, const float* part) {
+  constexpr int RPT = WIDE_RED_ROWS / 4;   // rows per thread
+  const int tid = threadIdx.x, f = tid & 127, rsub = tid >> 7;
+  const int n_tiles = a.N >> 4, nt = blockIdx.x * 8 + (f >> 4);
+  const int m0 = blockIdx.y * WIDE_RED_ROWS;
+  const size_t stride = (size_t)a.M * a.N;
+  const int S = a.KS;
+  if (nt >= n_tiles) return;   // whole 16-lane groups leave together
+  const int col = nt * 16 + (f & 15);
+  const float g = a.gain_next[col];
+  float v[RPT][WIDE_SPLIT_MAX], h[RPT];
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) {
+    const int m = min(m0 + rsub + 4 * i, a.M - 1);   // rows past the pass re-read its last row, never stored
+    const size_t off = (size_t)m * a.N + col;
+#pragma unroll
+    for (int k = 0; k < WIDE_SPLIT_MAX; ++k) v[i][k] = k < S ? part[k * stride + off] : 0.f;
+    h[i] = a.h[off];
+  }
+#pragma unroll
+  for (int i = 0; i < RPT; ++i) {
+    const int m = m0 + rsub + 4 * i;   // uniform across the wave (a wave is 64 features of one row)
+    float y = 0.f;
+#pragma unroll
+    for (int k = 0; k < WIDE_SPLIT_MAX; ++k)
+      if (k < S) y += v[i][k];
+    const float hv = h[i] + y;
+    float s = hv * hv;
+    s += __shfl_xor(s, 8);
+    s += __shfl_xor(s, 4);
+    s += __shfl_xor(s, 2);
+    s += __shfl_xor(s, 1);
+    if (m < a.M) {
+      const size_t off = (size_t)m * a.N + col;
+      a.h[off] = hv;
+      a.xg[off] = hv * g;
+      if ((f & 15) == 0) a.ssq_out[(size_t)m * n_tiles + nt] = s;
+    }
   }
 }
 
@@ -1111,6 +1182,19 @@ static int wide_width(int n_tiles, int MT) {
   return best;
 }
 
+// K-ranges of a residual projection's wide pass (8-n-tile workgroups): as many as keep the
+// workgroups of a 1024-row pass (8 token tiles) within two per CU (two 64 KB-LDS workgroups fit one
+// CU), at most WIDE_SPLIT_MAX. The count depends on the shape only, so a row's output does not
+// depend on the pass's row count. The 2560-wide projections of the 4B model (20 n-groups) take 3:
+// 480 workgroups; measured on its 1024-token prefill: 26.7 ms unsplit, 27.3 / 24.7 / 25.5 ms with
+// 2 / 3 / 4 k-ranges (2 leaves 64 CUs with two workgroups and the rest with one, 4 needs a third).
+static int wide_split(int n_tiles, int KT) {
+  constexpr int SLOTS = 2 * 256, MT_REF = 8;
+  const int ng = (n_tiles + 7) / 8;
+  const int S = std::max(1, std::min(SLOTS / (ng * MT_REF), WIDE_SPLIT_MAX));
+  return std::min(S, KT);
+}
+
 template <typename T, int PRO, int EPI>
 static void launch_linear_pe(const LinArgs& a0, int kind, hipStream_t s, const LaunchEvents* ev) {
   LinArgs a = a0;
@@ -1130,11 +1214,23 @@ static void launch_linear_pe(const LinArgs& a0, int kind, hipStream_t s, const L
     const int wn = wide_width<EPI>(n_tiles, MT);
     const int NG = (n_tiles + wn - 1) / wn;
     const dim3 grid((unsigned)((NG + 7) / 8 * 8 * MT)), block(512);
+    if constexpr (PRO == PRO_PLAIN && EPI == EPI_RESID) {
+      const int S = wn == 8 ? wide_split(n_tiles, a.K >> 5) : 1;
+      if (S > 1) {
+        a.KS = S;
+        const LaunchEvents e0{ev ? ev->start : nullptr, nullptr}, e1{nullptr, ev ? ev->stop : nullptr};
+        launch(k_linear_wide<T, PRO, EPI, 8, true>, dim3((unsigned)((NG * S + 7) / 8 * 8 * MT)), block, WIDE_LDS, s,
+               ev ? &e0 : nullptr, a);
+        const dim3 rgrid((unsigned)((n_tiles + 7) / 8), (unsigned)((a.M + WIDE_RED_ROWS - 1) / WIDE_RED_ROWS));
+        launch(k_wide_splitk_resid, rgrid, block, 0, s, ev ? &e1 : nullptr, a, (const float*)a.part);
+        return;
+      }
+    }
     switch (wn) {
-      case 20: if constexpr (EPI == EPI_SWIGLU) launch(k_linear_wide<T, PRO, EPI, 20>, grid, block, WIDE_LDS, s, ev, a); break;
-      case 12: if constexpr (EPI == EPI_QKV) launch(k_linear_wide<T, PRO, EPI, 12>, grid, block, WIDE_LDS, s, ev, a); break;
-      case 16: launch(k_linear_wide<T, PRO, EPI, 16>, grid, block, WIDE_LDS, s, ev, a); break;
-      default: launch(k_linear_wide<T, PRO, EPI, 8>, grid, block, WIDE_LDS, s, ev, a); break;
+      case 20: if constexpr (EPI == EPI_SWIGLU) launch(k_linear_wide<T, PRO, EPI, 20, false>, grid, block, WIDE_LDS, s, ev, a); break;
+      case 12: if constexpr (EPI == EPI_QKV) launch(k_linear_wide<T, PRO, EPI, 12, false>, grid, block, WIDE_LDS, s, ev, a); break;
+      case 16: launch(k_linear_wide<T, PRO, EPI, 16, false>, grid, block, WIDE_LDS, s, ev, a); break;
+      default: launch(k_linear_wide<T, PRO, EPI, 8, false>, grid, block, WIDE_LDS, s, ev, a); break;
     }
     return;
   }
@@ -1227,15 +1323,18 @@ static bool allow_big_lds(int bytes) {
                        reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 2>),
                        reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 3>),
                        reinterpret_cast<const void*>(&k_linear_mfma<T, PRO, EPI, 4>),
-                       reinterpret_cast<const void*>(&k_linear_wide<T, PRO, EPI, 16>),
-                       reinterpret_cast<const void*>(&k_linear_wide<T, PRO, EPI, 8>)};
+                       reinterpret_cast<const void*>(&k_linear_wide<T, PRO, EPI, 16, false>),
+                       reinterpret_cast<const void*>(&k_linear_wide<T, PRO, EPI, 8, false>)};
   bool ok = true;
   for (const void* f : fns) ok &= hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes) == hipSuccess;
   if constexpr (EPI == EPI_SWIGLU)
-    ok &= hipFuncSetAttribute(reinterpret_cast<const void*>(&k_linear_wide<T, PRO, EPI, 20>),
+    ok &= hipFuncSetAttribute(reinterpret_cast<const void*>(&k_linear_wide<T, PRO, EPI, 20, false>),
                               hipFuncAttributeMaxDynamicSharedMemorySize, bytes) == hipSuccess;
   if constexpr (EPI == EPI_QKV)
-    ok &= hipFuncSetAttribute(reinterpret_cast<const void*>(&k_linear_wide<T, PRO, EPI, 12>),
+    ok &= hipFuncSetAttribute(reinterpret_cast<const void*>(&k_linear_wide<T, PRO, EPI, 12, false>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, bytes) == hipSuccess;
+  if constexpr (PRO == PRO_PLAIN && EPI == EPI_RESID)
+    ok &= hipFuncSetAttribute(reinterpret_cast<const void*>(&k_linear_wide<T, PRO, EPI, 8, true>),
                               hipFuncAttributeMaxDynamicSharedMemorySize, bytes) == hipSuccess;
   return ok;
 }

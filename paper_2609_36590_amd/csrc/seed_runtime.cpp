@@ -66,7 +66,7 @@ struct Plan {
   std::vector<size_t> w_attn_norm, w_mlp_norm, w_qkv, w_o, w_gu, w_down;
   size_t kv_total;
   // workspace
-  size_t o_h, o_xg, o_ssq, o_q, o_attn, o_act, o_part, o_row_seq, o_row_pos, o_row_slot, o_row_blk, o_row_rope, o_amax_val,
+  size_t o_wide_part, o_h, o_xg, o_ssq, o_q, o_attn, o_act, o_part, o_row_seq, o_row_pos, o_row_slot, o_row_blk, o_row_rope, o_amax_val,
       o_amax_idx, o_vtok;
   size_t o_t, o_len, o_limit, o_active, o_nacc, o_bonus, o_rounds, o_counters, o_drafts, o_tokens,
       o_trace, o_log, o_bt, o_nll, o_splitk, o_splitk_rs, o_tree, o_tree_out, o_scratch, o_stamp, ws_total;
@@ -189,6 +189,7 @@ Plan make_plan(const seed_config& c) {
     p.o_splitk = take(ksn * MAX_ROWS * 4);   // only passes of at most MAX_ROWS rows split K
     p.o_splitk_rs = take((size_t)MAX_ROWS * 4);
   }
+  p.o_wide_part = take((size_t)seedk::WIDE_SPLIT_MAX * p.max_rows * p.H * 4);   // split wide passes (N = H)
   p.o_topk = take((size_t)TOPK_PARTS * (2 * TOPK_MAX + 2) * 4);
   p.o_tdraft = take((size_t)TREE_MAX_STEPS * (TOPK_MAX + 2) * 4 + 16);
   p.o_dlog = take((size_t)p.V * 4);
@@ -415,6 +416,7 @@ void linear(seed_ctx* c, LinArgs a, int pro, int epi, int phase, int op, bool ca
   tile_policy(a.N, a.K, epi == EPI_HEAD, a.NT, a.KS, a.S, a.NJ);
   if (epi == EPI_HEAD) a.NT = head_nt(a.M);
   const int kind = linear_kind(a, epi == EPI_HEAD);
+  if (kind == LIN_WIDE) a.part = c->ws<float>(c->p.o_wide_part);
   timed(c, phase, op, cap, [&](const LaunchEvents* ev) { launch_linear<T>(a, pro, epi, kind, c->s, ev); });
 }
 
