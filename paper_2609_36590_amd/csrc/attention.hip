@@ -570,21 +570,109 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
     }
   };
 
-  KA ka[NC][DS], kb[NC][DS];
-  VA va[NC][DT], vb[NC][DT];
-  // tile 0's loads strictly before tile 1's, here as in the loop: if the scheduler issued them in
-  // the other order, the first use of tile 0 would have to wait for both tiles on every iteration
-  load_tile(ka, va, 0);
-  __builtin_amdgcn_sched_barrier(0);
-  load_tile(kb, vb, 1);
-  __builtin_amdgcn_sched_barrier(0);
-  for (int t = 0; t <= t_last; t += 2) {
-    consume(ka, va, t);
-    load_tile(ka, va, t + 2);
+  if constexpr (sizeof(T) == 2) {
+    // bf16 caches: each tile is fetched once per workgroup (one 16-byte key chunk and one value
+    // chunk per thread and cache) and staged in LDS, from which every wave reads its fragments,
+    // instead of each wave fetching the whole tile for itself (a quarter of the memory requests).
+    // RD register stages keep RD - 1 tiles in flight; tiles alternate between two LDS slots, one
+    // barrier per tile. Key chunk c of position row r sits at column c ^ kswz(r) of its row and
+    // value chunk c of dim row d at c ^ ((d >> 3) & 1), so the 16 rows a fragment read touches fall
+    // on distinct banks.
+    constexpr int CPR = HD / 8;            // 16-byte chunks per key row (one position)
+    constexpr int NKC = 16 * CPR;          // key chunks per tile and cache
+    constexpr int NCH = 2 * NKC;           // key and value chunks per tile and cache
+    constexpr int TB = NCH * 16;           // bytes per tile and cache
+    constexpr int CPT = NC * NCH / 256;    // chunks per thread and tile
+    static_assert(NC * NCH % 256 == 0, "whole chunks per thread");
+    constexpr int RD = 4;                  // register stages r0..r3 below
+    char* stage = reinterpret_cast<char*>(s_bt) + prefill_bt_bytes(a.bt_stride);
+    auto kswz = [](int r) { return (r * CPR / 16) % CPR; };
+    auto gload = [&](u32x4 (&rg)[CPT], int t) __attribute__((always_inline)) {
+      const int tc = min(t, t_last);
+#pragma unroll
+      for (int u = 0; u < CPT; ++u) {
+        const int q = u * 256 + (int)threadIdx.x, cc = q / NCH, qq = q - cc * NCH;
+        const T* base = cc == 0 ? kvp : reinterpret_cast<const T*>(a.skv);
+        const size_t blk = cc == 0 ? layer_base + s_bt[tc] : (size_t)a.s_layer * a.s_n_blocks + tc;
+        const int r = qq / CPR, kc = (qq % CPR) ^ kswz(r);
+        const int d = (qq - NKC) >> 1, vc = ((qq - NKC) & 1) ^ ((d >> 3) & 1);
+        const T* src = qq < NKC ? base + ((blk * 2 + 0) * a.n_kv + h) * 16 * HD + r * HD + kc * 8
+                                : base + ((blk * 2 + 1) * a.n_kv + h) * HD * 16 + d * 16 + vc * 8;
+        rg[u] = *reinterpret_cast<const u32x4*>(src);
+      }
+    };
+    auto lstore = [&](const u32x4 (&rg)[CPT], int slot) __attribute__((always_inline)) {
+#pragma unroll
+      for (int u = 0; u < CPT; ++u)   // chunk q = cc * NCH + qq at byte 16 q of the slot
+        *reinterpret_cast<u32x4*>(stage + (size_t)slot * NC * TB + (size_t)(u * 256 + threadIdx.x) * 16) = rg[u];
+    };
+    auto lfrag = [&](KA (&kf)[NC][DS], VA (&vf)[NC][DT], int slot) __attribute__((always_inline)) {
+      const char* sb = stage + (size_t)slot * NC * TB;
+#pragma unroll
+      for (int cc = 0; cc < NC; ++cc) {
+#pragma unroll
+        for (int ds = 0; ds < DS; ++ds)
+          kf[cc][ds].v = *reinterpret_cast<const uint4*>(sb + cc * TB + tl * (HD * 2) + ((ds * 4 + kg) ^ kswz(tl)) * 16);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+          const int d = dt * 16 + tl;
+          vf[cc][dt].v = *reinterpret_cast<const uint2*>(sb + cc * TB + NKC * 16 + d * 32 +
+                                                          (((kg >> 1) ^ ((d >> 3) & 1)) * 16) + (kg & 1) * 8);
+        }
+      }
+    };
+    // register stages, named so that every index is a constant (tile j lives in stage j mod RD)
+    u32x4 r0[CPT], r1[CPT], r2[CPT], r3[CPT];
+    gload(r0, 0);   // each tile's loads strictly after the previous tile's
     __builtin_amdgcn_sched_barrier(0);
-    consume(kb, vb, t + 1);   // past t_last: the last tile again, every position masked
-    load_tile(kb, vb, t + 3);
+    gload(r1, 1);
     __builtin_amdgcn_sched_barrier(0);
+    gload(r2, 2);
+    __builtin_amdgcn_sched_barrier(0);
+    gload(r3, 3);
+    __builtin_amdgcn_sched_barrier(0);
+    lstore(r0, 0);
+    gload(r0, RD);
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();
+    // tile tt from slot tt & 1 (past t_last: the last tile again, every position masked); then tile
+    // tt + 1, fetched RD - 1 tiles ago into stage `next`, into the other slot (whose previous tile
+    // every wave finished before the last barrier), and `next` refilled with tile tt + 1 + RD
+    auto step = [&](int tt, int slot, u32x4 (&next)[CPT]) __attribute__((always_inline)) {
+      KA kf[NC][DS];
+      VA vf[NC][DT];
+      lfrag(kf, vf, slot);
+      consume(kf, vf, tt);
+      __builtin_amdgcn_sched_barrier(0);
+      lstore(next, slot ^ 1);
+      gload(next, tt + 1 + RD);
+      __builtin_amdgcn_sched_barrier(0);
+      __syncthreads();
+    };
+    for (int t = 0; t <= t_last; t += RD) {
+      step(t, 0, r1);
+      step(t + 1, 1, r2);
+      step(t + 2, 0, r3);
+      step(t + 3, 1, r0);
+    }
+  } else {
+    KA ka[NC][DS], kb[NC][DS];
+    VA va[NC][DT], vb[NC][DT];
+    // tile 0's loads strictly before tile 1's, here as in the loop: if the scheduler issued them
+    // in the other order, the first use of tile 0 would have to wait for both tiles on every
+    // iteration
+    load_tile(ka, va, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    load_tile(kb, vb, 1);
+    __builtin_amdgcn_sched_barrier(0);
+    for (int t = 0; t <= t_last; t += 2) {
+      consume(ka, va, t);
+      load_tile(ka, va, t + 2);
+      __builtin_amdgcn_sched_barrier(0);
+      consume(kb, vb, t + 1);   // past t_last: the last tile again, every position masked
+      load_tile(kb, vb, t + 3);
+      __builtin_amdgcn_sched_barrier(0);
+    }
   }
 
   // lane (qv, kg) holds dims dt*16 + 4kg .. +3 of query vector qv
@@ -658,15 +746,24 @@ void launch_attention(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev) 
   else launch_attention_hd<T, 64>(a, s, ev);
 }
 
+// LDS of one prefill workgroup: the block table, then (bf16) two tile slots of both caches
+static size_t prefill_lds(const AttnArgs& a, bool bf16) {
+  const size_t tile = (size_t)2 * 16 * a.head_dim * 2 * (a.s_block > 0 ? 2 : 1);
+  return prefill_bt_bytes(a.bt_stride) + (bf16 ? 2 * tile : 0);
+}
+
 bool attention_prefill_supported(const AttnArgs& a) {
-  return a.B == 1 && a.G >= 1 && 64 % a.G == 0 && (a.head_dim == 128 || a.head_dim == 64) && !a.tree;
+  // the block table must fit LDS beside the tile slots (capacities up to ~131k positions); longer
+  // ones take the split-KV kernel
+  return a.B == 1 && a.G >= 1 && 64 % a.G == 0 && (a.head_dim == 128 || a.head_dim == 64) && !a.tree &&
+         prefill_lds(a, true) <= 65536;
 }
 
 template <typename T>
 void launch_attention_prefill(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev) {
   const int rows_wg = 64 / a.G;
   const dim3 grid((unsigned)(((a.R + rows_wg - 1) / rows_wg) * a.n_kv));
-  const size_t lds = (size_t)a.bt_stride * sizeof(int);
+  const size_t lds = prefill_lds(a, sizeof(T) == 2);
   if (a.s_block > 0) {
     if (a.head_dim == 128) launch_kernel(k_attention_prefill<T, 128, true>, grid, s, ev, a, lds);
     else launch_kernel(k_attention_prefill<T, 64, true>, grid, s, ev, a, lds);

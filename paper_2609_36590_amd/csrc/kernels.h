@@ -92,6 +92,9 @@ struct AttnArgs {
   float* out;             // [M][n_heads*head_dim]
 };
 
+// bytes of a prefill attention workgroup's staged block table (16-byte aligned)
+__host__ __device__ inline int prefill_bt_bytes(int bt_stride) { return (bt_stride * 4 + 15) / 16 * 16; }
+
 // Per-pass row setup + embedding gather.
 enum SetupMode { SETUP_PREFILL = 0, SETUP_DRAFT = 1, SETUP_VERIFY = 2, SETUP_SPEC = 3, SETUP_TREE = 4 };
 

@@ -2,9 +2,9 @@
 against the oracle's block-by-block loop.
 
 Tiny models (fp32: logits within 1e-4; bf16 weights and caches: 2e-2), block sizes from 1 to
-larger than the sequence; a 100-token sequence makes blocks straddle the 48-row passes of the GPU
-path (rows of one block computed in two passes read each other's keys/values from the pass's own
-cache). Per-row negative log-likelihoods within the logit tolerance (+ rounding of the
+larger than the sequence; a 100-token sequence runs as one wide pass of 99 rows with a ragged last
+token tile, and an 1100-token one makes blocks straddle the 1024-row passes of the GPU path (rows
+of one block computed in two passes read each other's keys/values from the pass's own cache). Per-row negative log-likelihoods within the logit tolerance (+ rounding of the
 log-sum-exp), L_spec within n times that. The decoder-only split (n_dec = l) must reproduce the
 full model's causal logits for every block size.
 """
@@ -50,8 +50,13 @@ def test_spec_forward_matches_oracle(cfg, tol):
     _run(cfg, 33, [1, 4, 16, 64], tol)
 
 
-def test_blocks_straddle_passes():
+def test_one_ragged_wide_pass():
     _run(synth.C1_TINY, 100, [5, 16, 30], 1e-4, seed=3)
+
+
+def test_blocks_straddle_passes():
+    # 1099 rows: passes of 1024 and 75; blocks of 5 and 30 cross row 1024, blocks of 16 end on it
+    _run(synth.C1_TINY, 1100, [5, 16, 30], 1e-4, seed=4)
 
 
 def test_two_tokens():
