@@ -492,6 +492,20 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
     for (int j = 0; j < 8; ++j) x[j] = qok ? x[j] * a.scale_log2 : 0.f;
     qf[ds] = ET<T>::split(x);
   }
+  // positions split over a.pf_split workgroups: this one streams tiles [t0, t_end) and, when the
+  // pass is split, writes an unnormalised partial that k_prefill_merge combines
+  const int n_split = a.pf_split, ks = blockIdx.y;
+  const int t0 = ks * (t_last + 1) / n_split, t_end = (ks + 1) * (t_last + 1) / n_split;
+  const size_t pidx = ((size_t)ks * a.R + r0 + rl) * a.n_heads + h * a.G + gq;   // (split, row, head)
+  if (t_end <= t0) {   // no tile here (every wave of the workgroup takes this branch): the merge's identity
+    if (qok) {
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+        *reinterpret_cast<float4*>(a.pf_o + pidx * HD + dt * 16 + 4 * kg) = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (kg == 0) *reinterpret_cast<float2*>(a.pf_ml + pidx * 2) = make_float2(NEG_INF, 0.f);
+    }
+    return;
+  }
   __syncthreads();   // the block table is in LDS
 
   const T* kvp = reinterpret_cast<const T*>(a.kv);
@@ -500,7 +514,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
   typedef typename PV<T>::A VA;
   // cache 0: the deep cache through the block table; cache 1 (SPEC): the pass's own, by position
   auto load_tile = [&](KA (&kf)[NC][DS], VA (&vf)[NC][DT], int t) {
-    const int tc = min(t, t_last);
+    const int tc = min(t, t_end - 1);
 #pragma unroll
     for (int cc = 0; cc < NC; ++cc) {
       const T* base = cc == 0 ? kvp : reinterpret_cast<const T*>(a.skv);
@@ -526,11 +540,12 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
       for (int ds = 0; ds < DS; ++ds) ET<T>::mma(sacc[cc], kf[cc][ds], qf[ds]);
     }
     float sv[4], mx = NEG_INF;
+    const bool tv = t < t_end;   // a tile past this workgroup's range is masked whole
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int pos = 16 * t + 4 * kg + i;
-      if constexpr (SPEC) sv[i] = pos > qpos ? NEG_INF : (pos < qstart ? sacc[0][i] : sacc[1][i]);
-      else sv[i] = pos <= qpos ? sacc[0][i] : NEG_INF;
+      if constexpr (SPEC) sv[i] = (!tv || pos > qpos) ? NEG_INF : (pos < qstart ? sacc[0][i] : sacc[1][i]);
+      else sv[i] = (tv && pos <= qpos) ? sacc[0][i] : NEG_INF;
       mx = fmaxf(mx, sv[i]);
     }
     mx = fmaxf(mx, __shfl_xor(mx, 16));
@@ -588,7 +603,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
     char* stage = reinterpret_cast<char*>(s_bt) + prefill_bt_bytes(a.bt_stride);
     auto kswz = [](int r) { return (r * CPR / 16) % CPR; };
     auto gload = [&](u32x4 (&rg)[CPT], int t) __attribute__((always_inline)) {
-      const int tc = min(t, t_last);
+      const int tc = min(t, t_end - 1);
 #pragma unroll
       for (int u = 0; u < CPT; ++u) {
         const int q = u * 256 + (int)threadIdx.x, cc = q / NCH, qq = q - cc * NCH;
@@ -623,19 +638,19 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
     };
     // register stages, named so that every index is a constant (tile j lives in stage j mod RD)
     u32x4 r0[CPT], r1[CPT], r2[CPT], r3[CPT];
-    gload(r0, 0);   // each tile's loads strictly after the previous tile's
+    gload(r0, t0);   // each tile's loads strictly after the previous tile's
     __builtin_amdgcn_sched_barrier(0);
-    gload(r1, 1);
+    gload(r1, t0 + 1);
     __builtin_amdgcn_sched_barrier(0);
-    gload(r2, 2);
+    gload(r2, t0 + 2);
     __builtin_amdgcn_sched_barrier(0);
-    gload(r3, 3);
+    gload(r3, t0 + 3);
     __builtin_amdgcn_sched_barrier(0);
     lstore(r0, 0);
-    gload(r0, RD);
+    gload(r0, t0 + RD);
     __builtin_amdgcn_sched_barrier(0);
     __syncthreads();
-    // tile tt from slot tt & 1 (past t_last: the last tile again, every position masked); then tile
+    // tile tt from slot (tt - t0) & 1 (past t_end: the last tile again, every position masked); then tile
     // tt + 1, fetched RD - 1 tiles ago into stage `next`, into the other slot (whose previous tile
     // every wave finished before the last barrier), and `next` refilled with tile tt + 1 + RD
     auto step = [&](int tt, int slot, u32x4 (&next)[CPT]) __attribute__((always_inline)) {
@@ -649,7 +664,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
       __builtin_amdgcn_sched_barrier(0);
       __syncthreads();
     };
-    for (int t = 0; t <= t_last; t += RD) {
+    for (int t = t0; t < t_end; t += RD) {
       step(t, 0, r1);
       step(t + 1, 1, r2);
       step(t + 2, 0, r3);
@@ -661,11 +676,11 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
     // tile 0's loads strictly before tile 1's, here as in the loop: if the scheduler issued them
     // in the other order, the first use of tile 0 would have to wait for both tiles on every
     // iteration
-    load_tile(ka, va, 0);
+    load_tile(ka, va, t0);
     __builtin_amdgcn_sched_barrier(0);
-    load_tile(kb, vb, 1);
+    load_tile(kb, vb, t0 + 1);
     __builtin_amdgcn_sched_barrier(0);
-    for (int t = 0; t <= t_last; t += 2) {
+    for (int t = t0; t < t_end; t += 2) {
       consume(ka, va, t);
       load_tile(ka, va, t + 2);
       __builtin_amdgcn_sched_barrier(0);
@@ -676,14 +691,41 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) k
   }
 
   // lane (qv, kg) holds dims dt*16 + 4kg .. +3 of query vector qv
-  if (qok) {
+  if (qok && n_split == 1) {
     float* op = a.out + (size_t)(r0 + rl) * qstride + (h * a.G + gq) * HD;
     const float inv = 1.f / l_c;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
       *reinterpret_cast<float4*>(op + dt * 16 + 4 * kg) =
           make_float4(o_c[dt][0] * inv, o_c[dt][1] * inv, o_c[dt][2] * inv, o_c[dt][3] * inv);
+  } else if (qok) {
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+      *reinterpret_cast<float4*>(a.pf_o + pidx * HD + dt * 16 + 4 * kg) =
+          make_float4(o_c[dt][0], o_c[dt][1], o_c[dt][2], o_c[dt][3]);
+    if (kg == 0) *reinterpret_cast<float2*>(a.pf_ml + pidx * 2) = make_float2(m_c, l_c);
   }
+}
+
+// The partials of a split one-launch pass merged in split order (the online-softmax merge),
+// normalised and written: one thread per (row, head, 4 dims).
+__global__ void __launch_bounds__(256) k_prefill_merge(AttnArgs a) {
+  const int hd4 = a.head_dim / 4;
+  const long long rh_n = (long long)a.R * a.n_heads;
+  const long long e = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= rh_n * hd4) return;
+  const long long rh = e / hd4;   // row * n_heads + head
+  const int d = (int)(e - rh * hd4) * 4;
+  float m = NEG_INF, l = 0.f, o[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int k = 0; k < a.pf_split; ++k) {
+    const size_t pi = (size_t)k * rh_n + rh;
+    const float2 ml = *reinterpret_cast<const float2*>(a.pf_ml + pi * 2);
+    const float4 v = *reinterpret_cast<const float4*>(a.pf_o + pi * a.head_dim + d);
+    const float ov[4] = {v.x, v.y, v.z, v.w};
+    softmax_merge(m, l, o, ml.x, ml.y, ov, 4);
+  }
+  const float inv = 1.f / l;
+  *reinterpret_cast<float4*>(a.out + rh * a.head_dim + d) = make_float4(o[0] * inv, o[1] * inv, o[2] * inv, o[3] * inv);
 }
 
 template <typename Kern>
@@ -762,14 +804,20 @@ bool attention_prefill_supported(const AttnArgs& a) {
 template <typename T>
 void launch_attention_prefill(const AttnArgs& a, hipStream_t s, const LaunchEvents* ev) {
   const int rows_wg = 64 / a.G;
-  const dim3 grid((unsigned)(((a.R + rows_wg - 1) / rows_wg) * a.n_kv));
+  const dim3 grid((unsigned)(((a.R + rows_wg - 1) / rows_wg) * a.n_kv), (unsigned)a.pf_split);
   const size_t lds = prefill_lds(a, sizeof(T) == 2);
+  const LaunchEvents e0{ev ? ev->start : nullptr, nullptr}, e1{nullptr, ev ? ev->stop : nullptr};
+  const LaunchEvents* ea = ev ? (a.pf_split > 1 ? &e0 : ev) : nullptr;
   if (a.s_block > 0) {
-    if (a.head_dim == 128) launch_kernel(k_attention_prefill<T, 128, true>, grid, s, ev, a, lds);
-    else launch_kernel(k_attention_prefill<T, 64, true>, grid, s, ev, a, lds);
+    if (a.head_dim == 128) launch_kernel(k_attention_prefill<T, 128, true>, grid, s, ea, a, lds);
+    else launch_kernel(k_attention_prefill<T, 64, true>, grid, s, ea, a, lds);
   } else {
-    if (a.head_dim == 128) launch_kernel(k_attention_prefill<T, 128, false>, grid, s, ev, a, lds);
-    else launch_kernel(k_attention_prefill<T, 64, false>, grid, s, ev, a, lds);
+    if (a.head_dim == 128) launch_kernel(k_attention_prefill<T, 128, false>, grid, s, ea, a, lds);
+    else launch_kernel(k_attention_prefill<T, 64, false>, grid, s, ea, a, lds);
+  }
+  if (a.pf_split > 1) {
+    const long long items = (long long)a.R * a.n_heads * (a.head_dim / 4);
+    launch_kernel(k_prefill_merge, dim3((unsigned)((items + 255) / 256)), s, ev ? &e1 : nullptr, a);
   }
 }
 

@@ -84,6 +84,12 @@ struct AttnArgs {
   const void* skv;
   int s_layer, s_n_blocks, s_block;
   int tree;               // 1: packed draft tree rows (mask by row_pos and row_slot)
+  // one-launch pass attention (launch_attention_prefill): positions split over pf_split workgroups
+  // per row-block, whose partials [pf_split][R][n_heads] (o: head_dim floats, then m and l) are
+  // merged by a second kernel when pf_split > 1
+  int pf_split;
+  float* pf_o;
+  float* pf_ml;
   int span;               // positions per workgroup group: 64, 128 or 256 (attention_span)
   int nq_alloc;           // set by the launcher: query vectors per row-block the LDS is sized for
   int n_groups_max;       // grid extent over groups; n_groups_max * span == bt_stride * 16
@@ -165,6 +171,7 @@ struct DevState {
 enum LinearKind { LIN_LDS = 0, LIN_GLOBAL = 1, LIN_SPLITK = 2, LIN_WIDE = 3 };
 constexpr int LDS_MAX_PASSES = 8;   // n-tile passes (NJ) of one k_linear_lds workgroup
 constexpr int HEAD_WIDE_NT = 16;    // n-tiles (waves) per workgroup of the LM head for 17..64 rows
+constexpr int PF_SPLIT_MAX = 4;    // position splits of the one-launch pass attention
 constexpr int WIDE_SPLIT_MAX = 4;   // k-ranges of a split wide pass (its partials: WIDE_SPLIT_MAX x rows x N floats)
 
 // Optional timing events stamped by the launches themselves (hipExtLaunchKernel): `start` at the

@@ -49,6 +49,8 @@ seed_status fail(seed_status s, const std::string& msg) {
   } while (0)
 
 constexpr int PREFILL_ROWS = 1024; // rows per prefill / drafting-objective pass (tiled MFMA GEMMs)
+constexpr int PF_SPLIT_LONG = 3;   // position splits of a pass's attention beyond its first PREFILL_ROWS
+static_assert(PF_SPLIT_LONG <= seedk::PF_SPLIT_MAX, "split partials fit the workspace");
 constexpr int MAX_ROWS = 64;       // rows per decode pass: max_batch * (max_draft + 1)
 constexpr int ATT_ROWS = 256;      // rows per attention launch of a wider single-sequence pass
 
@@ -66,7 +68,7 @@ struct Plan {
   std::vector<size_t> w_attn_norm, w_mlp_norm, w_qkv, w_o, w_gu, w_down;
   size_t kv_total;
   // workspace
-  size_t o_wide_part, o_h, o_xg, o_ssq, o_q, o_attn, o_act, o_part, o_row_seq, o_row_pos, o_row_slot, o_row_blk, o_row_rope, o_amax_val,
+  size_t o_pf_o, o_pf_ml, o_wide_part, o_h, o_xg, o_ssq, o_q, o_attn, o_act, o_part, o_row_seq, o_row_pos, o_row_slot, o_row_blk, o_row_rope, o_amax_val,
       o_amax_idx, o_vtok;
   size_t o_t, o_len, o_limit, o_active, o_nacc, o_bonus, o_rounds, o_counters, o_drafts, o_tokens,
       o_trace, o_log, o_bt, o_nll, o_splitk, o_splitk_rs, o_tree, o_tree_out, o_scratch, o_stamp, ws_total;
@@ -189,6 +191,8 @@ Plan make_plan(const seed_config& c) {
     p.o_splitk = take(ksn * MAX_ROWS * 4);   // only passes of at most MAX_ROWS rows split K
     p.o_splitk_rs = take((size_t)MAX_ROWS * 4);
   }
+  p.o_pf_o = take((size_t)seedk::PF_SPLIT_MAX * p.max_rows * p.QD * 4);   // split pass attention partials
+  p.o_pf_ml = take((size_t)seedk::PF_SPLIT_MAX * p.max_rows * p.NQ * 2 * 4);
   p.o_wide_part = take((size_t)seedk::WIDE_SPLIT_MAX * p.max_rows * p.H * 4);   // split wide passes (N = H)
   p.o_topk = take((size_t)TOPK_PARTS * (2 * TOPK_MAX + 2) * 4);
   p.o_tdraft = take((size_t)TREE_MAX_STEPS * (TOPK_MAX + 2) * 4 + 16);
@@ -431,7 +435,8 @@ struct SpecPass {
 // Layers [l0, l1) over M rows (B sequences x R rows each, consecutive positions per sequence).
 template <typename T>
 void run_layers(seed_ctx* c, int M, int B, int R, int l0, int l1, int phase,
-                const int* bt_override, bool cap, const SpecPass* spec = nullptr, bool tree = false) {
+                const int* bt_override, bool cap, const SpecPass* spec = nullptr, bool tree = false,
+                int pass_pos0 = 0) {
   const Plan& p = c->p;
   float* h = c->ws<float>(p.o_h);
   for (int li = l0; li < l1; ++li) {
@@ -472,6 +477,13 @@ void run_layers(seed_ctx* c, int M, int B, int R, int l0, int l1, int phase,
     at.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)p.HD));
     at.part = c->ws<float>(p.o_part);
     at.out = c->ws<float>(p.o_attn);
+    at.pf_o = c->ws<float>(p.o_pf_o);
+    at.pf_ml = c->ws<float>(p.o_pf_ml);
+    // a one-launch pass over a long cache splits each row-block's positions over PF_SPLIT_LONG
+    // workgroups (4B 16k prefill 651 / 634 / 607 / 610 ms with 1 / 2 / 3 / 4); a pass from position 0
+    // stays whole (its 1024-token prefill 23.9 / 24.0 / 24.2 / 24.4 ms: the merge costs more than the
+    // shorter chains save)
+    at.pf_split = pass_pos0 >= PREFILL_ROWS ? PF_SPLIT_LONG : 1;
     // the prompt's prefill (one sequence, more than 64 rows): one launch over all of the pass's
     // rows, written directly. Otherwise group partials and their merge; a pass wider than the
     // partial buffer (the drafting objective's) runs its rows ATT_ROWS at a time, every row
@@ -811,7 +823,7 @@ seed_status do_prefill(seed_ctx* c, const std::vector<int>& tokens_packed) {
       s.mode = SETUP_PREFILL; s.M = M; s.R = M; s.pf_seq = b; s.pf_pos0 = s0;
       timed(c, SEED_PHASE_PREFILL, SEED_OP_SETUP, false, [&](const LaunchEvents*) { launch_setup<T>(s, c->s); });
       run_layers<T>(c, M, 1, M, 0, p.L, SEED_PHASE_PREFILL,
-                    c->ws<int>(p.o_bt) + (size_t)b * p.bt_stride, false);
+                    c->ws<int>(p.o_bt) + (size_t)b * p.bt_stride, false, nullptr, false, s0);
     }
   }
   HIPCHK(hipGetLastError());
@@ -842,7 +854,7 @@ seed_status do_spec(seed_ctx* c, int n, int block, void* skv, int skv_blocks, fl
     SetupArgs s = setup_base(c, p.LD);
     s.mode = SETUP_SPEC; s.M = M; s.R = M; s.pf_seq = 0; s.pf_pos0 = s0;
     timed(c, SEED_PHASE_SPEC, SEED_OP_SETUP, false, [&](const LaunchEvents*) { launch_setup<T>(s, c->s); });
-    run_layers<T>(c, M, 1, M, p.LD, p.L, SEED_PHASE_SPEC, c->ws<int>(p.o_bt), false, &sp);
+    run_layers<T>(c, M, 1, M, p.LD, p.L, SEED_PHASE_SPEC, c->ws<int>(p.o_bt), false, &sp, false, s0);
     run_head<T>(c, M, c->ws<int>(p.o_vtok), 1, logits + (size_t)s0 * p.V, (long long)p.V, SEED_PHASE_SPEC, false);
   }
   HIPCHK(hipGetLastError());
