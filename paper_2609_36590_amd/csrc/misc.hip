@@ -230,28 +230,74 @@ __global__ void __launch_bounds__(256) k_kv_move(const int* depth, const int* ou
 
 // ---------------------------------------------------------------------------------------------
 // Negative log-likelihood of each row's target under the softmax of its logits (the per-position
-// term of L_spec, Algorithm 1): one workgroup per row; max, then the sum of exponentials, both
-// reduced with a fixed tree.
+// term of L_spec, Algorithm 1): one workgroup per row, one pass over the row. Each thread keeps a
+// running (max m, sum of exp(x - m)) over steps of 16 values (four 16-byte loads in flight); the
+// pairs are then merged across the wave and the workgroup, each merge rescaling both sums to the
+// larger maximum.
 // ---------------------------------------------------------------------------------------------
+__device__ __forceinline__ void lse_merge(float& m, float& s, float mo, float so) {
+  const float mn = fmaxf(m, mo);
+  if (mn == NEG_INF) return;   // both empty
+  s = (m == NEG_INF ? 0.f : s * __expf(m - mn)) + (mo == NEG_INF ? 0.f : so * __expf(mo - mn));
+  m = mn;
+}
+
 __global__ void __launch_bounds__(256) k_row_nll(const float* logits, int V, const int* target, float* nll) {
   const int r = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const float* z = logits + (size_t)r * V;
-  __shared__ float s_red[4];
-  float mx = NEG_INF;
-  for (int j = tid; j < V; j += blockDim.x) mx = fmaxf(mx, z[j]);
+  __shared__ float s_m[4], s_s[4];
+  float m = NEG_INF, s = 0.f;
+  auto step = [&](const float (&x)[16]) {
+    float cm = x[0];
 #pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
-  if (lane == 0) s_red[wave] = mx;
-  __syncthreads();
-  mx = fmaxf(fmaxf(s_red[0], s_red[1]), fmaxf(s_red[2], s_red[3]));
-  __syncthreads();
-  float sum = 0.f;
-  for (int j = tid; j < V; j += blockDim.x) sum += __expf(z[j] - mx);
+    for (int i = 1; i < 16; ++i) cm = fmaxf(cm, x[i]);
+    float acc = 0.f;
+    if (cm != NEG_INF) {
 #pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) sum += __shfl_xor(sum, o);
-  if (lane == 0) s_red[wave] = sum;
+      for (int i = 0; i < 16; ++i) acc += x[i] == NEG_INF ? 0.f : __expf(x[i] - cm);
+    }
+    lse_merge(m, s, cm, acc);
+  };
+  if ((V & 3) == 0) {   // rows start 16-byte aligned
+    const int V4 = V >> 2;
+    const float4* z4 = reinterpret_cast<const float4*>(z);
+    for (int j0 = 0; j0 < V4; j0 += 4 * 256) {
+      float x[16];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {   // unconditional (clamped) loads; slots past the row are masked
+        const int idx = j0 + u * 256 + tid;
+        const float4 v = z4[min(idx, V4 - 1)];
+        const bool ok = idx < V4;
+        x[4 * u + 0] = ok ? v.x : NEG_INF;
+        x[4 * u + 1] = ok ? v.y : NEG_INF;
+        x[4 * u + 2] = ok ? v.z : NEG_INF;
+        x[4 * u + 3] = ok ? v.w : NEG_INF;
+      }
+      step(x);
+    }
+  } else {
+    for (int j0 = 0; j0 < V; j0 += 16 * 256) {
+      float x[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int idx = j0 + u * 256 + tid;
+        x[u] = idx < V ? z[idx] : NEG_INF;
+      }
+      step(x);
+    }
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) lse_merge(m, s, __shfl_xor(m, o), __shfl_xor(s, o));
+  if (lane == 0) {
+    s_m[wave] = m;
+    s_s[wave] = s;
+  }
   __syncthreads();
-  if (tid == 0) nll[r] = mx + logf((s_red[0] + s_red[1]) + (s_red[2] + s_red[3])) - z[target[r]];
+  if (tid == 0) {
+    float mm = s_m[0], ss = s_s[0];
+    for (int w = 1; w < 4; ++w) lse_merge(mm, ss, s_m[w], s_s[w]);
+    nll[r] = mm + logf(ss) - z[target[r]];
+  }
 }
 
 // ---------------------------------------------------------------------------------------------
