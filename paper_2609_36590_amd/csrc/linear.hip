@@ -143,9 +143,9 @@ __device__ void linear_epilogue(const LinArgs& a, Grp gr, const float* Y, int y_
     }
     // argmax of each row over each pass's n-group (lowest token id among equal maxima): one wave
     // per (pass, row), lane-strided candidates, then a butterfly; the partial of n-group g goes to
-    // slot g and k_argmax_finalize reduces the slots
+    // slot g and k_argmax_finalize reduces the slots (none when the caller wants the logits only)
     const int lane = tid & 63, wave = tid >> 6, nw = nthr >> 6;
-    for (int q = wave; q < a.NJ * M; q += nw) {
+    for (int q = wave; a.amax_val && q < a.NJ * M; q += nw) {
       const int j = q / M, m = q - j * M;
       const int grp = gr.g0 + j * gr.gs;
       if (grp * a.NT >= n_tiles) continue;
@@ -1162,15 +1162,17 @@ static void launch(K kernel, dim3 grid, dim3 block, size_t lds, hipStream_t s, c
 // Workgroup width (n-tiles) of a wide pass: the candidate with the lowest rounds x width x
 // per-tile cost, one workgroup per CU (the kernel holds ~200-240 registers per lane). The per-tile
 // cost falls with width, since an activation fragment feeds WN/4 n-tiles (128-feature tiles were
-// measured about 1.35x slower per tile than 256-feature ones). The LM head keeps 16 (its argmax
-// partials are per 8 n-tiles); only the tile-local epilogues take 12 (QKV) or 20 (gate/up).
+// measured about 1.35x slower per tile than 256-feature ones). The LM head keeps 16 when it ranks
+// its logits (its argmax partials are per 8 n-tiles); only the tile-local epilogues take 12 (QKV)
+// or 20 (gate/up, the head writing logits only).
 template <int EPI>
-static int wide_width(int n_tiles, int MT) {
-  const int cands[] = {16, 8, EPI == EPI_SWIGLU ? 20 : 0, EPI == EPI_QKV ? 12 : 0};
+static int wide_width(int n_tiles, int MT, bool argmax) {
+  const bool local = EPI != EPI_HEAD || !argmax;   // every epilogue group tile-local
+  const int cands[] = {16, 8, (EPI == EPI_SWIGLU || (EPI == EPI_HEAD && local)) ? 20 : 0, EPI == EPI_QKV ? 12 : 0};
   int best = n_tiles >= 192 ? 16 : 8;
   long long best_cost = -1;
   for (int wn : cands) {
-    if (wn == 0 || (EPI == EPI_HEAD && wn != 16 && n_tiles >= 192)) continue;
+    if (wn == 0 || (!local && wn != 16 && n_tiles >= 192)) continue;
     const int per_tile = wn == 8 ? 135 : wn == 12 ? 112 : wn == 16 ? 100 : 95;
     const long long wgs = (long long)((n_tiles + wn - 1) / wn) * MT;
     const long long cost = (wgs + 255) / 256 * wn * per_tile;
@@ -1211,7 +1213,7 @@ static void launch_linear_pe(const LinArgs& a0, int kind, hipStream_t s, const L
   }
   if (kind == LIN_WIDE) {
     const int MT = (a.M + WIDE_ROWS_TILE - 1) / WIDE_ROWS_TILE;
-    const int wn = wide_width<EPI>(n_tiles, MT);
+    const int wn = wide_width<EPI>(n_tiles, MT, a.amax_val != nullptr);
     const int NG = (n_tiles + wn - 1) / wn;
     const dim3 grid((unsigned)((NG + 7) / 8 * 8 * MT)), block(512);
     if constexpr (PRO == PRO_PLAIN && EPI == EPI_RESID) {
@@ -1227,7 +1229,7 @@ static void launch_linear_pe(const LinArgs& a0, int kind, hipStream_t s, const L
       }
     }
     switch (wn) {
-      case 20: if constexpr (EPI == EPI_SWIGLU) launch(k_linear_wide<T, PRO, EPI, 20, false>, grid, block, WIDE_LDS, s, ev, a); break;
+      case 20: if constexpr (EPI == EPI_SWIGLU || EPI == EPI_HEAD) launch(k_linear_wide<T, PRO, EPI, 20, false>, grid, block, WIDE_LDS, s, ev, a); break;
       case 12: if constexpr (EPI == EPI_QKV) launch(k_linear_wide<T, PRO, EPI, 12, false>, grid, block, WIDE_LDS, s, ev, a); break;
       case 16: launch(k_linear_wide<T, PRO, EPI, 16, false>, grid, block, WIDE_LDS, s, ev, a); break;
       default: launch(k_linear_wide<T, PRO, EPI, 8, false>, grid, block, WIDE_LDS, s, ev, a); break;
@@ -1327,7 +1329,7 @@ static bool allow_big_lds(int bytes) {
                        reinterpret_cast<const void*>(&k_linear_wide<T, PRO, EPI, 8, false>)};
   bool ok = true;
   for (const void* f : fns) ok &= hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, bytes) == hipSuccess;
-  if constexpr (EPI == EPI_SWIGLU)
+  if constexpr (EPI == EPI_SWIGLU || EPI == EPI_HEAD)
     ok &= hipFuncSetAttribute(reinterpret_cast<const void*>(&k_linear_wide<T, PRO, EPI, 20, false>),
                               hipFuncAttributeMaxDynamicSharedMemorySize, bytes) == hipSuccess;
   if constexpr (EPI == EPI_QKV)

@@ -531,6 +531,7 @@ void run_head(seed_ctx* c, int M, int* tok_out, int tok_stride, float* logits, l
   a.W = c->W + p.w_embed; a.N = p.V; a.K = p.H;
   a.X = c->ws<float>(p.o_xg); a.ldx = p.H;
   a.logits = logits; a.ld_logits = ld;
+  if (!tok_out) a.amax_val = nullptr, a.amax_idx = nullptr;   // logits only: no argmax partials
   linear<T>(c, a, PRO_NORM, EPI_HEAD, phase, SEED_OP_HEAD, cap);
   const int parts = cdiv(p.V / 16, head_nt(M));   // one argmax partial per n-group
   if (!tok_out) return;   // the caller ranks the logits itself (dynamic drafting)
@@ -855,7 +856,7 @@ seed_status do_spec(seed_ctx* c, int n, int block, void* skv, int skv_blocks, fl
     s.mode = SETUP_SPEC; s.M = M; s.R = M; s.pf_seq = 0; s.pf_pos0 = s0;
     timed(c, SEED_PHASE_SPEC, SEED_OP_SETUP, false, [&](const LaunchEvents*) { launch_setup<T>(s, c->s); });
     run_layers<T>(c, M, 1, M, p.LD, p.L, SEED_PHASE_SPEC, c->ws<int>(p.o_bt), false, &sp, false, s0);
-    run_head<T>(c, M, c->ws<int>(p.o_vtok), 1, logits + (size_t)s0 * p.V, (long long)p.V, SEED_PHASE_SPEC, false);
+    run_head<T>(c, M, nullptr, 1, logits + (size_t)s0 * p.V, (long long)p.V, SEED_PHASE_SPEC, false);
   }
   HIPCHK(hipGetLastError());
   return SEED_OK;
