@@ -62,12 +62,12 @@ COPY_BYTES = 1 << 30
 COMMANDS = """```
 cd /tmp && export TMPDIR=/tmp && cd <repository root>
 for c in FETCH_SIZE WRITE_SIZE; do
-  timeout -s KILL 120 rocprofv3 --pmc $c -d gpurun_out/pmc_copy_$c -o run -- python3 bench.py --copy-calib
+  timeout -s KILL 120 rocprofv3 --pmc $c -d {d}/pmc_copy_$c -o run -- python3 bench.py --copy-calib
 done
 for c in FETCH_SIZE WRITE_SIZE; do
-  timeout -s KILL 300 rocprofv3 --pmc $c -d gpurun_out/pmc_bench_$c -o run -- python3 bench.py --profile-run --steps 20 --warmup 5
+  timeout -s KILL 300 rocprofv3 --pmc $c -d {d}/pmc_bench_$c -o run -- python3 bench.py --profile-run --steps 20 --warmup 5
 done
-python3 paper_2609_36590_amd/profile_summary.py --traffic gpurun_out {args}
+python3 paper_2609_36590_amd/profile_summary.py --traffic {d} {args}
 ```"""
 
 
@@ -94,7 +94,7 @@ def traffic(argv):
              f"{kernel}: {kf:.1f} KiB fetched x {rec['fetch_scale']} + {kw:.1f} KiB written x {rec['write_scale']}"
              f" = {tb / 1e6:.2f} MB per launch (mean over {nf} / {nw} dispatches).", "",
              "Commands (one MI355X, library built by `__graft_entry__.build()`):", "",
-             COMMANDS.format(args=f"{kernel} '{name_sub}' {grid} {lds} {out}"), ""]
+             COMMANDS.format(d=d, args=f"{kernel} '{name_sub}' {grid} {lds} {out}"), ""]
     for c in ("copy_FETCH_SIZE", "copy_WRITE_SIZE", "bench_FETCH_SIZE", "bench_WRITE_SIZE"):
         import io
         import contextlib
