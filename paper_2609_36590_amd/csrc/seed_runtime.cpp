@@ -191,8 +191,8 @@ Plan make_plan(const seed_config& c) {
     p.o_splitk = take(ksn * MAX_ROWS * 4);   // only passes of at most MAX_ROWS rows split K
     p.o_splitk_rs = take((size_t)MAX_ROWS * 4);
   }
-  p.o_pf_o = take((size_t)seedk::PF_SPLIT_MAX * p.max_rows * p.QD * 4);   // split pass attention partials
-  p.o_pf_ml = take((size_t)seedk::PF_SPLIT_MAX * p.max_rows * p.NQ * 2 * 4);
+  p.o_pf_o = take((size_t)PF_SPLIT_LONG * p.max_rows * p.QD * 4);   // split pass attention partials
+  p.o_pf_ml = take((size_t)PF_SPLIT_LONG * p.max_rows * p.NQ * 2 * 4);
   p.o_wide_part = take((size_t)seedk::WIDE_SPLIT_MAX * p.max_rows * p.H * 4);   // split wide passes (N = H)
   p.o_topk = take((size_t)TOPK_PARTS * (2 * TOPK_MAX + 2) * 4);
   p.o_tdraft = take((size_t)TREE_MAX_STEPS * (TOPK_MAX + 2) * 4 + 16);
